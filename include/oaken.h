@@ -1,0 +1,169 @@
+/*
+ * oaken.h -- C ABI of the MI355X (gfx950) Oaken KV-cache library.
+ *
+ * Oaken (Kim et al., ISCA 2025) quantizes each new key/value vector online
+ * against four thresholds profiled offline, splitting it into an outer, a middle
+ * and an inner group (Sec. 4.3, Eq. 1), shifting outer and middle values by the
+ * threshold on their side (Sec. 4.4, Eq. 4), and min-max quantizing each group
+ * with a scale computed from that vector alone (Eq. 2-3).  Middle values become
+ * 4-bit codes in a dense nibble matrix; inner and outer values are 5-bit codes
+ * whose low 4 bits reuse their dense slot and whose remaining information is one
+ * 8-bit COO entry (Sec. 4.5).  Decode attention streams the packed pages and
+ * dequantizes them on the fly (Sec. 5.2).
+ *
+ * Conventions for every entry point:
+ *   - Data pointers are DEVICE pointers unless stated otherwise; `stream` is a
+ *     hipStream_t passed as void* (NULL = default stream).  Work is enqueued
+ *     asynchronously on `stream`; the call returns before it completes.
+ *   - The caller allocates and owns every buffer (pool, tables, inputs, outputs,
+ *     workspace).  The library allocates no device memory and keeps no pointer
+ *     after it returns.  Calls on distinct streams are thread-safe.
+ *   - Scalars and host pointers are validated before anything is launched; a
+ *     failed check returns a non-zero oaken_status and launches nothing.
+ *     Device-resident values (lengths, block ids, positions, threshold order)
+ *     are preconditions: the library does not read them on the host, and
+ *     violating them is undefined behaviour.
+ *   - No C++ exception crosses this interface.
+ *
+ * Quantizer rule (bit-exact contract).  For a vector x[0..d) of fp16 values and
+ * fp32 thresholds lo_o <= lo_i <= hi_i <= hi_o, in IEEE fp32 with one rounding
+ * per operation (no fused multiply-add):
+ *   group  OUTER if x < lo_o or x > hi_o; else MIDDLE if x < lo_i or x > hi_i;
+ *          else INNER                                                  (Eq. 1)
+ *   side   OUTER: x > hi_o; MIDDLE: x > hi_i; INNER: x >= 0
+ *   a      OUTER: |x - (side ? hi_o : lo_o)|; MIDDLE: |x - (side ? hi_i : lo_i)|;
+ *          INNER: |x|                                                  (Eq. 4)
+ *   per group g with b = 3 (MIDDLE) or 4 (INNER, OUTER), L = 2^b - 1:
+ *          Min, Max over the group's a (0, 0 if the group is empty);
+ *          R = Max - Min; sigma = (R == 0) ? 0 : L / R                 (Eq. 2)
+ *          c = clamp(rint_half_even((a - Min) * sigma), 0, L)          (Eq. 3)
+ *          code u = side ? 2^b + c : 2^b - 1 - c   (side is the top code bit)
+ *          meta   = fp16_rne(Min), fp16_rne(R / L)
+ *   COO byte of an INNER/OUTER value at index j:
+ *          bit 7 = side, bit 6 = (group == OUTER), bits 5..0 = j mod 64.
+ *
+ * Page record (one per physical block, KV head, and K or V; P = block_size):
+ *   counts  offset 0                     uint8 [P][d/64] COO entries per (slot, chunk)
+ *   meta    offset align16(P*d/64)       fp16  [P][6]  (Min, R/L) of INNER, MIDDLE, OUTER
+ *   dense   offset align16(meta + 12P)   P*d/2 bytes of nibbles (low nibble first):
+ *             K record: token-major,   element j of slot t at byte t*(d/2) + j/2
+ *             V record: channel-major, element j of slot t at byte j*(P/2) + t/2
+ *           each nibble is the low 4 bits of the element's code
+ *   sparse  offset dense + P*d/2         COO bytes, slot-major, then 64-value chunk,
+ *           then ascending index; slot t starts at the sum of the counts of slots < t;
+ *           capacity P*d bytes (every value an outlier never overflows)
+ *   stride  align128(sparse + P*d)
+ * The record of (block b, KV head h, which w: 0 = K, 1 = V) starts at
+ * pool + ((b * n_kv_heads + h) * 2 + w) * record_stride.
+ * Tokens are appended in position order (Sec. 5.2, MMU); writing slot t of a page
+ * invalidates any later slot of that page.
+ */
+#ifndef OAKEN_H
+#define OAKEN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    OAKEN_OK = 0,
+    OAKEN_ERR_INVALID_ARG = 1,   /* null pointer, non-positive size, bad ratio, ... */
+    OAKEN_ERR_UNSUPPORTED = 2,   /* block_size != 16, head_dim not in {64, 128} */
+    OAKEN_ERR_WORKSPACE = 3,     /* workspace missing or smaller than required */
+    OAKEN_ERR_HIP = 4            /* the HIP runtime rejected a launch */
+} oaken_status;
+
+/* One layer's quantized KV cache: host struct describing device buffers. */
+typedef struct oaken_cache {
+    int32_t num_blocks;          /* physical pages in the pool */
+    int32_t block_size;          /* tokens per page P; must be 16 */
+    int32_t n_kv_heads;          /* KV heads H */
+    int32_t head_dim;            /* d: 64 or 128 */
+    int64_t record_stride;       /* must equal oaken_record_bytes(block_size, head_dim) */
+    void* pool;                  /* device, num_blocks * n_kv_heads * 2 * record_stride bytes */
+    const float* thresholds;     /* device fp32 [n_kv_heads][2 (K, V)][4] = lo_o, lo_i, hi_i, hi_o */
+} oaken_cache;
+
+/* Bytes of one page record (see layout above); -1 if (block_size, head_dim) is unsupported. */
+int64_t oaken_record_bytes(int32_t block_size, int32_t head_dim);
+
+/* Host array out[5] = byte offsets of counts, meta, dense, sparse, and the stride.
+   Returns OAKEN_OK or OAKEN_ERR_UNSUPPORTED / OAKEN_ERR_INVALID_ARG. */
+int oaken_record_layout(int32_t block_size, int32_t head_dim, int64_t* out);
+
+/* Workspace bytes needed by oaken_calibrate_thresholds. */
+size_t oaken_calibrate_workspace_bytes(int32_t n_runs, int32_t n_kv_heads);
+
+/* Workspace bytes needed by oaken_decode_attention for these sizes (0 when the
+   attention needs none).  The same arguments must be passed to the call. */
+size_t oaken_attention_workspace_bytes(int32_t n_seqs, int32_t n_q_heads, int32_t n_kv_heads,
+                                       int32_t head_dim, int32_t max_seq_len);
+
+/*
+ * Offline threshold profiling (Sec. 4.3 "offline outlier threshold profiling";
+ * ratios of Sec. 6.1).  k_calib, v_calib: fp16 [n_runs][tokens_per_run][n_kv_heads]
+ * [head_dim].  For each run, head and K|V, with n = tokens_per_run * head_dim values
+ *   k_o = rne(n * outer_ratio / 2), k_i = rne(n * inner_ratio)   (computed in fp64)
+ *   lo_o = k_o-th smallest value, hi_o = k_o-th largest value (0-based),
+ *   t = k_i-th smallest |value| (1-based; 0 if k_i == 0), lo_i = -t, hi_i = t;
+ * each threshold is then averaged over runs (fp64 sum in run order, divided by
+ * n_runs, rounded once to fp32), the inner pair is clamped into the outer interval
+ * (lo_i = min(max(lo_i, lo_o), hi_o), hi_i = max(min(hi_i, hi_o), lo_i)) and -0 becomes +0.
+ * Requires 0 <= outer_ratio < 1, 0 <= inner_ratio <= 1, their sum <= 1, 2*k_o <= n-1.
+ * Inputs must be finite.  thresholds_out: fp32 [n_kv_heads][2][4].
+ * workspace: oaken_calibrate_workspace_bytes(n_runs, n_kv_heads) bytes.
+ */
+int oaken_calibrate_thresholds(const void* k_calib, const void* v_calib, int32_t n_runs,
+                               int32_t tokens_per_run, int32_t n_kv_heads, int32_t head_dim,
+                               float outer_ratio, float inner_ratio, float* thresholds_out,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Online quantization of new key/value rows into the paged cache (Sec. 4.3 "online
+ * KV cache quantization", Sec. 4.4-4.5, Sec. 5.2 quantization engine and MMU).
+ * k_new, v_new: fp16 [n_tokens][n_kv_heads][head_dim].  Rows cu_tokens[s] ..
+ * cu_tokens[s+1]-1 belong to sequence s and land at positions start_pos[s] + i.
+ * block_table: int32 [n_seqs][max_blocks_per_seq] maps logical page pos/P to a
+ * physical block.  cu_tokens: int32 [n_seqs+1]; start_pos: int32 [n_seqs].
+ * max_new_per_seq bounds cu_tokens[s+1]-cu_tokens[s] (it sizes the launch).
+ * Preconditions: every block id < num_blocks; each sequence owns its pages; the
+ * positions written are the sequence's next positions.
+ */
+int oaken_quantize_kv(const oaken_cache* cache, const void* k_new, const void* v_new,
+                      const int32_t* block_table, int32_t max_blocks_per_seq,
+                      const int32_t* start_pos, const int32_t* cu_tokens, int32_t n_seqs,
+                      int32_t n_tokens, int32_t max_new_per_seq, void* stream);
+
+/*
+ * Batched decode attention over the quantized cache (Sec. 2.1; dequantization
+ * engine of Sec. 5.2).  For sequence s and query head h (KV head g = h / (H_q/H)):
+ *   out[s][h] = sum_t softmax_t(softmax_scale * q[s][h] . K^[s][g][t]) V^[s][g][t]
+ * over t < seq_lens[s], where K^, V^ are the dequantized cache entries:
+ *   value = Min + c * Delta, then INNER: +-value, MIDDLE: hi_i + value | lo_i - value,
+ *   OUTER: hi_o + value | lo_o - value (upper | lower side).
+ * q: fp16 [n_seqs][n_q_heads][head_dim]; out: fp32 [n_seqs][n_q_heads][head_dim].
+ * seq_lens: int32 [n_seqs], each in [1, max_seq_len]; block_table as above.
+ * Arithmetic is fp32; results match an fp64 evaluation within 2e-3 + 1e-2 |ref|.
+ * workspace: oaken_attention_workspace_bytes(n_seqs, n_q_heads, n_kv_heads,
+ * head_dim, max_seq_len) bytes (may be NULL when that is 0).
+ */
+int oaken_decode_attention(const oaken_cache* cache, const void* q, int32_t n_q_heads,
+                           const int32_t* block_table, int32_t max_blocks_per_seq,
+                           const int32_t* seq_lens, int32_t n_seqs, int32_t max_seq_len,
+                           float softmax_scale, float* out, void* workspace,
+                           size_t workspace_bytes, void* stream);
+
+/* Static description of a status code. */
+const char* oaken_status_string(int status);
+
+/* Detail of the last non-OK return on the calling thread ("" if none). */
+const char* oaken_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OAKEN_H */

@@ -1,0 +1,184 @@
+"""ctypes binding of liboaken.so (include/oaken.h) for torch tensors.
+
+Argument marshalling only: tensors are checked for device, dtype and contiguity and
+passed by data pointer together with torch's current HIP stream.  Every step of the
+computation runs in the library's HIP kernels; there is no fallback path, and a
+missing library raises at first use.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liboaken.so")
+PAGE = 16
+
+_lib = None
+
+
+class OakenError(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        super().__init__(f"oaken status {status}: {detail}")
+        self.status = status
+
+
+class _CacheStruct(ctypes.Structure):
+    _fields_ = [
+        ("num_blocks", ctypes.c_int32),
+        ("block_size", ctypes.c_int32),
+        ("n_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("record_stride", ctypes.c_int64),
+        ("pool", ctypes.c_void_p),
+        ("thresholds", ctypes.c_void_p),
+    ]
+
+
+def lib():
+    """Load liboaken.so; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                           "(hipcc --offload-arch=gfx950)")
+    L = ctypes.CDLL(LIB_PATH)
+    P, i32, i64, f32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_size_t
+    L.oaken_record_bytes.argtypes = [i32, i32]
+    L.oaken_record_bytes.restype = i64
+    L.oaken_record_layout.argtypes = [i32, i32, P]
+    L.oaken_record_layout.restype = ctypes.c_int
+    L.oaken_calibrate_workspace_bytes.argtypes = [i32, i32]
+    L.oaken_calibrate_workspace_bytes.restype = sz
+    L.oaken_attention_workspace_bytes.argtypes = [i32, i32, i32, i32, i32]
+    L.oaken_attention_workspace_bytes.restype = sz
+    L.oaken_calibrate_thresholds.argtypes = [P, P, i32, i32, i32, i32, f32, f32, P, P, sz, P]
+    L.oaken_calibrate_thresholds.restype = ctypes.c_int
+    L.oaken_quantize_kv.argtypes = [ctypes.POINTER(_CacheStruct), P, P, P, i32, P, P, i32, i32, i32, P]
+    L.oaken_quantize_kv.restype = ctypes.c_int
+    L.oaken_decode_attention.argtypes = [ctypes.POINTER(_CacheStruct), P, i32, P, i32, P, i32, i32,
+                                         f32, P, P, sz, P]
+    L.oaken_decode_attention.restype = ctypes.c_int
+    L.oaken_status_string.argtypes = [ctypes.c_int]
+    L.oaken_status_string.restype = ctypes.c_char_p
+    L.oaken_last_error.argtypes = []
+    L.oaken_last_error.restype = ctypes.c_char_p
+    _lib = L
+    return L
+
+
+def _check(status: int):
+    if status != 0:
+        raise OakenError(status, lib().oaken_last_error().decode())
+
+
+def _dev(t: torch.Tensor, dtype, name: str) -> int:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on the GPU")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+def _stream() -> int:
+    return torch.cuda.current_stream().cuda_stream
+
+
+def record_bytes(head_dim: int, block_size: int = PAGE) -> int:
+    return int(lib().oaken_record_bytes(block_size, head_dim))
+
+
+def record_layout(head_dim: int, block_size: int = PAGE) -> dict:
+    out = (ctypes.c_int64 * 5)()
+    _check(lib().oaken_record_layout(block_size, head_dim, out))
+    return dict(counts=out[0], meta=out[1], dense=out[2], sparse=out[3], stride=out[4])
+
+
+class Cache:
+    """One layer's quantized KV cache: a uint8 page pool plus fp32 thresholds [H][2][4]."""
+
+    def __init__(self, num_blocks: int, n_kv_heads: int, head_dim: int, thresholds: torch.Tensor,
+                 pool: torch.Tensor | None = None):
+        stride = record_bytes(head_dim)
+        if stride < 0:
+            raise OakenError(2, f"head_dim {head_dim} unsupported")
+        nbytes = num_blocks * n_kv_heads * 2 * stride
+        if pool is None:
+            pool = torch.zeros(nbytes, dtype=torch.uint8, device=thresholds.device)
+        if pool.numel() < nbytes:
+            raise ValueError("pool too small")
+        if tuple(thresholds.shape) != (n_kv_heads, 2, 4):
+            raise ValueError("thresholds must be [n_kv_heads][2][4]")
+        self.pool = pool
+        self.thresholds = thresholds.contiguous()
+        self.num_blocks, self.n_kv_heads, self.head_dim, self.stride = num_blocks, n_kv_heads, head_dim, stride
+        self._s = _CacheStruct(num_blocks, PAGE, n_kv_heads, head_dim, stride,
+                               _dev(self.pool, torch.uint8, "pool"),
+                               _dev(self.thresholds, torch.float32, "thresholds"))
+
+    @property
+    def struct(self):
+        return ctypes.byref(self._s)
+
+
+def calibrate_thresholds(k_calib: torch.Tensor, v_calib: torch.Tensor, outer_ratio: float = 0.04,
+                         inner_ratio: float = 0.06) -> torch.Tensor:
+    """fp16 [R][T][H][d] calibration sets -> fp32 thresholds [H][2][4] (device)."""
+    if k_calib.shape != v_calib.shape or k_calib.dim() != 4:
+        raise ValueError("calibration sets must both be [R][T][H][d]")
+    R, T, H, d = k_calib.shape
+    out = torch.empty(H, 2, 4, dtype=torch.float32, device=k_calib.device)
+    ws_bytes = int(lib().oaken_calibrate_workspace_bytes(R, H))
+    ws = torch.empty(max(ws_bytes, 4), dtype=torch.uint8, device=k_calib.device)
+    _check(lib().oaken_calibrate_thresholds(
+        _dev(k_calib, torch.float16, "k_calib"), _dev(v_calib, torch.float16, "v_calib"),
+        R, T, H, d, float(outer_ratio), float(inner_ratio), out.data_ptr(), ws.data_ptr(), ws_bytes,
+        _stream()))
+    return out
+
+
+def quantize_kv(cache: Cache, k_new: torch.Tensor, v_new: torch.Tensor, block_table: torch.Tensor,
+                start_pos: torch.Tensor, cu_tokens: torch.Tensor, max_new_per_seq: int):
+    """Quantize fp16 rows [n_tokens][H][d] into the cache at positions start_pos[s] + i."""
+    n_tokens = k_new.shape[0]
+    if tuple(k_new.shape) != (n_tokens, cache.n_kv_heads, cache.head_dim) or v_new.shape != k_new.shape:
+        raise ValueError("k_new/v_new must be [n_tokens][n_kv_heads][head_dim]")
+    n_seqs = start_pos.numel()
+    if cu_tokens.numel() != n_seqs + 1 or block_table.dim() != 2 or block_table.shape[0] != n_seqs:
+        raise ValueError("cu_tokens must have n_seqs+1 entries and block_table n_seqs rows")
+    _check(lib().oaken_quantize_kv(
+        cache.struct, _dev(k_new, torch.float16, "k_new"), _dev(v_new, torch.float16, "v_new"),
+        _dev(block_table, torch.int32, "block_table"), block_table.shape[1],
+        _dev(start_pos, torch.int32, "start_pos"), _dev(cu_tokens, torch.int32, "cu_tokens"),
+        n_seqs, n_tokens, int(max_new_per_seq), _stream()))
+
+
+def attention_workspace_bytes(n_seqs, n_q_heads, n_kv_heads, head_dim, max_seq_len) -> int:
+    return int(lib().oaken_attention_workspace_bytes(n_seqs, n_q_heads, n_kv_heads, head_dim, max_seq_len))
+
+
+def decode_attention(cache: Cache, q: torch.Tensor, block_table: torch.Tensor, seq_lens: torch.Tensor,
+                     max_seq_len: int, scale: float, out: torch.Tensor | None = None,
+                     workspace: torch.Tensor | None = None) -> torch.Tensor:
+    """fp16 q [n_seqs][Hq][d] -> fp32 out [n_seqs][Hq][d]."""
+    n_seqs, Hq, d = q.shape
+    if d != cache.head_dim or seq_lens.numel() != n_seqs or block_table.shape[0] != n_seqs:
+        raise ValueError("q / seq_lens / block_table shapes disagree")
+    if out is None:
+        out = torch.empty(n_seqs, Hq, d, dtype=torch.float32, device=q.device)
+    ws_bytes = attention_workspace_bytes(n_seqs, Hq, cache.n_kv_heads, d, max_seq_len)
+    if ws_bytes and (workspace is None or workspace.numel() < ws_bytes):
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
+    ws_ptr = workspace.data_ptr() if (ws_bytes and workspace is not None) else None
+    _check(lib().oaken_decode_attention(
+        cache.struct, _dev(q, torch.float16, "q"), Hq, _dev(block_table, torch.int32, "block_table"),
+        block_table.shape[1], _dev(seq_lens, torch.int32, "seq_lens"), n_seqs, int(max_seq_len),
+        float(scale), _dev(out, torch.float32, "out"), ws_ptr, ws_bytes, _stream()))
+    return out

@@ -1,0 +1,215 @@
+// Host side of the C ABI declared in include/oaken.h: argument validation, launch
+// planning and error reporting.  Nothing here touches device memory contents.
+#include "../../include/oaken.h"
+#include "oaken_internal.h"
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int status, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int status, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof(g_err), fmt, ap);
+    va_end(ap);
+    return status;
+}
+
+int ok() {
+    g_err[0] = '\0';
+    return OAKEN_OK;
+}
+
+bool supported_dim(int32_t d) { return d == 64 || d == 128; }
+
+int check_cache(const oaken_cache* c) {
+    if (!c) return fail(OAKEN_ERR_INVALID_ARG, "cache is NULL");
+    if (c->block_size != oaken::kPage)
+        return fail(OAKEN_ERR_UNSUPPORTED, "block_size %d unsupported (only 16)", c->block_size);
+    if (!supported_dim(c->head_dim))
+        return fail(OAKEN_ERR_UNSUPPORTED, "head_dim %d unsupported (64 or 128)", c->head_dim);
+    if (c->num_blocks <= 0 || c->n_kv_heads <= 0)
+        return fail(OAKEN_ERR_INVALID_ARG, "num_blocks and n_kv_heads must be positive");
+    const int64_t want = oaken::make_layout(c->block_size, c->head_dim).stride;
+    if (c->record_stride != want)
+        return fail(OAKEN_ERR_INVALID_ARG, "record_stride %lld != %lld", (long long)c->record_stride,
+                    (long long)want);
+    if (!c->pool || !c->thresholds) return fail(OAKEN_ERR_INVALID_ARG, "pool or thresholds is NULL");
+    return OAKEN_OK;
+}
+
+int hip_status(hipError_t e, const char* what) {
+    if (e == hipSuccess) return ok();
+    return fail(OAKEN_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+}  // namespace
+
+extern "C" {
+
+int64_t oaken_record_bytes(int32_t block_size, int32_t head_dim) {
+    if (block_size != oaken::kPage || !supported_dim(head_dim)) return -1;
+    return oaken::make_layout(block_size, head_dim).stride;
+}
+
+int oaken_record_layout(int32_t block_size, int32_t head_dim, int64_t* out) {
+    if (!out) return fail(OAKEN_ERR_INVALID_ARG, "out is NULL");
+    if (block_size != oaken::kPage || !supported_dim(head_dim))
+        return fail(OAKEN_ERR_UNSUPPORTED, "unsupported block_size %d / head_dim %d", block_size,
+                    head_dim);
+    const oaken::Layout L = oaken::make_layout(block_size, head_dim);
+    out[0] = L.counts;
+    out[1] = L.meta;
+    out[2] = L.dense;
+    out[3] = L.sparse;
+    out[4] = L.stride;
+    return ok();
+}
+
+size_t oaken_calibrate_workspace_bytes(int32_t n_runs, int32_t n_kv_heads) {
+    if (n_runs <= 0 || n_kv_heads <= 0) return 0;
+    return (size_t)n_runs * n_kv_heads * 2 * 3 * sizeof(float);
+}
+
+size_t oaken_attention_workspace_bytes(int32_t n_seqs, int32_t n_q_heads, int32_t n_kv_heads,
+                                       int32_t head_dim, int32_t max_seq_len) {
+    if (n_seqs <= 0 || n_q_heads <= 0 || n_kv_heads <= 0 || n_q_heads % n_kv_heads != 0 ||
+        !supported_dim(head_dim) || max_seq_len <= 0)
+        return 0;
+    const oaken::SplitPlan sp = oaken::plan_splits(n_seqs, n_q_heads, n_kv_heads, head_dim, max_seq_len);
+    if (sp.n_splits <= 1) return 0;
+    return (size_t)n_seqs * n_q_heads * sp.n_splits * (head_dim + 2) * sizeof(float);
+}
+
+int oaken_calibrate_thresholds(const void* k_calib, const void* v_calib, int32_t n_runs,
+                               int32_t tokens_per_run, int32_t n_kv_heads, int32_t head_dim,
+                               float outer_ratio, float inner_ratio, float* thresholds_out,
+                               void* workspace, size_t workspace_bytes, void* stream) {
+    if (!k_calib || !v_calib || !thresholds_out)
+        return fail(OAKEN_ERR_INVALID_ARG, "calibration inputs or output NULL");
+    if (n_runs <= 0 || tokens_per_run <= 0 || n_kv_heads <= 0 || head_dim <= 0)
+        return fail(OAKEN_ERR_INVALID_ARG, "sizes must be positive");
+    if (!(outer_ratio >= 0.0f && outer_ratio < 1.0f && inner_ratio >= 0.0f && inner_ratio <= 1.0f &&
+          outer_ratio + inner_ratio <= 1.0f))
+        return fail(OAKEN_ERR_INVALID_ARG, "ratios (%g, %g) outside [0,1) x [0,1] or sum > 1",
+                    (double)outer_ratio, (double)inner_ratio);
+    const int64_t n = (int64_t)tokens_per_run * head_dim;
+    const int64_t k_o = (int64_t)std::nearbyint((double)n * (double)outer_ratio / 2.0);
+    const int64_t k_i = (int64_t)std::nearbyint((double)n * (double)inner_ratio);
+    if (2 * k_o > n - 1 || k_i > n)
+        return fail(OAKEN_ERR_INVALID_ARG, "outer ratio leaves no middle values (k_o=%lld, n=%lld)",
+                    (long long)k_o, (long long)n);
+    const size_t need = oaken_calibrate_workspace_bytes(n_runs, n_kv_heads);
+    if (!workspace || workspace_bytes < need)
+        return fail(OAKEN_ERR_WORKSPACE, "calibration workspace %zu < %zu bytes", workspace_bytes, need);
+    oaken::CalibArgs a{};
+    a.k = static_cast<const uint16_t*>(k_calib);
+    a.v = static_cast<const uint16_t*>(v_calib);
+    a.per_run = static_cast<float*>(workspace);
+    a.thr_out = thresholds_out;
+    a.n = n;
+    a.k_o = k_o;
+    a.k_i = k_i;
+    a.R = n_runs;
+    a.T = tokens_per_run;
+    a.H = n_kv_heads;
+    a.d = head_dim;
+    return hip_status(oaken::launch_calibrate(a, static_cast<hipStream_t>(stream)), "calibrate launch");
+}
+
+int oaken_quantize_kv(const oaken_cache* cache, const void* k_new, const void* v_new,
+                      const int32_t* block_table, int32_t max_blocks_per_seq,
+                      const int32_t* start_pos, const int32_t* cu_tokens, int32_t n_seqs,
+                      int32_t n_tokens, int32_t max_new_per_seq, void* stream) {
+    int st = check_cache(cache);
+    if (st != OAKEN_OK) return st;
+    if (!k_new || !v_new || !block_table || !start_pos || !cu_tokens)
+        return fail(OAKEN_ERR_INVALID_ARG, "a device array argument is NULL");
+    if (n_seqs <= 0 || n_tokens < 0 || max_blocks_per_seq <= 0 || max_new_per_seq < 0)
+        return fail(OAKEN_ERR_INVALID_ARG, "n_seqs/max_blocks must be positive, counts non-negative");
+    if (n_tokens == 0 || max_new_per_seq == 0) return ok();
+    oaken::QuantArgs a{};
+    a.pool = static_cast<uint8_t*>(cache->pool);
+    a.thr = cache->thresholds;
+    a.k_new = static_cast<const uint16_t*>(k_new);
+    a.v_new = static_cast<const uint16_t*>(v_new);
+    a.block_table = block_table;
+    a.start_pos = start_pos;
+    a.cu_tokens = cu_tokens;
+    a.stride = cache->record_stride;
+    a.num_blocks = cache->num_blocks;
+    a.H = cache->n_kv_heads;
+    a.max_blocks = max_blocks_per_seq;
+    a.n_seqs = n_seqs;
+    return hip_status(oaken::launch_quantize(a, cache->head_dim, max_new_per_seq,
+                                             static_cast<hipStream_t>(stream)),
+                      "quantize launch");
+}
+
+int oaken_decode_attention(const oaken_cache* cache, const void* q, int32_t n_q_heads,
+                           const int32_t* block_table, int32_t max_blocks_per_seq,
+                           const int32_t* seq_lens, int32_t n_seqs, int32_t max_seq_len,
+                           float softmax_scale, float* out, void* workspace,
+                           size_t workspace_bytes, void* stream) {
+    int st = check_cache(cache);
+    if (st != OAKEN_OK) return st;
+    if (!q || !block_table || !seq_lens || !out)
+        return fail(OAKEN_ERR_INVALID_ARG, "a device array argument is NULL");
+    if (n_seqs <= 0 || max_seq_len <= 0 || max_blocks_per_seq <= 0 || n_q_heads <= 0)
+        return fail(OAKEN_ERR_INVALID_ARG, "sizes must be positive");
+    if (n_q_heads % cache->n_kv_heads != 0)
+        return fail(OAKEN_ERR_INVALID_ARG, "n_q_heads %d not a multiple of n_kv_heads %d", n_q_heads,
+                    cache->n_kv_heads);
+    if (n_q_heads / cache->n_kv_heads > 8)
+        return fail(OAKEN_ERR_UNSUPPORTED, "more than 8 query heads per KV head");
+    if ((int64_t)max_blocks_per_seq * oaken::kPage < max_seq_len)
+        return fail(OAKEN_ERR_INVALID_ARG, "block table too narrow for max_seq_len");
+    if (!std::isfinite(softmax_scale)) return fail(OAKEN_ERR_INVALID_ARG, "softmax_scale not finite");
+    const size_t need = oaken_attention_workspace_bytes(n_seqs, n_q_heads, cache->n_kv_heads,
+                                                        cache->head_dim, max_seq_len);
+    if (need > 0 && (!workspace || workspace_bytes < need))
+        return fail(OAKEN_ERR_WORKSPACE, "attention workspace %zu < %zu bytes", workspace_bytes, need);
+    const oaken::SplitPlan sp = oaken::plan_splits(n_seqs, n_q_heads, cache->n_kv_heads,
+                                                   cache->head_dim, max_seq_len);
+    oaken::AttnArgs a{};
+    a.pool = static_cast<const uint8_t*>(cache->pool);
+    a.thr = cache->thresholds;
+    a.q = static_cast<const uint16_t*>(q);
+    a.block_table = block_table;
+    a.seq_lens = seq_lens;
+    a.out = out;
+    a.partial = static_cast<float*>(workspace);
+    a.stride = cache->record_stride;
+    a.num_blocks = cache->num_blocks;
+    a.H = cache->n_kv_heads;
+    a.Hq = n_q_heads;
+    a.max_blocks = max_blocks_per_seq;
+    a.n_seqs = n_seqs;
+    a.max_seq_len = max_seq_len;
+    a.pages_per_split = sp.pages_per_split;
+    a.n_splits = sp.n_splits;
+    a.scale = softmax_scale;
+    return hip_status(oaken::launch_attention(a, cache->head_dim, static_cast<hipStream_t>(stream)),
+                      "attention launch");
+}
+
+const char* oaken_status_string(int status) {
+    switch (status) {
+        case OAKEN_OK: return "ok";
+        case OAKEN_ERR_INVALID_ARG: return "invalid argument";
+        case OAKEN_ERR_UNSUPPORTED: return "unsupported configuration";
+        case OAKEN_ERR_WORKSPACE: return "workspace missing or too small";
+        case OAKEN_ERR_HIP: return "HIP runtime error";
+        default: return "unknown status";
+    }
+}
+
+const char* oaken_last_error(void) { return g_err; }
+
+}  // extern "C"

@@ -1,0 +1,74 @@
+// Private declarations shared by the translation units of liboaken.so.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace oaken {
+
+constexpr int kPage = 16;  // tokens per page (block_size)
+
+// Byte offsets of the fields of one page record (layout in include/oaken.h).
+struct Layout {
+    int64_t counts, meta, dense, sparse, stride;
+};
+
+__host__ __device__ constexpr int64_t round_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
+
+__host__ __device__ constexpr Layout make_layout(int P, int d) {
+    Layout L{};
+    L.counts = 0;
+    L.meta = round_up((int64_t)P * (d / 64), 16);
+    L.dense = round_up(L.meta + (int64_t)P * 12, 16);
+    L.sparse = L.dense + (int64_t)P * d / 2;
+    L.stride = round_up(L.sparse + (int64_t)P * d, 128);
+    return L;
+}
+
+struct QuantArgs {
+    uint8_t* pool;
+    const float* thr;             // [H][2][4]
+    const uint16_t* k_new;        // fp16 bits [n_tokens][H][d]
+    const uint16_t* v_new;
+    const int32_t* block_table;   // [n_seqs][max_blocks]
+    const int32_t* start_pos;     // [n_seqs]
+    const int32_t* cu_tokens;     // [n_seqs + 1]
+    int64_t stride;
+    int32_t num_blocks, H, max_blocks, n_seqs;
+};
+
+struct CalibArgs {
+    const uint16_t* k;            // fp16 bits [R][T][H][d]
+    const uint16_t* v;
+    float* per_run;               // [R][H][2][3] = lo_o, hi_o, t
+    float* thr_out;               // [H][2][4]
+    int64_t n, k_o, k_i;          // values per run and order-statistic ranks
+    int32_t R, T, H, d;
+};
+
+struct AttnArgs {
+    const uint8_t* pool;
+    const float* thr;             // [H][2][4]
+    const uint16_t* q;            // fp16 bits [n_seqs][Hq][d]
+    const int32_t* block_table;   // [n_seqs][max_blocks]
+    const int32_t* seq_lens;      // [n_seqs]
+    float* out;                   // fp32 [n_seqs][Hq][d]
+    float* partial;               // [n_seqs][Hq][n_splits][d + 2] when n_splits > 1
+    int64_t stride;
+    int32_t num_blocks, H, Hq, max_blocks, n_seqs, max_seq_len;
+    int32_t pages_per_split, n_splits;
+    float scale;
+};
+
+// Split-K plan used by both the workspace query and the launch.
+struct SplitPlan {
+    int32_t pages_per_split, n_splits;
+};
+SplitPlan plan_splits(int32_t n_seqs, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                      int32_t max_seq_len);
+
+hipError_t launch_quantize(const QuantArgs& a, int d, int max_new_per_seq, hipStream_t st);
+hipError_t launch_calibrate(const CalibArgs& a, hipStream_t st);
+hipError_t launch_attention(const AttnArgs& a, int d, hipStream_t st);
+
+}  // namespace oaken

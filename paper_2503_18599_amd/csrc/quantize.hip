@@ -1,0 +1,215 @@
+// Online KV quantization into the paged cache (Oaken Sec. 4.3-4.5, Sec. 5.2
+// quantization engine).
+//
+// One workgroup covers the new tokens of one sequence that fall into one page, for
+// one KV head and one of K/V; each wave64 quantizes one token's vector.  Lane l owns
+// elements j = 64*c + l, so a wave's ballot over chunk c is exactly that chunk's
+// outlier mask: its popcount is the chunk count and mbcnt gives each outlier's slot
+// in the COO stream (the zero-remove step of the engine) without any branch.
+// Group selection is done with compares and selects, so waves never diverge on the
+// value distribution.
+#include "oaken_internal.h"
+
+#include <hip/hip_fp16.h>
+
+// The quantizer's codes are a bit-exact contract: one IEEE rounding per operation.
+#pragma clang fp contract(off)
+
+namespace oaken {
+namespace {
+
+__device__ inline float half_bits_to_float(uint16_t b) {
+    return __half2float(__ushort_as_half(b));
+}
+
+__device__ inline uint16_t float_to_half_bits(float f) {
+    return __half_as_ushort(__float2half_rn(f));
+}
+
+__device__ inline float wave_min(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fminf(v, __shfl_xor(v, o, 64));
+    return v;
+}
+
+__device__ inline float wave_max(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+    return v;
+}
+
+template <int D>
+__global__ __launch_bounds__(1024) void quantize_kernel(QuantArgs a) {
+    constexpr int NC = D / 64;           // 64-value chunks per vector
+    constexpr Layout LY = make_layout(kPage, D);
+
+    __shared__ uint8_t s_counts[kPage][NC];
+    __shared__ uint8_t s_vnib[kPage][D];
+
+    const int s = blockIdx.y;
+    const int h = blockIdx.z >> 1;
+    const int which = blockIdx.z & 1;
+    const int wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+
+    const int row0 = a.cu_tokens[s];
+    const int n_new = a.cu_tokens[s + 1] - row0;
+    const int pos0 = a.start_pos[s];
+    const int page = pos0 / kPage + (int)blockIdx.x;
+    const int t_lo = max(pos0, page * kPage);
+    const int t_hi = min(pos0 + n_new, (page + 1) * kPage);
+    if (n_new <= 0 || t_lo >= t_hi || page >= a.max_blocks) return;   // uniform per block
+    const int blk = a.block_table[(int64_t)s * a.max_blocks + page];
+    if (blk < 0 || blk >= a.num_blocks) return;
+
+    const int slot0 = t_lo - page * kPage;
+    const int nslots = t_hi - t_lo;
+    uint8_t* rec = a.pool + (((int64_t)blk * a.H + h) * 2 + which) * a.stride;
+    const bool active = wave < nslots;
+    const int slot = slot0 + wave;
+
+    // ---- quantize this wave's vector (Eq. 1-4) -------------------------------------
+    const float* th = a.thr + (h * 2 + which) * 4;
+    const float lo_o = th[0], lo_i = th[1], hi_i = th[2], hi_o = th[3];
+
+    float av[NC];
+    int grp[NC];
+    bool side[NC];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) { av[c] = 0.0f; grp[c] = 1; side[c] = false; }
+    float mn[3] = {INFINITY, INFINITY, INFINITY};
+    float mx[3] = {-INFINITY, -INFINITY, -INFINITY};
+    if (active) {
+        const int row = row0 + (page * kPage + slot - pos0);
+        const uint16_t* x = (which ? a.v_new : a.k_new) + ((int64_t)row * a.H + h) * D;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            const float xf = half_bits_to_float(x[c * 64 + lane]);
+            const bool outer = (xf < lo_o) || (xf > hi_o);
+            const bool middle = !outer && ((xf < lo_i) || (xf > hi_i));
+            const int g = outer ? 2 : (middle ? 1 : 0);
+            const bool sd = outer ? (xf > hi_o) : (middle ? (xf > hi_i) : (xf >= 0.0f));
+            const float shift = outer ? (sd ? hi_o : lo_o) : (middle ? (sd ? hi_i : lo_i) : 0.0f);
+            const float mag = (g == 0) ? fabsf(xf) : fabsf(xf - shift);
+            av[c] = mag;
+            grp[c] = g;
+            side[c] = sd;
+#pragma unroll
+            for (int k = 0; k < 3; ++k) {
+                mn[k] = (g == k) ? fminf(mn[k], mag) : mn[k];
+                mx[k] = (g == k) ? fmaxf(mx[k], mag) : mx[k];
+            }
+        }
+    }
+    float gmin[3], grange[3], gsig[3];
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+        float lo = wave_min(mn[k]);
+        float hi = wave_max(mx[k]);
+        if (!(hi >= lo)) { lo = 0.0f; hi = 0.0f; }   // empty group
+        const float levels = (k == 1) ? 7.0f : 15.0f;
+        gmin[k] = lo;
+        grange[k] = hi - lo;
+        gsig[k] = (grange[k] == 0.0f) ? 0.0f : levels / grange[k];
+    }
+
+    uint8_t nib[NC];
+    uint8_t coo[NC];
+    uint64_t omask[NC];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+        const int g = grp[c];
+        const int lv = (g == 1) ? 7 : 15;
+        const float gm = (g == 0) ? gmin[0] : ((g == 1) ? gmin[1] : gmin[2]);
+        const float gs = (g == 0) ? gsig[0] : ((g == 1) ? gsig[1] : gsig[2]);
+        const float sh = av[c] - gm;
+        const float sc = sh * gs;
+        int code = (int)rintf(sc);
+        code = min(max(code, 0), lv);
+        const int u = side[c] ? (lv + 1) + code : lv - code;
+        nib[c] = (uint8_t)(u & 15);
+        coo[c] = (uint8_t)(((u >> 4) << 7) | ((g == 2) << 6) | lane);
+        omask[c] = __ballot(active && g != 1);
+    }
+    if (active && lane == 0) {
+#pragma unroll
+        for (int c = 0; c < NC; ++c) s_counts[slot][c] = (uint8_t)__popcll(omask[c]);
+    }
+    __syncthreads();
+
+    if (active) {
+        // sparse start of this slot: counts of earlier slots (older ones live in the record)
+        int base = 0;
+        for (int t = 0; t < slot; ++t)
+            for (int c = 0; c < NC; ++c)
+                base += (t < slot0) ? rec[LY.counts + t * NC + c] : s_counts[t][c];
+        const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+        int off = base;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            if ((omask[c] >> lane) & 1ull)
+                rec[LY.sparse + off + __popcll(omask[c] & below)] = coo[c];
+            off += __popcll(omask[c]);
+        }
+        if (lane < NC) rec[LY.counts + slot * NC + lane] = s_counts[slot][lane];
+        if (lane < 6) {
+            const int k = lane >> 1;
+            const float lv = (k == 1) ? 7.0f : 15.0f;
+            const float gm = (k == 0) ? gmin[0] : ((k == 1) ? gmin[1] : gmin[2]);
+            const float gr = (k == 0) ? grange[0] : ((k == 1) ? grange[1] : grange[2]);
+            const uint16_t hb = (lane & 1) ? float_to_half_bits(gr / lv) : float_to_half_bits(gm);
+            *reinterpret_cast<uint16_t*>(rec + LY.meta + slot * 12 + lane * 2) = hb;
+        }
+        if (which == 0) {
+            // K: token-major, element j at byte slot*D/2 + j/2, low nibble = even j
+#pragma unroll
+            for (int c = 0; c < NC; ++c) {
+                const int hi_n = __shfl_down((int)nib[c], 1, 64);
+                if ((lane & 1) == 0)
+                    rec[LY.dense + slot * (D / 2) + (c * 64 + lane) / 2] = (uint8_t)(nib[c] | (hi_n << 4));
+            }
+        } else {
+#pragma unroll
+            for (int c = 0; c < NC; ++c) s_vnib[slot][c * 64 + lane] = nib[c];
+        }
+    }
+    __syncthreads();
+
+    if (which == 1) {
+        // V: channel-major, element j of slot t at byte j*P/2 + t/2, low nibble = even t.
+        const int p_lo = slot0 >> 1, p_hi = (slot0 + nslots - 1) >> 1;
+        const int npairs = p_hi - p_lo + 1;
+        for (int i = threadIdx.x; i < npairs * D; i += blockDim.x) {
+            const int j = i % D;
+            const int p = p_lo + i / D;
+            const int te = 2 * p, to = 2 * p + 1;
+            const bool has_e = te >= slot0 && te < slot0 + nslots;
+            const bool has_o = to >= slot0 && to < slot0 + nslots;
+            uint8_t* dst = rec + LY.dense + j * (kPage / 2) + p;
+            if (has_e && has_o)
+                *dst = (uint8_t)(s_vnib[te][j] | (s_vnib[to][j] << 4));
+            else if (has_e)
+                *dst = s_vnib[te][j];
+            else
+                *dst = (uint8_t)((*dst & 0x0f) | (s_vnib[to][j] << 4));
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_quantize(const QuantArgs& a, int d, int max_new_per_seq, hipStream_t st) {
+    const int waves = max(1, min(kPage, max_new_per_seq));
+    const int segs = (max_new_per_seq + kPage - 1) / kPage + 1;   // pages one sequence can touch
+    dim3 grid(segs, a.n_seqs, a.H * 2);
+    dim3 block(64 * waves);
+    if (d == 64)
+        hipLaunchKernelGGL(quantize_kernel<64>, grid, block, 0, st, a);
+    else if (d == 128)
+        hipLaunchKernelGGL(quantize_kernel<128>, grid, block, 0, st, a);
+    else
+        return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
+}  // namespace oaken
