@@ -1,0 +1,249 @@
+"""Decode-step benchmark of the Oaken hot path on one MI355X.
+
+One step = quantize one new K/V token per sequence into the paged cache, then batched
+decode attention over every sequence's full cache.  Default workload: a
+Llama-2-13B-shaped layer (batch 256, 40 heads MHA, head_dim 128, context 2048 with the
+new token, 16-token pages on a shuffled block table), synthetic seeded data.
+
+Prints one JSON line with tokens/s, the attention kernel's achieved HBM bandwidth against
+the 8 TB/s peak (algorithmic bytes / its average duration, timed with HIP events on the
+launch stream), the CPU oracle timed on a bounded sample, and the sampled parity error.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+
+
+def log(msg: str):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", type=int, default=3, help="1..5 (3 = batch-256 Llama-2-13B layer)")
+    ap.add_argument("--cpu-sample-seqs", type=int, default=64)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="after timing, run one plain copy of this size (counter calibration)")
+    return ap.parse_args()
+
+
+def source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("attention.hip", "oaken_internal.h"):
+        with open(os.path.join(ROOT, "paper_2503_18599_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def stored_traffic(workload_name: str):
+    """HBM bytes per attention launch from committed counter runs, if they were taken on
+    the current kernel source (else None)."""
+    p = os.path.join(ROOT, "profiles", "attention_traffic.json")
+    if not os.path.exists(p):
+        return None
+    try:
+        d = json.load(open(p))
+    except (OSError, ValueError):
+        return None
+    if d.get("source_hash") != source_hash() or d.get("workload") != workload_name:
+        return None
+    return d.get("bytes_per_launch")
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this benchmark runs on exactly one GPU; multi-GPU runs are "
+                                   "not part of this build", "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2503_18599_amd import binding as B
+    from paper_2503_18599_amd import synth
+
+    dev = "cuda"
+    torch.cuda.set_device(0)
+    B.lib()
+    w = synth.WORKLOADS[args.workload]
+    H, Hq, d = w.n_kv_heads, w.n_q_heads, w.head_dim
+    n = w.n_seqs
+    log(f"workload {w.name}: B={n} Hq={Hq} Hkv={H} d={d} ctx={w.ctx_min}..{w.ctx}")
+
+    # ---- setup: thresholds, cache prefill (not timed) ----------------------------
+    kc = synth.calibration_set(w, "k", dev)
+    vc = synth.calibration_set(w, "v", dev)
+    thr = B.calibrate_thresholds(kc, vc, 0.04, 0.06)
+    del kc, vc
+    lens = synth.seq_lengths(w)
+    bt_cpu, nblk = synth.block_table(w, lens)
+    bt = bt_cpu.to(dev)
+    cache = B.Cache(nblk, H, d, thr)
+    log(f"pool {cache.pool.numel() / 2**30:.2f} GiB, {nblk} pages")
+    chunk = 16
+    t0 = time.time()
+    for s0 in range(0, n, chunk):
+        ss = list(range(s0, min(n, s0 + chunk)))
+        pre = [int(lens[s]) - 1 for s in ss]
+        k = torch.cat([synth.kv_values_seq(w, "k", s, p, dev) for s, p in zip(ss, pre)])
+        v = torch.cat([synth.kv_values_seq(w, "v", s, p, dev) for s, p in zip(ss, pre)])
+        cu = torch.zeros(len(ss) + 1, dtype=torch.int32)
+        cu[1:] = torch.cumsum(torch.tensor(pre, dtype=torch.int32), 0)
+        B.quantize_kv(cache, k, v, bt[s0:s0 + len(ss)].contiguous(),
+                      torch.zeros(len(ss), dtype=torch.int32, device=dev), cu.to(dev), max(pre))
+        del k, v
+    torch.cuda.synchronize()
+    log(f"prefill-quantized {int(lens.sum()) - n} tokens in {time.time() - t0:.1f}s")
+
+    k_new = synth.new_token_values(w, "k", 0, dev)
+    v_new = synth.new_token_values(w, "v", 0, dev)
+    start = (lens - 1).to(torch.int32).to(dev)
+    cu1 = torch.arange(n + 1, dtype=torch.int32, device=dev)
+    q = synth.queries(w, 0, dev)
+    lens_d = lens.to(dev)
+    max_len = int(lens.max())
+    scale = float(np.float32(1.0 / math.sqrt(d)))
+    out = torch.empty(n, Hq, d, dtype=torch.float32, device=dev)
+    ws_bytes = B.attention_workspace_bytes(n, Hq, H, d, max_len)
+    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+
+    def step(ev=None):
+        B.quantize_kv(cache, k_new, v_new, bt, start, cu1, 1)
+        if ev is not None:
+            ev[0].record()
+        B.decode_attention(cache, q, bt, lens_d, max_len, scale, out=out, workspace=ws)
+        if ev is not None:
+            ev[1].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    attn_ms = [a.elapsed_time(b) for a, b in evs]
+    attn_avg_s = sum(attn_ms) / len(attn_ms) / 1e3
+    log(f"{args.steps} steps in {elapsed * 1e3:.2f} ms; attention avg {attn_avg_s * 1e6:.1f} us")
+
+    if args.copy_probe_mib:
+        src = torch.ones(args.copy_probe_mib * 2**20 // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
+
+    # ---- algorithmic bytes of one attention launch ----------------------------------
+    # per (token, KV head, K|V) vector: d/2 dense + d/64 counts + 12 meta + its COO bytes
+    P = 16
+    nc = d // 64
+    stride = cache.stride
+    rec = cache.pool.view(nblk, H, 2, stride)
+    counts = rec[:, :, :, : P * nc].reshape(nblk, H, 2, P, nc).to(torch.int32).sum(-1)  # [blk,H,2,P]
+    valid = torch.zeros(nblk, P, dtype=torch.bool)
+    for s in range(n):
+        L = int(lens[s])
+        for pg in range((L + P - 1) // P):
+            m = min(P, L - pg * P)
+            valid[int(bt_cpu[s, pg]), :m] = True
+    n_out = int((counts * valid.to(dev)[:, None, None, :]).sum())
+    n_vec = int(lens.sum()) * H * 2
+    kv_bytes = n_vec * (d // 2 + nc + 12) + n_out
+    aux_bytes = n * Hq * d * (2 + 4) + sum((int(L) + P - 1) // P for L in lens) * 4 + n * 4
+    aux_bytes += 2 * ws_bytes          # split partials: written once, read once by the combine
+    alg_bytes = kv_bytes + aux_bytes
+    achieved = alg_bytes / attn_avg_s / 1e9
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": stored_traffic(w.name),
+                "bytes_per_launch": alg_bytes, "kernel_us": round(attn_avg_s * 1e6, 2),
+                "outlier_fraction": round(n_out / (n_vec * d), 4)}
+
+    # ---- CPU oracle on a bounded sample + sampled parity -------------------------------
+    cpu = None
+    parity = None
+    if not args.no_cpu_baseline:
+        import oracle
+        S = min(n, args.cpu_sample_seqs)
+        sample = list(range(0, n, max(1, n // S)))[:S]
+        thr_np = thr.cpu().numpy()
+        lay = oracle.layout(P, d)
+        nb_s = [(int(lens[s]) + P - 1) // P for s in sample]
+        bt_s = np.zeros((S, max(nb_s)), np.int32)
+        off = 0
+        for i, nb in enumerate(nb_s):
+            bt_s[i, :nb] = np.arange(off, off + nb)
+            off += nb
+        pool_s = np.zeros(off * H * 2 * lay["stride"], np.uint8)
+        pre = np.array([int(lens[s]) - 1 for s in sample], np.int32)
+        kk = torch.cat([synth.kv_values_seq(w, "k", s, int(p), dev) for s, p in zip(sample, pre)]).cpu().numpy()
+        vv = torch.cat([synth.kv_values_seq(w, "v", s, int(p), dev) for s, p in zip(sample, pre)]).cpu().numpy()
+        cu = np.concatenate([[0], np.cumsum(pre)]).astype(np.int32)
+        oracle.quantize_kv(pool_s, off, P, H, d, thr_np, kk, vv, bt_s, np.zeros(S, np.int32), cu)
+        del kk, vv
+        kn = k_new.cpu().numpy()[sample]
+        vn = v_new.cpu().numpy()[sample]
+        qs = q.cpu().numpy()[sample]
+        lens_s = np.array([int(lens[s]) for s in sample], np.int32)
+        log(f"oracle sample: {S} sequences built; timing one decode step")
+        t0 = time.perf_counter()
+        oracle.quantize_kv(pool_s, off, P, H, d, thr_np, kn, vn, bt_s, pre, np.arange(S + 1, dtype=np.int32))
+        want = oracle.decode_attention(pool_s, off, P, H, d, thr_np, qs, bt_s, lens_s, scale)
+        cpu_s = time.perf_counter() - t0
+        cpu = {"value": round(S / cpu_s, 2), "unit": "tokens/s", "cores": oracle.max_threads(),
+               "kind": "oracle",
+               "sample": f"{S} of {n} sequences (full context, all {Hq} heads), one decode step "
+                         f"(quantize + attention), {cpu_s:.2f} s"}
+        got = out.cpu().numpy()[sample]
+        err = np.abs(got.astype(np.float64) - want)
+        okm = err <= 2e-3 + 1e-2 * np.abs(want)
+        parity = {"seqs": S, "max_abs": float(err.max()), "pass": bool(okm.all())}
+        log(f"oracle {cpu_s:.2f}s, parity max_abs={err.max():.2e} pass={bool(okm.all())}")
+
+    res = {
+        "metric": "decode-attention tokens/sec + achieved HBM GB/s (% of peak) at batch 256",
+        "value": round(n * args.steps / elapsed, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(elapsed / args.steps * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}: batch {n}, {Hq} query / {H} KV heads, head_dim {d}, "
+                               f"context {w.ctx_min}..{w.ctx} incl. the new token, 16-token pages, "
+                               f"shuffled block table; step = quantize 1 token/seq + attention",
+                   "global_batch": n, "seq_len": max_len, "parallelism": "single GPU"},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "parity_sample": parity,
+        "attention_source": source_hash(),
+    }
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

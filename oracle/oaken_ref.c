@@ -220,20 +220,23 @@ int oaken_ref_quantize_kv(uint8_t* pool, int num_blocks, int P, int H, int d, in
                           const int32_t* block_table, int max_blocks,
                           const int32_t* start_pos, const int32_t* cu_tokens, int n_seqs)
 {
-    uint8_t* code = (uint8_t*)malloc(d);
-    uint8_t* group = (uint8_t*)malloc(d);
-    uint8_t* coo = (uint8_t*)malloc(d);
-    uint8_t counts[16];
-    uint16_t meta[6];
-    int rc = 0;
-    for (int s = 0; s < n_seqs && rc == 0; ++s) {
-        for (int row = cu_tokens[s]; row < cu_tokens[s + 1]; ++row) {
-            const int pos = start_pos[s] + (row - cu_tokens[s]);
-            const int lb = pos / P, slot = pos % P;
-            if (lb >= max_blocks) { rc = -1; break; }
-            const int blk = block_table[(int64_t)s * max_blocks + lb];
-            if (blk < 0 || blk >= num_blocks) { rc = -1; break; }
-            for (int h = 0; h < H; ++h)
+    int bad = 0;
+    /* records of different (sequence, KV head) pairs are disjoint; within one record the
+       tokens are written in position order */
+#pragma omp parallel for collapse(2) schedule(dynamic)
+    for (int s = 0; s < n_seqs; ++s)
+        for (int h = 0; h < H; ++h) {
+            uint8_t* code = (uint8_t*)malloc(d);
+            uint8_t* group = (uint8_t*)malloc(d);
+            uint8_t* coo = (uint8_t*)malloc(d);
+            uint8_t counts[16];
+            uint16_t meta[6];
+            for (int row = cu_tokens[s]; row < cu_tokens[s + 1]; ++row) {
+                const int pos = start_pos[s] + (row - cu_tokens[s]);
+                const int lb = pos / P, slot = pos % P;
+                if (lb >= max_blocks) { bad = 1; break; }
+                const int blk = block_table[(int64_t)s * max_blocks + lb];
+                if (blk < 0 || blk >= num_blocks) { bad = 1; break; }
                 for (int which = 0; which < 2; ++which) {
                     const uint16_t* x = (which ? v_new : k_new) + ((int64_t)row * H + h) * d;
                     int n_coo = 0;
@@ -242,10 +245,10 @@ int oaken_ref_quantize_kv(uint8_t* pool, int num_blocks, int P, int H, int d, in
                     uint8_t* rec = pool + (((int64_t)blk * H + h) * 2 + which) * stride;
                     write_slot(rec, which, P, d, slot, code, meta, counts, coo, n_coo);
                 }
+            }
+            free(code); free(group); free(coo);
         }
-    }
-    free(code); free(group); free(coo);
-    return rc;
+    return bad ? -1 : 0;
 }
 
 /* ------------------------------------------------------------------------ */

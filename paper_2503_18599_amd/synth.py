@@ -149,3 +149,15 @@ def block_table(w: Workload, lens: torch.Tensor, extra_tokens: int = 0):
         bt[s, :n] = perm[off: off + n]
         off += n
     return bt, total
+
+
+def kv_values_seq(w: Workload, which: str, seq: int, n_tokens: int, device="cpu") -> torch.Tensor:
+    """fp16 [n_tokens][H_kv][d] for one sequence, reproducible on its own (seeded by the
+    data seed and the sequence index), so large caches can be built in chunks and any
+    sampled sequence regenerated later."""
+    return kv_values(w, which, n_tokens, w.seed("data") * 100003 + seq, device)
+
+
+def new_token_values(w: Workload, which: str, step: int, device="cpu") -> torch.Tensor:
+    """fp16 [n_seqs][H_kv][d]: the K or V row each sequence appends at decode step `step`."""
+    return kv_values(w, which, w.n_seqs, w.seed("data") * 7919 + 1000 + step, device)
