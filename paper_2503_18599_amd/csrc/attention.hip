@@ -224,7 +224,6 @@ __global__ __launch_bounds__(D) void attn_combine_kernel(AttnArgs a) {
 
 SplitPlan plan_splits(int32_t n_seqs, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
                       int32_t max_seq_len) {
-    (void)head_dim;
     const int G = n_q_heads / n_kv_heads;
     const int max_pages = (max_seq_len + kPage - 1) / kPage;
     const int64_t units = (int64_t)n_seqs * n_kv_heads;
@@ -232,7 +231,8 @@ SplitPlan plan_splits(int32_t n_seqs, int32_t n_q_heads, int32_t n_kv_heads, int
     int want = (int)((target + units - 1) / units);
     int pps = (max_pages + want - 1) / want;
     pps = max(pps, 8);
-    pps = min(pps, kScoreCap / (kPage * G));
+    const int cap = mfma_attention_supported(head_dim, G) ? mfma_score_cap() : kScoreCap;
+    pps = min(pps, cap / (kPage * G));
     pps = max(pps, 1);
     SplitPlan sp;
     sp.pages_per_split = pps;
@@ -245,6 +245,12 @@ hipError_t launch_attention(const AttnArgs& a, int d, hipStream_t st) {
     if (G > kMaxG) return hipErrorInvalidValue;
     const size_t shm = (size_t)G * a.pages_per_split * kPage * sizeof(float);
     dim3 grid(a.n_splits, a.H, a.n_seqs);
+    if (mfma_attention_supported(d, G)) {
+        hipError_t e = launch_attention_mfma(a, st);
+        if (e != hipSuccess || a.n_splits == 1) return e;
+        hipLaunchKernelGGL(attn_combine_kernel<128>, dim3(a.n_seqs * a.Hq), dim3(128), 0, st, a);
+        return hipGetLastError();
+    }
     if (d == 64) {
         hipLaunchKernelGGL(attn_split_kernel<64>, grid, dim3(kThreads), shm, st, a);
     } else if (d == 128) {

@@ -65,6 +65,8 @@ CASES = {
     "llama2-13b": (3, dict(n_seqs=3, ctx=2048)),
     "mistral-gqa": (4, dict(n_seqs=5, ctx=1500, ctx_min=1)),
     "llama3-32k": (5, dict(n_seqs=2, ctx=3000)),
+    # many (sequence, head) units: one page range per unit, no split combine
+    "llama2-13b-wide": (3, dict(n_seqs=103, ctx=37)),
 }
 
 
