@@ -1,6 +1,6 @@
 // Host side of the C ABI declared in include/oaken.h: argument validation, launch
 // planning and error reporting.  Nothing here touches device memory contents.
-#include "../../include/oaken.h"
+#include "oaken.h"
 #include "oaken_internal.h"
 
 #include <cmath>

@@ -231,8 +231,10 @@ SplitPlan plan_splits(int32_t n_seqs, int32_t n_q_heads, int32_t n_kv_heads, int
     int want = (int)((target + units - 1) / units);
     int pps = (max_pages + want - 1) / want;
     pps = max(pps, 8);
-    const int cap = mfma_attention_supported(head_dim, G) ? mfma_score_cap() : kScoreCap;
-    pps = min(pps, cap / (kPage * G));
+    if (mfma_attention_supported(head_dim, G))
+        pps = min(pps, mfma_score_cap() / kPage);
+    else
+        pps = min(pps, kScoreCap / (kPage * G));
     pps = max(pps, 1);
     SplitPlan sp;
     sp.pages_per_split = pps;

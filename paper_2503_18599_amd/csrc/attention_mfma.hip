@@ -1,5 +1,5 @@
 // Decode attention over the Oaken-quantized cache on CDNA4 int8 matrix cores
-// (head_dim 128, 1, 2 or 4 query heads per KV head).
+// (head_dim 128; 1, 2 or 4 query heads per KV head).
 //
 // Dequantization is split into a dense part that runs on MFMA and a sparse part that
 // runs on the vector units, mirroring the paper's dense/sparse split (Sec. 4.5) and
@@ -15,15 +15,17 @@
 //   operations per eight elements) span u and h of both nibbles, and the real-valued
 //   weights (the query, or p*Delta and p*Gp) enter as four balanced base-256 int8
 //   limbs.  v_mfma_i32_16x16x64_i8 then computes the sums exactly in int32.
-// * Inner and outer values (the COO stream) are corrected afterwards: each entry
-//   adds its true value minus the middle reading of its nibble.  One lane walks the
-//   entries of one (token, 64-value chunk) bucket, with a per-token table of the
-//   eight (group, side, h) offsets in LDS.
+// * Inner and outer values (the COO stream) are corrected afterwards: each entry adds
+//   its true value minus the middle reading of its nibble.  One lane walks the entries
+//   of one (token, 64-value chunk) bucket; a per-token table gives the correction as
+//   an affine function of the nibble for each (group, side) class.
 //
 // One wave owns (sequence, KV head, page range).  Pass 1 streams the key pages and
-// leaves scores in LDS, then the range's softmax, then pass 2 streams the value
-// pages.  Pages are handled in groups of eight: the group's record heads (counts and
-// scales) arrive first, so every sparse offset is known before its bytes are loaded.
+// leaves scores in LDS, then the range's softmax, then pass 2 streams the value pages.
+// Pages move in groups of four through a software pipeline: while a group is being
+// processed, the dense and sparse bytes of the next group and the record heads
+// (counts and scales) of the group after it are already in flight, so every sparse
+// offset is known before its bytes are requested.
 #include "oaken_internal.h"
 
 #include <hip/hip_fp16.h>
@@ -37,9 +39,12 @@ constexpr int D = 128;
 constexpr int P = kPage;
 constexpr Layout LY = make_layout(P, D);   // counts 0, meta 32, dense 224, sparse 1248
 constexpr int HB = 224;                    // counts + meta bytes at the start of a record
-constexpr int GRP = 8;                     // pages per group
-constexpr int KROW = 80;                   // LDS stride of a key token's 64 dense bytes
+constexpr int HCH = HB / 16;               // 16-byte chunks of a record head
+constexpr int GRP = 4;                     // pages per group (two correction pairs)
+constexpr int GT = GRP * P;                // tokens per group
+constexpr int PSTR = 1088;                 // LDS stride of a page's dense bytes (bank skew)
 constexpr int SPCAP = P * D;               // sparse capacity of one record
+constexpr int SPL = 2048;                  // group sparse bytes staged in LDS
 
 static_assert(LY.meta == 32 && LY.dense == HB && LY.sparse == 1248, "record layout");
 
@@ -87,7 +92,16 @@ __device__ __forceinline__ int wave_max_i(int v) {
     return v;
 }
 
-// Fixed-point shift so that |x| * 2^shift < 2^22 for every |x| <= mx.
+// Inclusive prefix sum within each row of 16 lanes (DPP row shifts).
+__device__ __forceinline__ int row_scan16(int x) {
+    x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false);   // row_shr:1
+    x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false);   // row_shr:2
+    x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false);   // row_shr:4
+    x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false);   // row_shr:8
+    return x;
+}
+
+// Fixed-point shift so that |x| * 2^shift <= 2^22 for every |x| <= mx.
 __device__ __forceinline__ int fix_shift(float mx) {
     if (!(mx > 0.0f)) return 0;
     int e;
@@ -121,17 +135,14 @@ __device__ __forceinline__ Tok token_consts(const uint8_t* meta, const float* th
     return T;
 }
 
-// Offsets (true value minus middle reading) indexed by ((COO >> 6) << 1) | h, and the
-// slope difference per nibble step: delta = tab.x + n * tab.y.
-__device__ __forceinline__ void write_table(float2* tab, const Tok& T) {
-    tab[0] = make_float2(T.b_il - T.base, T.kd_i);
-    tab[1] = make_float2(T.b_il - T.base - T.gp, T.kd_i);
-    tab[2] = make_float2(T.b_ol - T.base, T.kd_o);
-    tab[3] = make_float2(T.b_ol - T.base - T.gp, T.kd_o);
-    tab[4] = make_float2(T.b_ih - T.base, T.kd_i);
-    tab[5] = make_float2(T.b_ih - T.base - T.gp, T.kd_i);
-    tab[6] = make_float2(T.b_oh - T.base, T.kd_o);
-    tab[7] = make_float2(T.b_oh - T.base - T.gp, T.kd_o);
+// The kernel runs one wave per workgroup.  LDS operations of a wave execute in order,
+// so handing data between its lanes through LDS needs only the LDS counter to drain and
+// a compiler fence; a workgroup barrier would also wait for every global load in flight
+// and stall the prefetch pipeline.
+__device__ __forceinline__ void wave_sync() {
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0); vmcnt and expcnt left open
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
 __device__ __forceinline__ uint4 ld16(const uint8_t* p) {
@@ -140,23 +151,241 @@ __device__ __forceinline__ uint4 ld16(const uint8_t* p) {
 
 template <int G>
 struct Smem {
-    float q[G][D];
+    __align__(256) float q[G][D];
     int qi[G][D];
     float qsum[G];
     int qshift[G];
-    int vshift[G];
     float pbase[G];
     float m[G], l[G];
-    __align__(16) uint8_t head[GRP][HB];
-    int start[GRP][P + 1];                  // sparse start of each valid slot; [P] = total
-    __align__(16) uint8_t dense[2][P * KROW];
-    __align__(16) uint8_t sparse[2][SPCAP];
-    __align__(16) float2 tab[64][8];
-    __align__(16) float2 cgf[G][GRP * P];   // p*Delta, p*Gp of the group's tokens
-    int2 cg[G][GRP * P];                    // the same in fixed point
-    __align__(16) uint32_t at[G][4][4][4];  // value-pass A operand [head][limb][k-group][feature]
-    float oc[G][D];                         // value corrections
+    __align__(16) uint8_t head[2][GRP][HB];   // record heads of the current / next group
+    int start[2][GRP][P];                     // offset of each slot's COO bytes in its page
+    int soff[2][GRP + 1];                     // page offsets in the staged group sparse bytes
+    __align__(16) uint8_t dense[GRP][PSTR];   // K: token rows of 64 bytes; V: channel rows of 8
+    __align__(16) uint8_t sparse[SPL + 80];   // + slack for whole-dword reads past a bucket
+    __align__(16) float4 tokc[GT];            // base, Delta, Gp of the group's tokens
+    __align__(16) float2 tab[4][GT];          // correction table [COO class][token of the group]
+    int2 cg[G][GT];                           // fixed-point p*Delta, p*Gp of the group's tokens
+    __align__(16) uint32_t at[G][4][4][4];    // value-pass A operand [head][limb][k-group][feature]
+    float oc[G][D];                           // value corrections
 };
+
+// Wave-uniform description of a group of consecutive pages of one sequence.
+struct Grp {
+    const uint8_t* rec[GRP];
+    int nval[GRP];   // valid slots per page (0 when the page is outside the range)
+    int npg;
+};
+
+// `blk_lane` holds, in lane i, the block id of page p_begin + i of the range (or -1).
+__device__ __forceinline__ Grp make_group(const AttnArgs& a, int blk_lane, int p_begin, int g0,
+                                          int p_end, int L, int h, int which) {
+    Grp gr;
+    gr.npg = max(0, min(GRP, p_end - g0));
+#pragma unroll
+    for (int pg = 0; pg < GRP; ++pg) {
+        gr.rec[pg] = nullptr;
+        gr.nval[pg] = 0;
+        if (pg < gr.npg) {
+            const int blk = __builtin_amdgcn_readlane(blk_lane, g0 + pg - p_begin);
+            if (blk >= 0 && blk < a.num_blocks) {
+                gr.rec[pg] = a.pool + (((int64_t)blk * a.H + h) * 2 + which) * a.stride;
+                gr.nval[pg] = max(0, min(P, L - (g0 + pg) * P));
+            }
+        }
+    }
+    return gr;
+}
+
+template <typename T>
+__device__ __forceinline__ T pick4(int i, T a0, T a1, T a2, T a3) {
+    return i == 0 ? a0 : i == 1 ? a1 : i == 2 ? a2 : a3;
+}
+
+// Global loads are issued unconditionally, so the compiler never has to merge a loaded
+// and a default value (which would make it wait for the load right away and defeat the
+// prefetch).  Missing pages read a valid stand-in record whose bytes are never used:
+// every consumer masks by the page's valid-slot count.
+__device__ __forceinline__ const uint8_t* or_pool(const uint8_t* r, const uint8_t* pool) {
+    return r ? r : pool;
+}
+
+// One 16-byte chunk of the group's record heads (lanes >= 56 repeat a chunk).
+__device__ __forceinline__ uint4 head_chunk(const Grp& gr, const uint8_t* pool, int lane) {
+    const int c = lane < GRP * HCH ? lane : lane - GRP * HCH;
+    const int pg = c / HCH;
+    const uint8_t* r = or_pool(pick4(pg, gr.rec[0], gr.rec[1], gr.rec[2], gr.rec[3]), pool);
+    return ld16(r + (c % HCH) * 16);
+}
+
+// Sparse offsets of group buffer b from its heads; returns the group's staged size.
+template <int G>
+__device__ __forceinline__ int group_layout(Smem<G>& S, int b, const Grp& gr, int lane) {
+    const int pg = lane >> 4, t = lane & 15;
+    const int nv = pick4(pg, gr.nval[0], gr.nval[1], gr.nval[2], gr.nval[3]);
+    const int tot = (t < nv) ? (int)S.head[b][pg][2 * t] + (int)S.head[b][pg][2 * t + 1] : 0;
+    const int incl = row_scan16(tot);
+    S.start[b][pg][t] = incl - tot;
+    const int n0 = (min(__builtin_amdgcn_readlane(incl, 15), SPCAP) + 15) & ~15;
+    const int n1 = (min(__builtin_amdgcn_readlane(incl, 31), SPCAP) + 15) & ~15;
+    const int n2 = (min(__builtin_amdgcn_readlane(incl, 47), SPCAP) + 15) & ~15;
+    const int n3 = (min(__builtin_amdgcn_readlane(incl, 63), SPCAP) + 15) & ~15;
+    if (lane == 0) {
+        S.soff[b][0] = 0;
+        S.soff[b][1] = n0;
+        S.soff[b][2] = n0 + n1;
+        S.soff[b][3] = n0 + n1 + n2;
+        S.soff[b][4] = n0 + n1 + n2 + n3;
+    }
+    return n0 + n1 + n2 + n3;
+}
+
+// Loads of a group's used sparse bytes (16-byte chunks `lane` and `lane + 64` of the
+// concatenated, 16-byte padded page streams).  Chunks past the end reload chunk 0.
+__device__ __forceinline__ void sparse_chunks(const Grp& gr, const uint8_t* pool, int total, int s1,
+                                              int s2, int s3, int lane, uint4& r0, uint4& r1) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        int off = 16 * (lane + 64 * i);
+        off = (off < total && total <= SPL) ? off : 0;
+        const int pg = (off >= s1) + (off >= s2) + (off >= s3);
+        const int base = pick4(pg, 0, s1, s2, s3);
+        const uint8_t* r = or_pool(pick4(pg, gr.rec[0], gr.rec[1], gr.rec[2], gr.rec[3]), pool);
+        const uint4 v = ld16(r + LY.sparse + (off - base));
+        if (i == 0) r0 = v; else r1 = v;
+    }
+}
+
+// Writes the token's correction table: for COO class cls = COO >> 6 (bit 0 outer,
+// bit 1 upper side) and nibble n, the true value minus the nibble's middle reading is
+// x + n*y - (n >= 8 ? Gp : 0) with (x, y) = tab[cls] = (B_cls - base, Delta_g - Delta_m).
+// Everything is scaled by w.
+template <int G>
+__device__ __forceinline__ void token_table(Smem<G>& S, int tg, const Tok& T, float w) {
+    S.tab[0][tg] = make_float2(w * (T.b_il - T.base), w * T.kd_i);
+    S.tab[1][tg] = make_float2(w * (T.b_ol - T.base), w * T.kd_o);
+    S.tab[2][tg] = make_float2(w * (T.b_ih - T.base), w * T.kd_i);
+    S.tab[3][tg] = make_float2(w * (T.b_oh - T.base), w * T.kd_o);
+}
+
+// Per-lane bucket of COO entries: lane = (page of the pair, 64-value chunk, token).
+struct Bucket {
+    int pg, c, t, tg, cnt, st;
+    bool vt;
+};
+
+template <int G>
+__device__ __forceinline__ Bucket bucket_of(Smem<G>& S, int b, const Grp& gr, int pp, int lane) {
+    Bucket k;
+    k.c = (lane >> 4) & 1;
+    k.t = lane & 15;
+    k.pg = pp + (lane >> 5);
+    k.tg = k.pg * P + k.t;
+    const int nv = pick4(k.pg, gr.nval[0], gr.nval[1], gr.nval[2], gr.nval[3]);
+    k.vt = k.t < nv;
+    const int c0 = k.vt ? (int)S.head[b][k.pg][2 * k.t] : 0;
+    const int c1 = k.vt ? (int)S.head[b][k.pg][2 * k.t + 1] : 0;
+    k.st = k.vt ? S.start[b][k.pg][k.t] + (k.c ? c0 : 0) : 0;
+    // a 64-value chunk has at most 64 entries; larger counts are not a valid record
+    k.cnt = max(0, min(min(k.c ? c1 : c0, 64), SPCAP - k.st));
+    return k;
+}
+
+// Correction of COO entry e whose nibble is n, from the token's table and Gp.
+template <int G>
+__device__ __forceinline__ float entry_delta(const Smem<G>& S, int tg, uint32_t e, uint32_t n, float gp) {
+    const float2 kv = S.tab[e >> 6][tg];
+    return fmaf((float)n, kv.y, kv.x) - (n >= 8u ? gp : 0.0f);
+}
+
+// Walks each lane's bucket and adds every entry's q-weighted correction (true value
+// minus middle reading) to its token's score.  Staged entries are read four at a time
+// from one aligned dword pair; the four corrections of a block are independent, and
+// entries past the bucket contribute zero.
+template <int G, bool STAGED>
+__device__ __forceinline__ void key_corrections(Smem<G>& S, float* sc, int cap, float scale, int b,
+                                                const Grp& gr, int pp, int tok0, int lane) {
+    const Bucket k = bucket_of(S, b, gr, pp, lane);
+    const float gp = S.tokc[k.tg].z;
+    const uint8_t* drow = &S.dense[k.pg][k.t * 64 + k.c * 32];
+    const float* qc = &S.q[0][k.c * 64];
+    float corr[G];
+#pragma unroll
+    for (int hd = 0; hd < G; ++hd) corr[hd] = 0.0f;
+    const int maxc = wave_max_i(k.cnt);
+    auto slot = [&](uint32_t e, bool valid) {
+        const uint32_t dw = *reinterpret_cast<const uint32_t*>(drow + ((e >> 1) & 0x1cu));
+        const uint32_t n = (dw >> ((e & 7u) << 2)) & 15u;
+        const float delta = valid ? entry_delta(S, k.tg, e, n, gp) : 0.0f;
+#pragma unroll
+        for (int hd = 0; hd < G; ++hd) corr[hd] = fmaf(qc[hd * D + (e & 63u)], delta, corr[hd]);
+    };
+    if (STAGED) {
+        const int pos = S.soff[b][k.pg] + k.st;
+        const uint32_t* w = reinterpret_cast<const uint32_t*>(&S.sparse[pos & ~3]);
+        const uint32_t sh = pos & 3;
+        uint32_t cur = w[0];
+        for (int kk = 0; kk < maxc; kk += 4) {
+            const uint32_t nxt = w[(kk >> 2) + 1];
+            const uint32_t ent = __builtin_amdgcn_alignbyte(nxt, cur, sh);
+            cur = nxt;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) slot((ent >> (8 * i)) & 0xffu, kk + i < k.cnt);
+        }
+    } else {
+        const uint8_t* r = pick4(k.pg, gr.rec[0], gr.rec[1], gr.rec[2], gr.rec[3]);
+        const uint8_t* spp = r ? r + LY.sparse + k.st : nullptr;
+        for (int kk = 0; kk < maxc; ++kk)
+            if (kk < k.cnt) slot(spp[kk], true);
+    }
+#pragma unroll
+    for (int hd = 0; hd < G; ++hd) {
+        const float o = corr[hd] + __shfl_xor(corr[hd], 16, 64);
+        if (k.c == 0 && k.vt) sc[hd * cap + tok0 + k.tg] += scale * o;
+    }
+}
+
+// Same walk for values: each entry adds p_t * (true value - middle reading) to its
+// channel.  With one head the probability is already folded into the table and Gp.
+template <int G, bool STAGED>
+__device__ __forceinline__ void value_corrections(Smem<G>& S, const float* sc, int cap, int b,
+                                                  const Grp& gr, int pp, int tok0, int lane) {
+    const Bucket k = bucket_of(S, b, gr, pp, lane);
+    const float gp = S.tokc[k.tg].z;
+    float pt[G];
+#pragma unroll
+    for (int hd = 0; hd < G; ++hd) pt[hd] = (G > 1 && k.vt) ? sc[hd * cap + tok0 + k.tg] : 1.0f;
+    const uint8_t* dcol = &S.dense[k.pg][(k.t >> 3) * 4 + k.c * 512];
+    const uint32_t nsh = (k.t & 7) * 4;
+    float* occ = &S.oc[0][k.c * 64];
+    const int maxc = wave_max_i(k.cnt);
+    auto slot = [&](uint32_t e, bool valid) {
+        const uint32_t jj = e & 63u;
+        const uint32_t n = (*reinterpret_cast<const uint32_t*>(dcol + jj * 8) >> nsh) & 15u;
+        const float delta = entry_delta(S, k.tg, e, n, gp);
+        if (valid) {
+#pragma unroll
+            for (int hd = 0; hd < G; ++hd) atomicAdd(&occ[hd * D + jj], G == 1 ? delta : pt[hd] * delta);
+        }
+    };
+    if (STAGED) {
+        const int pos = S.soff[b][k.pg] + k.st;
+        const uint32_t* w = reinterpret_cast<const uint32_t*>(&S.sparse[pos & ~3]);
+        const uint32_t sh = pos & 3;
+        uint32_t cur = w[0];
+        for (int kk = 0; kk < maxc; kk += 4) {
+            const uint32_t nxt = w[(kk >> 2) + 1];
+            const uint32_t ent = __builtin_amdgcn_alignbyte(nxt, cur, sh);
+            cur = nxt;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) slot((ent >> (8 * i)) & 0xffu, kk + i < k.cnt);
+        }
+    } else {
+        const uint8_t* r = pick4(k.pg, gr.rec[0], gr.rec[1], gr.rec[2], gr.rec[3]);
+        const uint8_t* spp = r ? r + LY.sparse + k.st : nullptr;
+        for (int kk = 0; kk < maxc; ++kk)
+            if (kk < k.cnt) slot(spp[kk], true);
+    }
+}
 
 template <int G>
 __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
@@ -173,6 +402,8 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
     const int cap = a.pages_per_split * P;
     const int n_tok = max(0, min(L, p_end * P) - p_begin * P);
     const int32_t* btab = a.block_table + (int64_t)s * a.max_blocks;
+    // block ids of the range, one page per lane (a range spans at most 64 pages)
+    const int blk_lane = (p_begin + lane < p_end) ? btab[p_begin + lane] : -1;
 
     float tk[4], tv[4];
 #pragma unroll
@@ -180,12 +411,10 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
         tk[i] = fin(a.thr[(h * 2 + 0) * 4 + i]);
         tv[i] = fin(a.thr[(h * 2 + 1) * 4 + i]);
     }
-    auto record = [&](int page, int which) -> const uint8_t* {
-        const int blk = btab[page];
-        if (blk < 0 || blk >= a.num_blocks) return nullptr;
-        return a.pool + (((int64_t)blk * a.H + h) * 2 + which) * a.stride;
-    };
-    auto valid_slots = [&](int page) -> int { return max(0, min(P, L - page * P)); };
+
+    // the first key group's heads are needed before anything else
+    Grp gc = make_group(a, blk_lane, p_begin, p_begin, p_end, L, h, 0);
+    uint4 hreg = head_chunk(gc, a.pool, lane);
 
     // ---- query in fp32 and in fixed point -----------------------------------------
 #pragma unroll
@@ -204,7 +433,8 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
             S.qshift[hd] = sh;
         }
     }
-    __syncthreads();
+    if (lane < GRP * HCH) *reinterpret_cast<uint4*>(&S.head[0][0][16 * lane]) = hreg;
+    wave_sync();
 
     // Key-pass A operand: row = 8*(head%2) + 4*type + limb, type 0 -> sum q u, 1 -> sum q h.
     // Byte (4f + b) of k-group g4 in MFMA m pairs with feature f of dense byte 16*g4+4*m+b.
@@ -219,17 +449,17 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
                 uint32_t f0 = 0, f1 = 0, f2 = 0, f3 = 0;
                 if (hd < G) {
 #pragma unroll
-                    for (int b = 0; b < 4; ++b) {
-                        const int pr = g4 * 16 + m * 4 + b;
+                    for (int bb = 0; bb < 4; ++bb) {
+                        const int pr = g4 * 16 + m * 4 + bb;
                         const int qe = S.qi[hd][2 * pr], qo = S.qi[hd][2 * pr + 1];
                         const int w0 = type ? 0 : 8 * qo;
                         const int w1 = type ? 0 : 128 * qe - 8 * qo;
                         const int w2 = type ? -qo : -16 * qo;
                         const int w3 = type ? 16 * qe + qo : 16 * qo;
-                        f0 |= byte_of(enc(w0), r) << (8 * b);
-                        f1 |= byte_of(enc(w1), r) << (8 * b);
-                        f2 |= byte_of(enc(w2), r) << (8 * b);
-                        f3 |= byte_of(enc(w3), r) << (8 * b);
+                        f0 |= byte_of(enc(w0), r) << (8 * bb);
+                        f1 |= byte_of(enc(w1), r) << (8 * bb);
+                        f2 |= byte_of(enc(w2), r) << (8 * bb);
+                        f3 |= byte_of(enc(w3), r) << (8 * bb);
                     }
                 }
                 afk[rs][m][0] = (int)f0;
@@ -240,135 +470,96 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
         }
     }
 
-    // Loads the heads of a group and the sparse start offsets of its valid slots.
-    auto load_group_heads = [&](int g0, int npg, int which) {
-        for (int c = lane; c < GRP * 14; c += 64) {
-            const int pg = c / 14, off = (c % 14) * 16;
-            uint4 v = make_uint4(0, 0, 0, 0);
-            if (pg < npg) {
-                const uint8_t* rec = record(g0 + pg, which);
-                if (rec) v = ld16(rec + off);
-            }
-            *reinterpret_cast<uint4*>(&S.head[pg][off]) = v;
-        }
-        __syncthreads();
-#pragma unroll
-        for (int half = 0; half < 2; ++half) {
-            const int pg = half * 4 + (lane >> 4), t = lane & 15;
-            const bool ok = pg < npg && record(g0 + pg, which) != nullptr && t < valid_slots(g0 + pg);
-            const int tot = ok ? (int)S.head[pg][2 * t] + (int)S.head[pg][2 * t + 1] : 0;
-            int incl = tot;
-#pragma unroll
-            for (int d = 1; d < 16; d <<= 1) {
-                const int y = __shfl_up(incl, d, 16);
-                if (t >= d) incl += y;
-            }
-            S.start[pg][t] = incl - tot;
-            if (t == 15) S.start[pg][P] = min(incl, SPCAP);
-        }
-        __syncthreads();
-    };
-    // Copies the used sparse bytes of one page into LDS buffer k2.
-    auto load_sparse = [&](int g0, int pg, int npg, int which, int k2) {
-        if (pg >= npg) return;
-        const uint8_t* rec = record(g0 + pg, which);
-        if (!rec) return;
-        const int nch = (S.start[pg][P] + 15) >> 4;
-        for (int c = lane; c < nch; c += 64)
-            *reinterpret_cast<uint4*>(&S.sparse[k2][16 * c]) = ld16(rec + LY.sparse + 16 * c);
-    };
-
     // ---- pass 1: keys -------------------------------------------------------------
-    for (int g0 = p_begin; g0 < p_end; g0 += GRP) {
-        const int npg = min(GRP, p_end - g0);
-        load_group_heads(g0, npg, 0);
-        uint4 dreg[GRP];
+    uint4 dreg[GRP], sreg0, sreg1;
+    {
+        const int tot = group_layout(S, 0, gc, lane);
+        wave_sync();
+#pragma unroll
+        for (int pg = 0; pg < GRP; ++pg)
+            dreg[pg] = ld16(or_pool(gc.rec[pg], a.pool) + LY.dense + (lane & 15) * 64 + (lane >> 4) * 16);
+        sparse_chunks(gc, a.pool, tot, S.soff[0][1], S.soff[0][2], S.soff[0][3], lane, sreg0, sreg1);
+    }
+    Grp gn = make_group(a, blk_lane, p_begin, p_begin + GRP, p_end, L, h, 0);
+    hreg = head_chunk(gn, a.pool, lane);
+    int b = 0;
+    for (int g0 = p_begin; g0 < p_end; g0 += GRP, b ^= 1) {
+        const int tok0 = (g0 - p_begin) * P;
+        const bool staged = S.soff[b][GRP] <= SPL;
+        // token constants of the group (lane = token) and the key correction tables
+        {
+            const int pg = lane >> 4, t = lane & 15;
+            const Tok T = token_consts(&S.head[b][pg][LY.meta + 12 * t], tk);
+            S.tokc[lane] = make_float4(T.base, T.dm, T.gp, 0.0f);
+            token_table(S, lane, T, 1.0f);
+        }
+        wave_sync();
+        // dense part on the matrix cores; stage the group in LDS
 #pragma unroll
         for (int pg = 0; pg < GRP; ++pg) {
-            dreg[pg] = make_uint4(0, 0, 0, 0);
-            if (pg < npg) {
-                const uint8_t* rec = record(g0 + pg, 0);
-                if (rec) dreg[pg] = ld16(rec + LY.dense + (lane & 15) * 64 + (lane >> 4) * 16);
+            const uint4 dv = dreg[pg];
+            v4i acc[NRS];
+#pragma unroll
+            for (int rs = 0; rs < NRS; ++rs) acc[rs] = v4i{0, 0, 0, 0};
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+                const uint32_t dw = m == 0 ? dv.x : m == 1 ? dv.y : m == 2 ? dv.z : dv.w;
+                const v4i B = features(dw);
+#pragma unroll
+                for (int rs = 0; rs < NRS; ++rs) acc[rs] = mfma(afk[rs][m], B, acc[rs]);
+            }
+            *reinterpret_cast<uint4*>(&S.dense[pg][(lane & 15) * 64 + (lane >> 4) * 16]) = dv;
+            const int t = lane & 15, grp4 = lane >> 4;
+            const float4 tc = S.tokc[pg * P + t];
+            const int nv = gc.nval[pg];
+#pragma unroll
+            for (int rs = 0; rs < NRS; ++rs) {
+                const float v = limbs(acc[rs]);
+                const float o = __shfl_xor(v, 16, 64);
+                const int hd = rs * 2 + (grp4 >> 1);
+                if ((grp4 & 1) == 0 && hd < G && pg < gc.npg) {
+                    const int e = S.qshift[hd] + 7;
+                    const float dot = tc.x * S.qsum[hd] + tc.y * ldexpf(v, -e) + tc.z * ldexpf(o, -e);
+                    sc[hd * cap + tok0 + pg * P + t] = (t < nv) ? a.scale * dot : -INFINITY;
+                }
             }
         }
+        if (staged) {
+            *reinterpret_cast<uint4*>(&S.sparse[16 * lane]) = sreg0;
+            *reinterpret_cast<uint4*>(&S.sparse[16 * (lane + 64)]) = sreg1;
+        }
+        // next group: heads -> layout -> issue its dense/sparse and the heads after it
+        Grp gnn = gn;
+        if (gn.npg > 0) {
+            if (lane < GRP * HCH) *reinterpret_cast<uint4*>(&S.head[b ^ 1][0][16 * lane]) = hreg;
+            wave_sync();
+            const int tot = group_layout(S, b ^ 1, gn, lane);
+            wave_sync();
+#pragma unroll
+            for (int pg = 0; pg < GRP; ++pg)
+                dreg[pg] = ld16(or_pool(gn.rec[pg], a.pool) + LY.dense + (lane & 15) * 64 + (lane >> 4) * 16);
+            sparse_chunks(gn, a.pool, tot, S.soff[b ^ 1][1], S.soff[b ^ 1][2], S.soff[b ^ 1][3], lane,
+                          sreg0, sreg1);
+            gnn = make_group(a, blk_lane, p_begin, g0 + 2 * GRP, p_end, L, h, 0);
+            hreg = head_chunk(gnn, a.pool, lane);
+        }
+        wave_sync();
+        // sparse part
 #pragma unroll
         for (int pp = 0; pp < GRP; pp += 2) {
-            if (pp >= npg) break;
-            load_sparse(g0, pp, npg, 0, 0);
-            load_sparse(g0, pp + 1, npg, 0, 1);
-            *reinterpret_cast<uint4*>(&S.dense[0][(lane & 15) * KROW + (lane >> 4) * 16]) = dreg[pp];
-            *reinterpret_cast<uint4*>(&S.dense[1][(lane & 15) * KROW + (lane >> 4) * 16]) = dreg[pp + 1];
-            // dense part on the matrix cores
-#pragma unroll
-            for (int k2 = 0; k2 < 2; ++k2) {
-                const int pg = pp + k2;
-                const uint4 dv = dreg[pg];
-                v4i acc[NRS];
-#pragma unroll
-                for (int rs = 0; rs < NRS; ++rs) acc[rs] = v4i{0, 0, 0, 0};
-#pragma unroll
-                for (int m = 0; m < 4; ++m) {
-                    const uint32_t dw = m == 0 ? dv.x : m == 1 ? dv.y : m == 2 ? dv.z : dv.w;
-                    const v4i B = features(dw);
-#pragma unroll
-                    for (int rs = 0; rs < NRS; ++rs) acc[rs] = mfma(afk[rs][m], B, acc[rs]);
-                }
-                const int t = lane & 15, grp4 = lane >> 4;
-                const bool pv = pg < npg && record(g0 + pg, 0) != nullptr;
-                const int nval = pv ? valid_slots(g0 + pg) : 0;
-                const Tok T = token_consts(&S.head[pg][LY.meta + 12 * t], tk);
-                const int tok = (g0 + pg - p_begin) * P + t;
-#pragma unroll
-                for (int rs = 0; rs < NRS; ++rs) {
-                    const float v = limbs(acc[rs]);
-                    const float o = __shfl_xor(v, 16, 64);
-                    const int hd = rs * 2 + (grp4 >> 1);
-                    if ((grp4 & 1) == 0 && hd < G && pg < npg) {
-                        const int e = S.qshift[hd] + 7;
-                        const float dot = T.base * S.qsum[hd] + T.dm * ldexpf(v, -e) + T.gp * ldexpf(o, -e);
-                        sc[hd * cap + tok] = (t < nval) ? a.scale * dot : -INFINITY;
-                    }
-                }
-            }
-            __syncthreads();
-            // sparse part: lane = (page of pair, chunk, token)
-            {
-                const int k2 = lane >> 5, c = (lane >> 4) & 1, t = lane & 15;
-                const int pg = pp + k2;
-                const bool pv = pg < npg && record(g0 + pg, 0) != nullptr;
-                const bool vt = pv && t < valid_slots(g0 + pg);
-                const int c0 = vt ? (int)S.head[pg][2 * t] : 0;
-                const int c1 = vt ? (int)S.head[pg][2 * t + 1] : 0;
-                const int st = (vt ? S.start[pg][t] : 0) + (c ? c0 : 0);
-                const int cnt = max(0, min(c ? c1 : c0, SPCAP - st));
-                if (vt) write_table(S.tab[lane], token_consts(&S.head[pg][LY.meta + 12 * t], tk));
-                const int maxc = wave_max_i(cnt);
-                const uint8_t* spp = &S.sparse[k2][st];
-                const uint8_t* drow = &S.dense[k2][t * KROW + c * 32];
-                float corr[G];
-#pragma unroll
-                for (int hd = 0; hd < G; ++hd) corr[hd] = 0.0f;
-                for (int k = 0; k < maxc; ++k) {
-                    if (k < cnt) {
-                        const uint32_t b = spp[k];
-                        const uint32_t dw = *reinterpret_cast<const uint32_t*>(drow + ((b >> 1) & 0x1cu));
-                        const uint32_t n = (dw >> ((b & 7u) << 2)) & 15u;
-                        const float2 kv = S.tab[lane][((b >> 6) << 1) | (n >> 3)];
-                        const float delta = fmaf((float)n, kv.y, kv.x);
-                        const int j = c * 64 + (int)(b & 63u);
-#pragma unroll
-                        for (int hd = 0; hd < G; ++hd) corr[hd] = fmaf(S.q[hd][j], delta, corr[hd]);
-                    }
-                }
-#pragma unroll
-                for (int hd = 0; hd < G; ++hd) {
-                    const float o = corr[hd] + __shfl_xor(corr[hd], 16, 64);
-                    if (c == 0 && vt) sc[hd * cap + (g0 + pg - p_begin) * P + t] += a.scale * o;
-                }
-            }
-            __syncthreads();
+            if (staged)
+                key_corrections<G, true>(S, sc, cap, a.scale, b, gc, pp, tok0, lane);
+            else
+                key_corrections<G, false>(S, sc, cap, a.scale, b, gc, pp, tok0, lane);
         }
+        wave_sync();
+        gc = gn;
+        gn = gnn;
     }
+
+    // the first value group's heads go out before the softmax
+    gc = make_group(a, blk_lane, p_begin, p_begin, p_end, L, h, 1);
+    hreg = head_chunk(gc, a.pool, lane);
 
     // ---- softmax over the range ----------------------------------------------------
 #pragma unroll
@@ -390,7 +581,8 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
         S.oc[hd][lane] = 0.0f;
         S.oc[hd][lane + 64] = 0.0f;
     }
-    __syncthreads();
+    if (lane < GRP * HCH) *reinterpret_cast<uint4*>(&S.head[0][0][16 * lane]) = hreg;
+    wave_sync();
 
     // ---- pass 2: values ------------------------------------------------------------
     const int hq = lane >> 4;               // output lane owns (head hq, dim 16*nt + (lane&15))
@@ -400,57 +592,71 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
     float pb[G];
 #pragma unroll
     for (int hd = 0; hd < G; ++hd) pb[hd] = 0.0f;
-
-    for (int g0 = p_begin; g0 < p_end; g0 += GRP) {
-        const int npg = min(GRP, p_end - g0);
-        load_group_heads(g0, npg, 1);
-        uint4 dreg[GRP];
+    {
+        const int tot = group_layout(S, 0, gc, lane);
+        wave_sync();
 #pragma unroll
-        for (int pg = 0; pg < GRP; ++pg) {
-            dreg[pg] = make_uint4(0, 0, 0, 0);
-            if (pg < npg) {
-                const uint8_t* rec = record(g0 + pg, 1);
-                if (rec) dreg[pg] = ld16(rec + LY.dense + lane * 16);
-            }
-        }
-        // fixed-point coefficients p*Delta, p*Gp of the group's tokens, one shift per head
+        for (int pg = 0; pg < GRP; ++pg) dreg[pg] = ld16(or_pool(gc.rec[pg], a.pool) + LY.dense + lane * 16);
+        sparse_chunks(gc, a.pool, tot, S.soff[0][1], S.soff[0][2], S.soff[0][3], lane, sreg0, sreg1);
+    }
+    gn = make_group(a, blk_lane, p_begin, p_begin + GRP, p_end, L, h, 1);
+    hreg = head_chunk(gn, a.pool, lane);
+    b = 0;
+    for (int g0 = p_begin; g0 < p_end; g0 += GRP, b ^= 1) {
+        const int tok0 = (g0 - p_begin) * P;
+        const bool staged = S.soff[b][GRP] <= SPL;
 #pragma unroll
-        for (int hd = 0; hd < G; ++hd) {
-            float mx = 0.0f;
-            for (int tg = lane; tg < GRP * P; tg += 64) {
-                const int pg = tg >> 4, t = tg & 15;
-                const bool vt = pg < npg && record(g0 + pg, 1) != nullptr && t < valid_slots(g0 + pg);
-                float cx = 0.0f, gx = 0.0f;
-                if (vt) {
-                    const float p = sc[hd * cap + (g0 + pg - p_begin) * P + t];
-                    const Tok T = token_consts(&S.head[pg][LY.meta + 12 * t], tv);
-                    cx = p * T.dm;
-                    gx = p * T.gp;
-                    pb[hd] = fmaf(p, T.base, pb[hd]);
-                }
-                S.cgf[hd][tg] = make_float2(cx, gx);
-                mx = fmaxf(mx, fmaxf(fabsf(cx), fabsf(gx)));
-            }
-            const int sh = fix_shift(wave_max(mx));
-            for (int tg = lane; tg < GRP * P; tg += 64) {
-                const float2 f = S.cgf[hd][tg];
-                S.cg[hd][tg] = make_int2((int)rintf(ldexpf(f.x, sh)), (int)rintf(ldexpf(f.y, sh)));
-            }
-            if (lane == 0) S.vshift[hd] = sh;
+        for (int pg = 0; pg < GRP; ++pg) *reinterpret_cast<uint4*>(&S.dense[pg][lane * 16]) = dreg[pg];
+        if (staged) {
+            *reinterpret_cast<uint4*>(&S.sparse[16 * lane]) = sreg0;
+            *reinterpret_cast<uint4*>(&S.sparse[16 * (lane + 64)]) = sreg1;
         }
-        __syncthreads();
-
+        // fixed-point coefficients p*Delta, p*Gp of the group's tokens (lane = token), one
+        // shift per head; correction tables (scaled by p when one head reads them)
+        int vsh[G];
+        {
+            const int pg = lane >> 4, t = lane & 15;
+            const int nv = pick4(pg, gc.nval[0], gc.nval[1], gc.nval[2], gc.nval[3]);
+            const bool vt = t < nv;
+            const Tok T = token_consts(&S.head[b][pg][LY.meta + 12 * t], tv);
+            float p0 = 0.0f;
+#pragma unroll
+            for (int hd = 0; hd < G; ++hd) {
+                const float p = vt ? sc[hd * cap + tok0 + lane] : 0.0f;
+                if (hd == 0) p0 = p;
+                const float cx = vt ? p * T.dm : 0.0f;
+                const float gx = vt ? p * T.gp : 0.0f;
+                if (vt) pb[hd] = fmaf(p, T.base, pb[hd]);
+                const int sh = fix_shift(wave_max(fmaxf(fabsf(cx), fabsf(gx))));
+                S.cg[hd][lane] = make_int2((int)rintf(ldexpf(cx, sh)), (int)rintf(ldexpf(gx, sh)));
+                vsh[hd] = sh;
+            }
+            const float w = G == 1 ? p0 : 1.0f;
+            S.tokc[lane] = make_float4(T.base, T.dm, vt ? w * T.gp : 0.0f, 0.0f);
+            token_table(S, lane, T, vt ? w : 0.0f);
+        }
+        // next group: heads -> layout -> issue its loads
+        Grp gnn = gn;
+        if (gn.npg > 0) {
+            if (lane < GRP * HCH) *reinterpret_cast<uint4*>(&S.head[b ^ 1][0][16 * lane]) = hreg;
+            wave_sync();
+            const int tot = group_layout(S, b ^ 1, gn, lane);
+            wave_sync();
+#pragma unroll
+            for (int pg = 0; pg < GRP; ++pg)
+                dreg[pg] = ld16(or_pool(gn.rec[pg], a.pool) + LY.dense + lane * 16);
+            sparse_chunks(gn, a.pool, tot, S.soff[b ^ 1][1], S.soff[b ^ 1][2], S.soff[b ^ 1][3], lane,
+                          sreg0, sreg1);
+            gnn = make_group(a, blk_lane, p_begin, g0 + 2 * GRP, p_end, L, h, 1);
+            hreg = head_chunk(gnn, a.pool, lane);
+        }
+        wave_sync();
         v4i gacc[8];
 #pragma unroll
         for (int nt = 0; nt < 8; ++nt) gacc[nt] = v4i{0, 0, 0, 0};
 #pragma unroll
         for (int pp = 0; pp < GRP; pp += 2) {
-            if (pp >= npg) break;
-            load_sparse(g0, pp, npg, 1, 0);
-            load_sparse(g0, pp + 1, npg, 1, 1);
-            *reinterpret_cast<uint4*>(&S.dense[0][lane * 16]) = dreg[pp];
-            *reinterpret_cast<uint4*>(&S.dense[1][lane * 16]) = dreg[pp + 1];
-            // A operand: lane = (limb r, feature f, k-group g4); token pair 4*g4 + b
+            // A operand: lane = (limb r, feature f, k-group g4); token pair 4*g4 + bb
             {
                 const int r = lane & 3, f = (lane >> 2) & 3, g4 = lane >> 4;
                 const int al = f == 1 ? 128 : 0;
@@ -461,69 +667,43 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
                 for (int hd = 0; hd < G; ++hd) {
                     uint32_t dw = 0;
 #pragma unroll
-                    for (int b = 0; b < 4; ++b) {
-                        const int te = pp * P + 2 * (g4 * 4 + b);
-                        const int2 e = S.cg[hd][te], o = S.cg[hd][te + 1];
-                        const int w = al * e.x + be * o.x + ga * e.y + de * o.y;
-                        dw |= byte_of(enc(w), r) << (8 * b);
+                    for (int bb = 0; bb < 4; ++bb) {
+                        const int te = pp * P + 2 * (g4 * 4 + bb);
+                        const int2 ev = S.cg[hd][te], ov = S.cg[hd][te + 1];
+                        const int w = __mul24(al, ev.x) + __mul24(be, ov.x) + __mul24(ga, ev.y) +
+                                      __mul24(de, ov.y);
+                        dw |= byte_of(enc(w), r) << (8 * bb);
                     }
                     S.at[hd][r][g4][f] = dw;
                 }
             }
-            __syncthreads();
+            wave_sync();
             {
                 const int row = lane & 15, hdr = row >> 2, g4 = lane >> 4;
                 v4i av = v4i{0, 0, 0, 0};
                 if (hdr < G) av = *reinterpret_cast<const v4i*>(&S.at[hdr][row & 3][g4][0]);
+                const uint8_t* dsrc = &S.dense[pp + (g4 >> 1)][(g4 & 1) * 4];
 #pragma unroll
                 for (int nt = 0; nt < 8; ++nt) {
                     const int j = nt * 16 + (lane & 15);
-                    const uint32_t dw =
-                        *reinterpret_cast<const uint32_t*>(&S.dense[g4 >> 1][j * 8 + (g4 & 1) * 4]);
+                    const uint32_t dw = *reinterpret_cast<const uint32_t*>(dsrc + j * 8);
                     gacc[nt] = mfma(av, features(dw), gacc[nt]);
                 }
             }
-            // sparse part: lane = (page of pair, chunk, token)
-            {
-                const int k2 = lane >> 5, c = (lane >> 4) & 1, t = lane & 15;
-                const int pg = pp + k2;
-                const bool pv = pg < npg && record(g0 + pg, 1) != nullptr;
-                const bool vt = pv && t < valid_slots(g0 + pg);
-                const int c0 = vt ? (int)S.head[pg][2 * t] : 0;
-                const int c1 = vt ? (int)S.head[pg][2 * t + 1] : 0;
-                const int st = (vt ? S.start[pg][t] : 0) + (c ? c0 : 0);
-                const int cnt = max(0, min(c ? c1 : c0, SPCAP - st));
-                float pt[G];
-#pragma unroll
-                for (int hd = 0; hd < G; ++hd)
-                    pt[hd] = vt ? sc[hd * cap + (g0 + pg - p_begin) * P + t] : 0.0f;
-                if (vt) write_table(S.tab[lane], token_consts(&S.head[pg][LY.meta + 12 * t], tv));
-                const int maxc = wave_max_i(cnt);
-                const uint8_t* spp = &S.sparse[k2][st];
-                const uint8_t* dcol = &S.dense[k2][(t >> 3) * 4];
-                const int shift = (t & 7) * 4;
-                for (int k = 0; k < maxc; ++k) {
-                    if (k < cnt) {
-                        const uint32_t b = spp[k];
-                        const int j = c * 64 + (int)(b & 63u);
-                        const uint32_t dw = *reinterpret_cast<const uint32_t*>(dcol + j * 8);
-                        const uint32_t n = (dw >> shift) & 15u;
-                        const float2 kv = S.tab[lane][((b >> 6) << 1) | (n >> 3)];
-                        const float delta = fmaf((float)n, kv.y, kv.x);
-#pragma unroll
-                        for (int hd = 0; hd < G; ++hd) atomicAdd(&S.oc[hd][j], pt[hd] * delta);
-                    }
-                }
-            }
-            __syncthreads();
+            if (staged)
+                value_corrections<G, true>(S, sc, cap, b, gc, pp, tok0, lane);
+            else
+                value_corrections<G, false>(S, sc, cap, b, gc, pp, tok0, lane);
+            wave_sync();
         }
         // fold the group's integer sums into the fp32 outputs
         if (hq < G) {
-            const int e = S.vshift[hq] + 7;
+            const int e = pick4(hq, vsh[0], vsh[G > 1 ? 1 : 0], vsh[G > 2 ? 2 : 0], vsh[G > 3 ? 3 : 0]) + 7;
 #pragma unroll
             for (int nt = 0; nt < 8; ++nt) oacc[nt] += ldexpf(limbs(gacc[nt]), -e);
         }
-        __syncthreads();
+        gc = gn;
+        gn = gnn;
     }
 
 #pragma unroll
@@ -531,7 +711,7 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
         const float v = wave_sum(pb[hd]);
         if (lane == 0) S.pbase[hd] = v;
     }
-    __syncthreads();
+    wave_sync();
     if (hq < G) {
         const int64_t row = (int64_t)s * a.Hq + h * G + hq;
         const float l = S.l[hq];
@@ -557,10 +737,11 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
 
 bool mfma_attention_supported(int d, int G) { return d == D && (G == 1 || G == 2 || G == 4); }
 
-int mfma_score_cap() { return 2048; }
+int mfma_score_cap() { return 512; }
 
 hipError_t launch_attention_mfma(const AttnArgs& a, hipStream_t st) {
     const int G = a.Hq / a.H;
+    if (a.pages_per_split > 64) return hipErrorInvalidValue;
     const size_t shm = (size_t)G * a.pages_per_split * P * sizeof(float);
     dim3 grid(a.n_splits, a.H, a.n_seqs);
     if (G == 1)

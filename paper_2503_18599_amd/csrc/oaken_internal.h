@@ -73,7 +73,7 @@ hipError_t launch_attention(const AttnArgs& a, int d, hipStream_t st);
 
 // Matrix-core decode attention (head_dim 128; 1, 2 or 4 query heads per KV head).
 bool mfma_attention_supported(int d, int G);
-int mfma_score_cap();   // fp32 scores per workgroup (G * tokens in its page range)
+int mfma_score_cap();   // tokens per query head in one workgroup's page range
 hipError_t launch_attention_mfma(const AttnArgs& a, hipStream_t st);
 
 }  // namespace oaken
