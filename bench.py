@@ -35,7 +35,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", type=int, default=3, help="1..5 (3 = batch-256 Llama-2-13B layer)")
-    ap.add_argument("--cpu-sample-seqs", type=int, default=64)
+    ap.add_argument("--cpu-sample-seqs", type=int, default=128)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after timing, run one plain copy of this size (counter calibration)")
@@ -44,7 +44,7 @@ def parse():
 
 def source_hash() -> str:
     h = hashlib.sha256()
-    for f in ("attention.hip", "oaken_internal.h"):
+    for f in ("attention.hip", "attention_mfma.hip", "oaken_internal.h"):
         with open(os.path.join(ROOT, "paper_2503_18599_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -206,14 +206,17 @@ def main():
         qs = q.cpu().numpy()[sample]
         lens_s = np.array([int(lens[s]) for s in sample], np.int32)
         log(f"oracle sample: {S} sequences built; timing one decode step")
-        t0 = time.perf_counter()
-        oracle.quantize_kv(pool_s, off, P, H, d, thr_np, kn, vn, bt_s, pre, np.arange(S + 1, dtype=np.int32))
-        want = oracle.decode_attention(pool_s, off, P, H, d, thr_np, qs, bt_s, lens_s, scale)
-        cpu_s = time.perf_counter() - t0
+        times = []
+        for _ in range(3):   # median of three steps (re-quantizing the same slot is idempotent)
+            t0 = time.perf_counter()
+            oracle.quantize_kv(pool_s, off, P, H, d, thr_np, kn, vn, bt_s, pre, np.arange(S + 1, dtype=np.int32))
+            want = oracle.decode_attention(pool_s, off, P, H, d, thr_np, qs, bt_s, lens_s, scale)
+            times.append(time.perf_counter() - t0)
+        cpu_s = sorted(times)[1]
         cpu = {"value": round(S / cpu_s, 2), "unit": "tokens/s", "cores": oracle.max_threads(),
                "kind": "oracle",
                "sample": f"{S} of {n} sequences (full context, all {Hq} heads), one decode step "
-                         f"(quantize + attention), {cpu_s:.2f} s"}
+                         f"(quantize + attention), median of 3: {cpu_s:.2f} s"}
         got = out.cpu().numpy()[sample]
         err = np.abs(got.astype(np.float64) - want)
         okm = err <= 2e-3 + 1e-2 * np.abs(want)
