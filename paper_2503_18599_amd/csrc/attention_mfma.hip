@@ -167,6 +167,7 @@ struct Smem {
     int2 cg[G][GT];                           // fixed-point p*Delta, p*Gp of the group's tokens
     __align__(16) uint32_t at[G][4][4][4];    // value-pass A operand [head][limb][k-group][feature]
     float oc[G][D];                           // value corrections
+    int oci[G][D];                            // value corrections of one group, fixed point
 };
 
 // Wave-uniform description of a group of consecutive pages of one sequence.
@@ -356,7 +357,7 @@ __device__ __forceinline__ void value_corrections(Smem<G>& S, const float* sc, i
     for (int hd = 0; hd < G; ++hd) pt[hd] = (G > 1 && k.vt) ? sc[hd * cap + tok0 + k.tg] : 1.0f;
     const uint8_t* dcol = &S.dense[k.pg][(k.t >> 3) * 4 + k.c * 512];
     const uint32_t nsh = (k.t & 7) * 4;
-    float* occ = &S.oc[0][k.c * 64];
+    int* occ = &S.oci[0][k.c * 64];
     const int maxc = wave_max_i(k.cnt);
     auto slot = [&](uint32_t e, bool valid) {
         const uint32_t jj = e & 63u;
@@ -364,7 +365,7 @@ __device__ __forceinline__ void value_corrections(Smem<G>& S, const float* sc, i
         const float delta = entry_delta(S, k.tg, e, n, gp);
         if (valid) {
 #pragma unroll
-            for (int hd = 0; hd < G; ++hd) atomicAdd(&occ[hd * D + jj], G == 1 ? delta : pt[hd] * delta);
+            for (int hd = 0; hd < G; ++hd) atomicAdd(&occ[hd * D + jj], (int)(G == 1 ? delta : pt[hd] * delta));
         }
     };
     if (STAGED) {
@@ -580,6 +581,8 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
         }
         S.oc[hd][lane] = 0.0f;
         S.oc[hd][lane + 64] = 0.0f;
+        S.oci[hd][lane] = 0;
+        S.oci[hd][lane + 64] = 0;
     }
     if (lane < GRP * HCH) *reinterpret_cast<uint4*>(&S.head[0][0][16 * lane]) = hreg;
     wave_sync();
@@ -614,6 +617,7 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
         // fixed-point coefficients p*Delta, p*Gp of the group's tokens (lane = token), one
         // shift per head; correction tables (scaled by p when one head reads them)
         int vsh[G];
+        int fsh;
         {
             const int pg = lane >> 4, t = lane & 15;
             const int nv = pick4(pg, gc.nval[0], gc.nval[1], gc.nval[2], gc.nval[3]);
@@ -631,9 +635,20 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
                 S.cg[hd][lane] = make_int2((int)rintf(ldexpf(cx, sh)), (int)rintf(ldexpf(gx, sh)));
                 vsh[hd] = sh;
             }
-            const float w = G == 1 ? p0 : 1.0f;
-            S.tokc[lane] = make_float4(T.base, T.dm, vt ? w * T.gp : 0.0f, 0.0f);
-            token_table(S, lane, T, vt ? w : 0.0f);
+            // Value corrections accumulate as integers (LDS float atomics are slow): the
+            // table is scaled by 2^fsh, chosen so that 64 tokens' largest corrections
+            // stay below 2^30 in magnitude.
+            const float w = vt ? (G == 1 ? p0 : 1.0f) : 0.0f;
+            const float bound = w * (fmaxf(fmaxf(fabsf(T.b_il - T.base), fabsf(T.b_ol - T.base)),
+                                           fmaxf(fabsf(T.b_ih - T.base), fabsf(T.b_oh - T.base))) +
+                                     15.0f * fmaxf(fabsf(T.kd_i), fabsf(T.kd_o)) + fabsf(T.gp));
+            const float gb = wave_max(bound);
+            int ge = 0;
+            if (gb > 0.0f) frexpf(gb, &ge);
+            fsh = gb > 0.0f ? 24 - ge : 0;
+            const float ws = ldexpf(w, fsh);
+            S.tokc[lane] = make_float4(T.base, T.dm, ws * T.gp, 0.0f);
+            token_table(S, lane, T, ws);
         }
         // next group: heads -> layout -> issue its loads
         Grp gnn = gn;
@@ -697,6 +712,13 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
             wave_sync();
         }
         // fold the group's integer sums into the fp32 outputs
+#pragma unroll
+        for (int hd = 0; hd < G; ++hd) {
+            S.oc[hd][lane] += ldexpf((float)S.oci[hd][lane], -fsh);
+            S.oc[hd][lane + 64] += ldexpf((float)S.oci[hd][lane + 64], -fsh);
+            S.oci[hd][lane] = 0;
+            S.oci[hd][lane + 64] = 0;
+        }
         if (hq < G) {
             const int e = pick4(hq, vsh[0], vsh[G > 1 ? 1 : 0], vsh[G > 2 ? 2 : 0], vsh[G > 3 ? 3 : 0]) + 7;
 #pragma unroll

@@ -170,6 +170,37 @@ def test_attention_single_token_and_ragged(B, ref):
     assert ok, (max_abs, max_rel)
 
 
+@pytest.mark.parametrize("mode", ["all-outliers", "no-inner", "mixed"])
+def test_attention_edge_thresholds(B, ref, mode):
+    """Attention over extreme COO loads: every value an outlier (the largest page groups,
+    read from HBM instead of staged), no inner group, and heads alternating between the
+    two; with collapsed intervals, zero and constant vectors."""
+    w = synth.scaled(synth.WORKLOADS[3], n_seqs=3, ctx=300)
+    case = Case(w)
+    H = case.H
+    thr = np.zeros((H, 2, 4), np.float32)
+    if mode in ("all-outliers", "mixed"):
+        thr[:, :, 0], thr[:, :, 1], thr[:, :, 2], thr[:, :, 3] = -np.inf, -np.inf, np.inf, np.inf
+    if mode in ("no-inner", "mixed"):
+        sel = slice(None) if mode == "no-inner" else slice(1, None, 2)
+        thr[sel] = np.array([-1.0, 0.0, 0.0, 1.0], np.float32)
+    case.thr = thr
+    case.k[3] = 0.0
+    case.v[5] = 1.5
+    case.k[7, :, :64] = -2.0
+    pool_ref = case.oracle_pool(ref)
+    cache, bt = _gpu_cache(B, case)
+    compare_pools(ref, case, cache.pool.cpu().numpy(), pool_ref)
+    q = synth.queries(case.w)
+    scale = float(np.float32(1.0 / math.sqrt(case.d)))
+    want = ref.decode_attention(pool_ref, case.num_blocks, 16, case.H, case.d, case.thr, np16(q),
+                                case.bt.numpy(), case.lens.numpy(), scale)
+    got = B.decode_attention(cache, q.to(DEV), bt, case.lens.to(DEV), int(case.lens.max()), scale)
+    ok, max_abs, max_rel = attention_tolerance(got.cpu().numpy(), want)
+    print(f"{mode}: max_abs={max_abs:.3e} max_rel={max_rel:.3e}")
+    assert ok, (max_abs, max_rel)
+
+
 def test_abi_rejects_bad_arguments_on_gpu(B):
     thr = torch.zeros(2, 2, 4, device=DEV)
     cache = B.Cache(4, 2, 128, thr)
