@@ -42,7 +42,7 @@ constexpr int HB = 224;                    // counts + meta bytes at the start o
 constexpr int HCH = HB / 16;               // 16-byte chunks of a record head
 constexpr int GRP = 4;                     // pages per group (two correction pairs)
 constexpr int GT = GRP * P;                // tokens per group
-constexpr int PSTR = 1088;                 // LDS stride of a page's dense bytes (bank skew)
+constexpr int PSTR = 1024;                 // LDS stride of a page's dense bytes
 constexpr int SPCAP = P * D;               // sparse capacity of one record
 constexpr int SPL = 2048;                  // group sparse bytes staged in LDS
 
@@ -76,20 +76,32 @@ __device__ __forceinline__ float limbs(v4i c) {
     return fmaf(fmaf(fmaf((float)c[3], 256.f, (float)c[2]), 256.f, (float)c[1]), 256.f, (float)c[0]);
 }
 
+// Wave reductions: a shift-scan within each row of 16 lanes (DPP row_shr 1, 2, 4, 8
+// leaves the row's total in its lane 15), then the four row totals through readlane.
+// No LDS round trip; the result is wave-uniform.
+template <typename T, typename Op>
+__device__ __forceinline__ T wave_reduce(T v, T ident, Op op) {
+    static_assert(sizeof(T) == 4, "32-bit values");
+    const int id = __builtin_bit_cast(int, ident);
+    v = op(v, __builtin_bit_cast(T, __builtin_amdgcn_update_dpp(id, __builtin_bit_cast(int, v), 0x111, 0xf, 0xf, false)));
+    v = op(v, __builtin_bit_cast(T, __builtin_amdgcn_update_dpp(id, __builtin_bit_cast(int, v), 0x112, 0xf, 0xf, false)));
+    v = op(v, __builtin_bit_cast(T, __builtin_amdgcn_update_dpp(id, __builtin_bit_cast(int, v), 0x114, 0xf, 0xf, false)));
+    v = op(v, __builtin_bit_cast(T, __builtin_amdgcn_update_dpp(id, __builtin_bit_cast(int, v), 0x118, 0xf, 0xf, false)));
+    const int x = __builtin_bit_cast(int, v);
+    const T r0 = __builtin_bit_cast(T, __builtin_amdgcn_readlane(x, 15));
+    const T r1 = __builtin_bit_cast(T, __builtin_amdgcn_readlane(x, 31));
+    const T r2 = __builtin_bit_cast(T, __builtin_amdgcn_readlane(x, 47));
+    const T r3 = __builtin_bit_cast(T, __builtin_amdgcn_readlane(x, 63));
+    return op(op(r0, r1), op(r2, r3));
+}
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-    return v;
+    return wave_reduce(v, -INFINITY, [](float a, float b) { return fmaxf(a, b); });
 }
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-    return v;
+    return wave_reduce(v, 0.0f, [](float a, float b) { return a + b; });
 }
 __device__ __forceinline__ int wave_max_i(int v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o, 64));
-    return v;
+    return wave_reduce(v, (int)0x80000000, [](int a, int b) { return max(a, b); });
 }
 
 // Inclusive prefix sum within each row of 16 lanes (DPP row shifts).
@@ -149,25 +161,27 @@ __device__ __forceinline__ uint4 ld16(const uint8_t* p) {
     return *reinterpret_cast<const uint4*>(p);
 }
 
+// The correction slots build LDS addresses by OR-ing entry bits into aligned bases, so
+// the first members sit at offsets that are multiples of their sizes: tab at 0 (bits
+// 10-11 select the class, bit 3 the nibble half), dense at 4096 (a page per 1024 bytes;
+// K rows of 64 bytes, V channel rows of 8 bytes), q and oci 256-aligned.
 template <int G>
 struct Smem {
-    __align__(256) float q[G][D];
+    __align__(16) float2 tab[4][GT][2];       // correction table [COO class][token][nibble bit 3]
+    __align__(16) uint8_t dense[GRP][PSTR];   // K: token rows of 64 bytes; V: channel rows of 8
+    __align__(16) float q[G][D];
+    __align__(16) int oci[G][D];              // value corrections of one group, fixed point
     int qi[G][D];
-    float qsum[G];
-    int qshift[G];
     float pbase[G];
     float m[G], l[G];
     __align__(16) uint8_t head[2][GRP][HB];   // record heads of the current / next group
     int start[2][GRP][P];                     // offset of each slot's COO bytes in its page
     int soff[2][GRP + 1];                     // page offsets in the staged group sparse bytes
-    __align__(16) uint8_t dense[GRP][PSTR];   // K: token rows of 64 bytes; V: channel rows of 8
     __align__(16) uint8_t sparse[SPL + 80];   // + slack for whole-dword reads past a bucket
     __align__(16) float4 tokc[GT];            // base, Delta, Gp of the group's tokens
-    __align__(16) float2 tab[4][GT];          // correction table [COO class][token of the group]
     int2 cg[G][GT];                           // fixed-point p*Delta, p*Gp of the group's tokens
     __align__(16) uint32_t at[G][4][4][4];    // value-pass A operand [head][limb][k-group][feature]
     float oc[G][D];                           // value corrections
-    int oci[G][D];                            // value corrections of one group, fixed point
 };
 
 // Wave-uniform description of a group of consecutive pages of one sequence.
@@ -257,15 +271,17 @@ __device__ __forceinline__ void sparse_chunks(const Grp& gr, const uint8_t* pool
 }
 
 // Writes the token's correction table: for COO class cls = COO >> 6 (bit 0 outer,
-// bit 1 upper side) and nibble n, the true value minus the nibble's middle reading is
-// x + n*y - (n >= 8 ? Gp : 0) with (x, y) = tab[cls] = (B_cls - base, Delta_g - Delta_m).
-// Everything is scaled by w.
+// bit 1 upper side) and nibble n with high bit h, the true value minus the nibble's
+// middle reading is x + n*y with (x, y) = tab[cls][tg][h]: x = B_cls - base - h*Gp,
+// y = Delta_group - Delta_middle.  Everything is scaled by w.
 template <int G>
 __device__ __forceinline__ void token_table(Smem<G>& S, int tg, const Tok& T, float w) {
-    S.tab[0][tg] = make_float2(w * (T.b_il - T.base), w * T.kd_i);
-    S.tab[1][tg] = make_float2(w * (T.b_ol - T.base), w * T.kd_o);
-    S.tab[2][tg] = make_float2(w * (T.b_ih - T.base), w * T.kd_i);
-    S.tab[3][tg] = make_float2(w * (T.b_oh - T.base), w * T.kd_o);
+    const float x[4] = {T.b_il - T.base, T.b_ol - T.base, T.b_ih - T.base, T.b_oh - T.base};
+    const float y[4] = {T.kd_i, T.kd_o, T.kd_i, T.kd_o};
+#pragma unroll
+    for (int cls = 0; cls < 4; ++cls)
+        *reinterpret_cast<float4*>(&S.tab[cls][tg][0]) =
+            make_float4(w * x[cls], w * y[cls], w * (x[cls] - T.gp), w * y[cls]);
 }
 
 // Per-lane bucket of COO entries: lane = (page of the pair, 64-value chunk, token).
@@ -291,11 +307,29 @@ __device__ __forceinline__ Bucket bucket_of(Smem<G>& S, int b, const Grp& gr, in
     return k;
 }
 
-// Correction of COO entry e whose nibble is n, from the token's table and Gp.
+// x >> s for s >= 0, x << -s otherwise (s is a compile-time constant after unrolling).
+__device__ __forceinline__ uint32_t shr(uint32_t x, int s) { return s >= 0 ? x >> s : x << -s; }
+
+template <typename T, int G>
+__device__ __forceinline__ const T& lds_at(const Smem<G>& S, uint32_t off) {
+    return *reinterpret_cast<const T*>(reinterpret_cast<const char*>(&S) + off);
+}
+
+// Correction of the COO entry held in bits o..o+7 of ent, whose nibble is n; tbo is
+// the LDS offset of the token's table row tab[0][tg][0].
 template <int G>
-__device__ __forceinline__ float entry_delta(const Smem<G>& S, int tg, uint32_t e, uint32_t n, float gp) {
-    const float2 kv = S.tab[e >> 6][tg];
-    return fmaf((float)n, kv.y, kv.x) - (n >= 8u ? gp : 0.0f);
+__device__ __forceinline__ float entry_delta(Smem<G>& S, uint32_t tbo, uint32_t ent, int o, uint32_t n) {
+    const uint32_t ta = (tbo | (shr(ent, o - 4) & 0xc00u)) | (n & 8u);
+    const float2 kv = *reinterpret_cast<const float2*>(reinterpret_cast<const char*>(&S) + ta);
+    return fmaf((float)n, kv.y, kv.x);
+}
+
+static_assert(offsetof(Smem<1>, dense) == 4096 && offsetof(Smem<4>, q) == 8192 &&
+              offsetof(Smem<4>, oci) == 8192 + 4 * 512, "LDS layout the correction addressing relies on");
+
+template <int G>
+__device__ __forceinline__ uint32_t off_of(const Smem<G>& S, const void* p) {
+    return (uint32_t)(reinterpret_cast<const char*>(p) - reinterpret_cast<const char*>(&S));
 }
 
 // Walks each lane's bucket and adds every entry's q-weighted correction (true value
@@ -306,19 +340,25 @@ template <int G, bool STAGED>
 __device__ __forceinline__ void key_corrections(Smem<G>& S, float* sc, int cap, float scale, int b,
                                                 const Grp& gr, int pp, int tok0, int lane) {
     const Bucket k = bucket_of(S, b, gr, pp, lane);
-    const float gp = S.tokc[k.tg].z;
-    const uint8_t* drow = &S.dense[k.pg][k.t * 64 + k.c * 32];
-    const float* qc = &S.q[0][k.c * 64];
+    const uint32_t tbo = off_of(S, &S.tab[0][k.tg][0]);
+    const uint32_t drow = off_of(S, &S.dense[k.pg][k.t * 64 + k.c * 32]);
+    const uint32_t qc = off_of(S, &S.q[0][k.c * 64]);
     float corr[G];
 #pragma unroll
     for (int hd = 0; hd < G; ++hd) corr[hd] = 0.0f;
     const int maxc = wave_max_i(k.cnt);
-    auto slot = [&](uint32_t e, bool valid) {
-        const uint32_t dw = *reinterpret_cast<const uint32_t*>(drow + ((e >> 1) & 0x1cu));
-        const uint32_t n = (dw >> ((e & 7u) << 2)) & 15u;
-        const float delta = valid ? entry_delta(S, k.tg, e, n, gp) : 0.0f;
+    // The entry in bits o..o+7 of ent: index j (6 bits), class (2 bits).  Every slot is
+    // computed; slots past the bucket get a zero weight (no branches).
+    auto slot = [&](uint32_t ent, int o, bool valid) {
+        const uint32_t dw = lds_at<uint32_t>(S, drow | (shr(ent, o + 1) & 0x1cu));
+        const uint32_t n = __builtin_amdgcn_ubfe(dw, ((ent >> o) & 0xffu) << 2, 4);
+        const float delta = entry_delta(S, tbo, ent, o, n);
+        const uint32_t qo = qc | (shr(ent, o - 2) & 0xfcu);
 #pragma unroll
-        for (int hd = 0; hd < G; ++hd) corr[hd] = fmaf(qc[hd * D + (e & 63u)], delta, corr[hd]);
+        for (int hd = 0; hd < G; ++hd) {
+            const float q = lds_at<float>(S, qo + hd * D * 4);
+            corr[hd] = fmaf(valid ? q : 0.0f, delta, corr[hd]);
+        }
     };
     if (STAGED) {
         const int pos = S.soff[b][k.pg] + k.st;
@@ -330,13 +370,13 @@ __device__ __forceinline__ void key_corrections(Smem<G>& S, float* sc, int cap, 
             const uint32_t ent = __builtin_amdgcn_alignbyte(nxt, cur, sh);
             cur = nxt;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) slot((ent >> (8 * i)) & 0xffu, kk + i < k.cnt);
+            for (int i = 0; i < 4; ++i) slot(ent, 8 * i, kk + i < k.cnt);
         }
     } else {
         const uint8_t* r = pick4(k.pg, gr.rec[0], gr.rec[1], gr.rec[2], gr.rec[3]);
         const uint8_t* spp = r ? r + LY.sparse + k.st : nullptr;
         for (int kk = 0; kk < maxc; ++kk)
-            if (kk < k.cnt) slot(spp[kk], true);
+            if (kk < k.cnt) slot(spp[kk], 0, true);
     }
 #pragma unroll
     for (int hd = 0; hd < G; ++hd) {
@@ -351,22 +391,37 @@ template <int G, bool STAGED>
 __device__ __forceinline__ void value_corrections(Smem<G>& S, const float* sc, int cap, int b,
                                                   const Grp& gr, int pp, int tok0, int lane) {
     const Bucket k = bucket_of(S, b, gr, pp, lane);
-    const float gp = S.tokc[k.tg].z;
+    const uint32_t tbo = off_of(S, &S.tab[0][k.tg][0]);
     float pt[G];
 #pragma unroll
     for (int hd = 0; hd < G; ++hd) pt[hd] = (G > 1 && k.vt) ? sc[hd * cap + tok0 + k.tg] : 1.0f;
-    const uint8_t* dcol = &S.dense[k.pg][(k.t >> 3) * 4 + k.c * 512];
+    const uint32_t dcol = off_of(S, &S.dense[k.pg][(k.t >> 3) * 4 + k.c * 512]);
     const uint32_t nsh = (k.t & 7) * 4;
-    int* occ = &S.oci[0][k.c * 64];
+    const uint32_t occ = off_of(S, &S.oci[0][k.c * 64]);
     const int maxc = wave_max_i(k.cnt);
-    auto slot = [&](uint32_t e, bool valid) {
-        const uint32_t jj = e & 63u;
-        const uint32_t n = (*reinterpret_cast<const uint32_t*>(dcol + jj * 8) >> nsh) & 15u;
-        const float delta = entry_delta(S, k.tg, e, n, gp);
-        if (valid) {
+    // Every slot is computed and added; slots past the bucket add zero (no branches).
+    // The loads of a block's slots come first, then its LDS additions, so that the
+    // additions do not serialise the loads behind them.
+    struct Upd {
+        uint32_t addr;
+        int v[G];
+    };
+    auto slot = [&](uint32_t ent, int o, bool valid) {
+        const uint32_t dw = lds_at<uint32_t>(S, dcol | (shr(ent, o - 3) & 0x1f8u));
+        const uint32_t n = __builtin_amdgcn_ubfe(dw, nsh, 4);
+        const float delta = entry_delta(S, tbo, ent, o, n);
+        Upd u;
+        u.addr = occ | (shr(ent, o - 2) & 0xfcu);
 #pragma unroll
-            for (int hd = 0; hd < G; ++hd) atomicAdd(&occ[hd * D + jj], (int)(G == 1 ? delta : pt[hd] * delta));
+        for (int hd = 0; hd < G; ++hd) {
+            const int v = (int)(G == 1 ? delta : pt[hd] * delta);
+            u.v[hd] = valid ? v : 0;
         }
+        return u;
+    };
+    auto apply = [&](const Upd& u) {
+#pragma unroll
+        for (int hd = 0; hd < G; ++hd) atomicAdd(&const_cast<int&>(lds_at<int>(S, u.addr + hd * D * 4)), u.v[hd]);
     };
     if (STAGED) {
         const int pos = S.soff[b][k.pg] + k.st;
@@ -377,14 +432,17 @@ __device__ __forceinline__ void value_corrections(Smem<G>& S, const float* sc, i
             const uint32_t nxt = w[(kk >> 2) + 1];
             const uint32_t ent = __builtin_amdgcn_alignbyte(nxt, cur, sh);
             cur = nxt;
+            Upd u[4];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) slot((ent >> (8 * i)) & 0xffu, kk + i < k.cnt);
+            for (int i = 0; i < 4; ++i) u[i] = slot(ent, 8 * i, kk + i < k.cnt);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) apply(u[i]);
         }
     } else {
         const uint8_t* r = pick4(k.pg, gr.rec[0], gr.rec[1], gr.rec[2], gr.rec[3]);
         const uint8_t* spp = r ? r + LY.sparse + k.st : nullptr;
         for (int kk = 0; kk < maxc; ++kk)
-            if (kk < k.cnt) slot(spp[kk], true);
+            if (kk < k.cnt) apply(slot(spp[kk], 0, true));
     }
 }
 
@@ -418,6 +476,7 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
     uint4 hreg = head_chunk(gc, a.pool, lane);
 
     // ---- query in fp32 and in fixed point -----------------------------------------
+    float ssum[G], sfix[G];
 #pragma unroll
     for (int hd = 0; hd < G; ++hd) {
         const uint16_t* qp = a.q + ((int64_t)s * a.Hq + h * G + hd) * D;
@@ -429,10 +488,9 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
         const int sh = fix_shift(mx);
         S.qi[hd][lane] = (int)rintf(ldexpf(x0, sh));
         S.qi[hd][lane + 64] = (int)rintf(ldexpf(x1, sh));
-        if (lane == 0) {
-            S.qsum[hd] = sum;
-            S.qshift[hd] = sh;
-        }
+        // score = scale * (base * sum(q) + (Delta * U + Gp * H) * 2^-(shift + 7))
+        ssum[hd] = a.scale * sum;
+        sfix[hd] = ldexpf(a.scale, -(sh + 7));
     }
     if (lane < GRP * HCH) *reinterpret_cast<uint4*>(&S.head[0][0][16 * lane]) = hreg;
     wave_sync();
@@ -519,9 +577,8 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
                 const float o = __shfl_xor(v, 16, 64);
                 const int hd = rs * 2 + (grp4 >> 1);
                 if ((grp4 & 1) == 0 && hd < G && pg < gc.npg) {
-                    const int e = S.qshift[hd] + 7;
-                    const float dot = tc.x * S.qsum[hd] + tc.y * ldexpf(v, -e) + tc.z * ldexpf(o, -e);
-                    sc[hd * cap + tok0 + pg * P + t] = (t < nv) ? a.scale * dot : -INFINITY;
+                    const float dot = fmaf(tc.x, ssum[hd], fmaf(tc.y, v, tc.z * o) * sfix[hd]);
+                    sc[hd * cap + tok0 + pg * P + t] = (t < nv) ? dot : -INFINITY;
                 }
             }
         }
@@ -647,7 +704,6 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
             if (gb > 0.0f) frexpf(gb, &ge);
             fsh = gb > 0.0f ? 24 - ge : 0;
             const float ws = ldexpf(w, fsh);
-            S.tokc[lane] = make_float4(T.base, T.dm, ws * T.gp, 0.0f);
             token_table(S, lane, T, ws);
         }
         // next group: heads -> layout -> issue its loads
