@@ -365,12 +365,21 @@ __device__ __forceinline__ void key_corrections(Smem<G>& S, float* sc, int cap, 
         const uint32_t* w = reinterpret_cast<const uint32_t*>(&S.sparse[pos & ~3]);
         const uint32_t sh = pos & 3;
         uint32_t cur = w[0];
-        for (int kk = 0; kk < maxc; kk += 4) {
+        const int full = maxc & ~3;
+        for (int kk = 0; kk < full; kk += 4) {
             const uint32_t nxt = w[(kk >> 2) + 1];
             const uint32_t ent = __builtin_amdgcn_alignbyte(nxt, cur, sh);
             cur = nxt;
 #pragma unroll
             for (int i = 0; i < 4; ++i) slot(ent, 8 * i, kk + i < k.cnt);
+        }
+        // the last 1-3 slots (the wave's longest bucket decides how many)
+        const int rem = maxc - full;
+        if (rem > 0) {
+            const uint32_t ent = __builtin_amdgcn_alignbyte(w[(full >> 2) + 1], cur, sh);
+            slot(ent, 0, full < k.cnt);
+            if (rem > 1) slot(ent, 8, full + 1 < k.cnt);
+            if (rem > 2) slot(ent, 16, full + 2 < k.cnt);
         }
     } else {
         const uint8_t* r = pick4(k.pg, gr.rec[0], gr.rec[1], gr.rec[2], gr.rec[3]);
@@ -428,7 +437,8 @@ __device__ __forceinline__ void value_corrections(Smem<G>& S, const float* sc, i
         const uint32_t* w = reinterpret_cast<const uint32_t*>(&S.sparse[pos & ~3]);
         const uint32_t sh = pos & 3;
         uint32_t cur = w[0];
-        for (int kk = 0; kk < maxc; kk += 4) {
+        const int full = maxc & ~3;
+        for (int kk = 0; kk < full; kk += 4) {
             const uint32_t nxt = w[(kk >> 2) + 1];
             const uint32_t ent = __builtin_amdgcn_alignbyte(nxt, cur, sh);
             cur = nxt;
@@ -437,6 +447,17 @@ __device__ __forceinline__ void value_corrections(Smem<G>& S, const float* sc, i
             for (int i = 0; i < 4; ++i) u[i] = slot(ent, 8 * i, kk + i < k.cnt);
 #pragma unroll
             for (int i = 0; i < 4; ++i) apply(u[i]);
+        }
+        // the last 1-3 slots (the wave's longest bucket decides how many)
+        const int rem = maxc - full;
+        if (rem > 0) {
+            const uint32_t ent = __builtin_amdgcn_alignbyte(w[(full >> 2) + 1], cur, sh);
+            Upd u0 = slot(ent, 0, full < k.cnt), u1 = u0, u2 = u0;
+            if (rem > 1) u1 = slot(ent, 8, full + 1 < k.cnt);
+            if (rem > 2) u2 = slot(ent, 16, full + 2 < k.cnt);
+            apply(u0);
+            if (rem > 1) apply(u1);
+            if (rem > 2) apply(u2);
         }
     } else {
         const uint8_t* r = pick4(k.pg, gr.rec[0], gr.rec[1], gr.rec[2], gr.rec[3]);
