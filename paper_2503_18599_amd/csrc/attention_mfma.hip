@@ -71,9 +71,11 @@ __device__ __forceinline__ v4i mfma(v4i a, v4i b, v4i c) {
     return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
 }
 
-// Value of four base-256 limbs.
+// Value of four base-256 limbs (each |limb sum| < 2^22: the pairs combine exactly in
+// int32 before the two conversions).
 __device__ __forceinline__ float limbs(v4i c) {
-    return fmaf(fmaf(fmaf((float)c[3], 256.f, (float)c[2]), 256.f, (float)c[1]), 256.f, (float)c[0]);
+    const int lo = __mul24(c[1], 256) + c[0], hi = __mul24(c[3], 256) + c[2];
+    return fmaf((float)hi, 65536.0f, (float)lo);
 }
 
 // Wave reductions: a shift-scan within each row of 16 lanes (DPP row_shr 1, 2, 4, 8
@@ -179,8 +181,7 @@ struct Smem {
     int soff[2][GRP + 1];                     // page offsets in the staged group sparse bytes
     __align__(16) uint8_t sparse[SPL + 80];   // + slack for whole-dword reads past a bucket
     __align__(16) float4 tokc[GT];            // base, Delta, Gp of the group's tokens
-    int2 cg[G][GT];                           // fixed-point p*Delta, p*Gp of the group's tokens
-    __align__(16) uint32_t at[G][4][4][4];    // value-pass A operand [head][limb][k-group][feature]
+    __align__(16) uint4 wv[G][GT / 2];        // value-pass weights of token pairs: 4 features, 4 limbs
     float oc[G][D];                           // value corrections
 };
 
@@ -710,8 +711,16 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
                 const float gx = vt ? p * T.gp : 0.0f;
                 if (vt) pb[hd] = fmaf(p, T.base, pb[hd]);
                 const int sh = fix_shift(wave_max(fmaxf(fabsf(cx), fabsf(gx))));
-                S.cg[hd][lane] = make_int2((int)rintf(ldexpf(cx, sh)), (int)rintf(ldexpf(gx, sh)));
                 vsh[hd] = sh;
+                // Weights of token pair lane/2 (even lane: its own C, G and the odd
+                // partner's): 128 (C_e u_e + C_o u_o + G_e h_e + G_o h_o) over the features
+                // (raw byte, low nibble, bits 7|3, bit 3) of the nibble byte, as 4 limbs each.
+                const int ce = (int)rintf(ldexpf(cx, sh)), ge = (int)rintf(ldexpf(gx, sh));
+                const int co = __builtin_amdgcn_update_dpp(0, ce, 0x101, 0xf, 0xf, false);   // row_shl:1
+                const int go = __builtin_amdgcn_update_dpp(0, ge, 0x101, 0xf, 0xf, false);
+                if ((lane & 1) == 0)
+                    S.wv[hd][lane >> 1] = make_uint4(enc(8 * co), enc(128 * ce - 8 * co), enc(-(go + 16 * co)),
+                                                     enc(16 * ge + go + 16 * co));
             }
             // Value corrections accumulate as integers (LDS float atomics are slow): the
             // table is scaled by 2^fsh, chosen so that 64 tokens' largest corrections
@@ -748,32 +757,25 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
         for (int nt = 0; nt < 8; ++nt) gacc[nt] = v4i{0, 0, 0, 0};
 #pragma unroll
         for (int pp = 0; pp < GRP; pp += 2) {
-            // A operand: lane = (limb r, feature f, k-group g4); token pair 4*g4 + bb
+            // A operand of lane (row = 4*head + limb r, k-group g4): for each feature f the
+            // limb-r bytes of token pairs 4*g4 + 0..3 of this page pair (a byte transpose)
             {
-                const int r = lane & 3, f = (lane >> 2) & 3, g4 = lane >> 4;
-                const int al = f == 1 ? 128 : 0;
-                const int be = f == 0 ? 8 : f == 1 ? -8 : f == 2 ? -16 : 16;
-                const int ga = f == 3 ? 16 : 0;
-                const int de = f == 2 ? -1 : f == 3 ? 1 : 0;
-#pragma unroll
-                for (int hd = 0; hd < G; ++hd) {
-                    uint32_t dw = 0;
-#pragma unroll
-                    for (int bb = 0; bb < 4; ++bb) {
-                        const int te = pp * P + 2 * (g4 * 4 + bb);
-                        const int2 ev = S.cg[hd][te], ov = S.cg[hd][te + 1];
-                        const int w = __mul24(al, ev.x) + __mul24(be, ov.x) + __mul24(ga, ev.y) +
-                                      __mul24(de, ov.y);
-                        dw |= byte_of(enc(w), r) << (8 * bb);
-                    }
-                    S.at[hd][r][g4][f] = dw;
-                }
-            }
-            wave_sync();
-            {
-                const int row = lane & 15, hdr = row >> 2, g4 = lane >> 4;
+                const int row = lane & 15, hdr = row >> 2, g4 = lane >> 4, r = row & 3;
                 v4i av = v4i{0, 0, 0, 0};
-                if (hdr < G) av = *reinterpret_cast<const v4i*>(&S.at[hdr][row & 3][g4][0]);
+                if (hdr < G) {
+                    const uint4* wp = &S.wv[hdr][(pp >> 1) * 16 + g4 * 4];
+                    const uint4 w0 = wp[0], w1 = wp[1], w2 = wp[2], w3 = wp[3];
+                    const uint32_t sel = (uint32_t)r | ((uint32_t)(r + 4) << 8);
+                    auto col = [&](uint32_t a0, uint32_t a1, uint32_t a2, uint32_t a3) {
+                        const uint32_t t01 = __builtin_amdgcn_perm(a1, a0, sel);
+                        const uint32_t t23 = __builtin_amdgcn_perm(a3, a2, sel);
+                        return (int)__builtin_amdgcn_perm(t23, t01, 0x05040100u);
+                    };
+                    av[0] = col(w0.x, w1.x, w2.x, w3.x);
+                    av[1] = col(w0.y, w1.y, w2.y, w3.y);
+                    av[2] = col(w0.z, w1.z, w2.z, w3.z);
+                    av[3] = col(w0.w, w1.w, w2.w, w3.w);
+                }
                 const uint8_t* dsrc = &S.dense[pp + (g4 >> 1)][(g4 & 1) * 4];
 #pragma unroll
                 for (int nt = 0; nt < 8; ++nt) {
