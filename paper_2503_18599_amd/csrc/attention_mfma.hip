@@ -44,7 +44,8 @@ constexpr int GRP = 4;                     // pages per group (two correction pa
 constexpr int GT = GRP * P;                // tokens per group
 constexpr int PSTR = 1024;                 // LDS stride of a page's dense bytes
 constexpr int SPCAP = P * D;               // sparse capacity of one record
-constexpr int SPL = 2048;                  // group sparse bytes staged in LDS
+constexpr int SSLOT = 512;                 // staged COO bytes per page (larger pages: read from HBM)
+constexpr int SPL = GRP * SSLOT;           // group sparse bytes staged in LDS
 
 static_assert(LY.meta == 32 && LY.dense == HB && LY.sparse == 1248, "record layout");
 
@@ -178,8 +179,8 @@ struct Smem {
     float m[G], l[G];
     __align__(16) uint8_t head[2][GRP][HB];   // record heads of the current / next group
     int start[2][GRP][P];                     // offset of each slot's COO bytes in its page
-    int soff[2][GRP + 1];                     // page offsets in the staged group sparse bytes
-    __align__(16) uint8_t sparse[SPL + 80];   // + slack for whole-dword reads past a bucket
+    __align__(16) uint8_t sparse[SPL + 80];   // page p's COO bytes at p*SSLOT; + slack for
+                                              // whole-dword reads past a bucket
     __align__(16) float4 tokc[GT];            // base, Delta, Gp of the group's tokens
     __align__(16) uint4 wv[G][GT / 2];        // value-pass weights of token pairs: 4 features, 4 limbs
     float oc[G][D];                           // value corrections
@@ -188,6 +189,7 @@ struct Smem {
 // Wave-uniform description of a group of consecutive pages of one sequence.
 struct Grp {
     const uint8_t* rec[GRP];
+    const uint8_t* base[GRP];   // rec, or a valid stand-in record for missing pages
     int nval[GRP];   // valid slots per page (0 when the page is outside the range)
     int npg;
 };
@@ -208,6 +210,7 @@ __device__ __forceinline__ Grp make_group(const AttnArgs& a, int blk_lane, int p
                 gr.nval[pg] = max(0, min(P, L - (g0 + pg) * P));
             }
         }
+        gr.base[pg] = gr.rec[pg] ? gr.rec[pg] : a.pool;
     }
     return gr;
 }
@@ -220,55 +223,39 @@ __device__ __forceinline__ T pick4(int i, T a0, T a1, T a2, T a3) {
 // Global loads are issued unconditionally, so the compiler never has to merge a loaded
 // and a default value (which would make it wait for the load right away and defeat the
 // prefetch).  Missing pages read a valid stand-in record whose bytes are never used:
-// every consumer masks by the page's valid-slot count.
-__device__ __forceinline__ const uint8_t* or_pool(const uint8_t* r, const uint8_t* pool) {
-    return r ? r : pool;
+// every consumer masks by the page's valid-slot count.  A lane's page is a fixed lane
+// range, so its base pointer is a branch-free select of the group's uniform pointers.
+
+// One 16-byte chunk of the group's record heads: lanes 14p .. 14p+13 read page p; lanes
+// 56..63 re-read chunk 0 of page 3.  hoff = 16 * (lane % 14) for lanes < 56, else 0.
+__device__ __forceinline__ uint4 head_chunk(const Grp& gr, int lane, uint32_t hoff) {
+    const int pg = (lane >= HCH) + (lane >= 2 * HCH) + (lane >= 3 * HCH);
+    return ld16(pick4(pg, gr.base[0], gr.base[1], gr.base[2], gr.base[3]) + hoff);
 }
 
-// One 16-byte chunk of the group's record heads (lanes >= 56 repeat a chunk).
-__device__ __forceinline__ uint4 head_chunk(const Grp& gr, const uint8_t* pool, int lane) {
-    const int c = lane < GRP * HCH ? lane : lane - GRP * HCH;
-    const int pg = c / HCH;
-    const uint8_t* r = or_pool(pick4(pg, gr.rec[0], gr.rec[1], gr.rec[2], gr.rec[3]), pool);
-    return ld16(r + (c % HCH) * 16);
-}
-
-// Sparse offsets of group buffer b from its heads; returns the group's staged size.
+// Start of each slot's COO bytes in its page, from group buffer b's counts.  Returns the
+// COO bytes used by the lane's page (lane >> 4) and whether every page fits its staging
+// slot.
 template <int G>
-__device__ __forceinline__ int group_layout(Smem<G>& S, int b, const Grp& gr, int lane) {
+__device__ __forceinline__ int group_layout(Smem<G>& S, int b, const Grp& gr, int lane, bool& fits) {
     const int pg = lane >> 4, t = lane & 15;
     const int nv = pick4(pg, gr.nval[0], gr.nval[1], gr.nval[2], gr.nval[3]);
     const int tot = (t < nv) ? (int)S.head[b][pg][2 * t] + (int)S.head[b][pg][2 * t + 1] : 0;
     const int incl = row_scan16(tot);
     S.start[b][pg][t] = incl - tot;
-    const int n0 = (min(__builtin_amdgcn_readlane(incl, 15), SPCAP) + 15) & ~15;
-    const int n1 = (min(__builtin_amdgcn_readlane(incl, 31), SPCAP) + 15) & ~15;
-    const int n2 = (min(__builtin_amdgcn_readlane(incl, 47), SPCAP) + 15) & ~15;
-    const int n3 = (min(__builtin_amdgcn_readlane(incl, 63), SPCAP) + 15) & ~15;
-    if (lane == 0) {
-        S.soff[b][0] = 0;
-        S.soff[b][1] = n0;
-        S.soff[b][2] = n0 + n1;
-        S.soff[b][3] = n0 + n1 + n2;
-        S.soff[b][4] = n0 + n1 + n2 + n3;
-    }
-    return n0 + n1 + n2 + n3;
+    const int u0 = __builtin_amdgcn_readlane(incl, 15), u1 = __builtin_amdgcn_readlane(incl, 31);
+    const int u2 = __builtin_amdgcn_readlane(incl, 47), u3 = __builtin_amdgcn_readlane(incl, 63);
+    fits = max(max(u0, u1), max(u2, u3)) <= SSLOT;
+    return lane < 16 ? u0 : lane < 32 ? u1 : lane < 48 ? u2 : u3;
 }
 
-// Loads of a group's used sparse bytes (16-byte chunks `lane` and `lane + 64` of the
-// concatenated, 16-byte padded page streams).  Chunks past the end reload chunk 0.
-__device__ __forceinline__ void sparse_chunks(const Grp& gr, const uint8_t* pool, int total, int s1,
-                                              int s2, int s3, int lane, uint4& r0, uint4& r1) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        int off = 16 * (lane + 64 * i);
-        off = (off < total && total <= SPL) ? off : 0;
-        const int pg = (off >= s1) + (off >= s2) + (off >= s3);
-        const int base = pick4(pg, 0, s1, s2, s3);
-        const uint8_t* r = or_pool(pick4(pg, gr.rec[0], gr.rec[1], gr.rec[2], gr.rec[3]), pool);
-        const uint4 v = ld16(r + LY.sparse + (off - base));
-        if (i == 0) r0 = v; else r1 = v;
-    }
+// The lane's two 16-byte chunks of its page's COO bytes: chunks (lane & 15) and
+// (lane & 15) + 16 of page lane >> 4.  Chunks past the page's used bytes re-read chunk 0.
+__device__ __forceinline__ void sparse_chunks(const Grp& gr, int used, int lane, uint4& r0, uint4& r1) {
+    const uint8_t* r = pick4(lane >> 4, gr.base[0], gr.base[1], gr.base[2], gr.base[3]);
+    const uint32_t o0 = (uint32_t)(lane & 15) * 16u, o1 = o0 + 256u;
+    r0 = ld16(r + LY.sparse + ((int)o0 < used ? o0 : 0u));
+    r1 = ld16(r + LY.sparse + ((int)o1 < used ? o1 : 0u));
 }
 
 // Writes the token's correction table: for COO class cls = COO >> 6 (bit 0 outer,
@@ -362,7 +349,7 @@ __device__ __forceinline__ void key_corrections(Smem<G>& S, float* sc, int cap, 
         }
     };
     if (STAGED) {
-        const int pos = S.soff[b][k.pg] + k.st;
+        const int pos = k.pg * SSLOT + k.st;
         const uint32_t* w = reinterpret_cast<const uint32_t*>(&S.sparse[pos & ~3]);
         const uint32_t sh = pos & 3;
         uint32_t cur = w[0];
@@ -434,7 +421,7 @@ __device__ __forceinline__ void value_corrections(Smem<G>& S, const float* sc, i
         for (int hd = 0; hd < G; ++hd) atomicAdd(&const_cast<int&>(lds_at<int>(S, u.addr + hd * D * 4)), u.v[hd]);
     };
     if (STAGED) {
-        const int pos = S.soff[b][k.pg] + k.st;
+        const int pos = k.pg * SSLOT + k.st;
         const uint32_t* w = reinterpret_cast<const uint32_t*>(&S.sparse[pos & ~3]);
         const uint32_t sh = pos & 3;
         uint32_t cur = w[0];
@@ -495,7 +482,8 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
 
     // the first key group's heads are needed before anything else
     Grp gc = make_group(a, blk_lane, p_begin, p_begin, p_end, L, h, 0);
-    uint4 hreg = head_chunk(gc, a.pool, lane);
+    const uint32_t hoff = lane < GRP * HCH ? (uint32_t)(lane % HCH) * 16u : 0u;
+    uint4 hreg = head_chunk(gc, lane, hoff);
 
     // ---- query in fp32 and in fixed point -----------------------------------------
     float ssum[G], sfix[G];
@@ -553,20 +541,23 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
 
     // ---- pass 1: keys -------------------------------------------------------------
     uint4 dreg[GRP], sreg0, sreg1;
+    const uint32_t koff = (uint32_t)LY.dense + (uint32_t)((lane & 15) * 64 + (lane >> 4) * 16);
+    const uint32_t voff = (uint32_t)LY.dense + (uint32_t)lane * 16u;
+    const uint32_t stg = (uint32_t)((lane >> 4) * SSLOT + (lane & 15) * 16);   // LDS staging slot
+    bool fits_c, fits_n;
     {
-        const int tot = group_layout(S, 0, gc, lane);
+        const int used = group_layout(S, 0, gc, lane, fits_c);
         wave_sync();
 #pragma unroll
-        for (int pg = 0; pg < GRP; ++pg)
-            dreg[pg] = ld16(or_pool(gc.rec[pg], a.pool) + LY.dense + (lane & 15) * 64 + (lane >> 4) * 16);
-        sparse_chunks(gc, a.pool, tot, S.soff[0][1], S.soff[0][2], S.soff[0][3], lane, sreg0, sreg1);
+        for (int pg = 0; pg < GRP; ++pg) dreg[pg] = ld16(gc.base[pg] + koff);
+        sparse_chunks(gc, used, lane, sreg0, sreg1);
     }
     Grp gn = make_group(a, blk_lane, p_begin, p_begin + GRP, p_end, L, h, 0);
-    hreg = head_chunk(gn, a.pool, lane);
+    hreg = head_chunk(gn, lane, hoff);
     int b = 0;
     for (int g0 = p_begin; g0 < p_end; g0 += GRP, b ^= 1) {
         const int tok0 = (g0 - p_begin) * P;
-        const bool staged = S.soff[b][GRP] <= SPL;
+        const bool staged = fits_c;
         // token constants of the group (lane = token) and the key correction tables
         {
             const int pg = lane >> 4, t = lane & 15;
@@ -605,23 +596,22 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
             }
         }
         if (staged) {
-            *reinterpret_cast<uint4*>(&S.sparse[16 * lane]) = sreg0;
-            *reinterpret_cast<uint4*>(&S.sparse[16 * (lane + 64)]) = sreg1;
+            *reinterpret_cast<uint4*>(&S.sparse[stg]) = sreg0;
+            *reinterpret_cast<uint4*>(&S.sparse[stg + 256]) = sreg1;
         }
         // next group: heads -> layout -> issue its dense/sparse and the heads after it
         Grp gnn = gn;
+        fits_n = true;
         if (gn.npg > 0) {
             if (lane < GRP * HCH) *reinterpret_cast<uint4*>(&S.head[b ^ 1][0][16 * lane]) = hreg;
             wave_sync();
-            const int tot = group_layout(S, b ^ 1, gn, lane);
+            const int used = group_layout(S, b ^ 1, gn, lane, fits_n);
             wave_sync();
 #pragma unroll
-            for (int pg = 0; pg < GRP; ++pg)
-                dreg[pg] = ld16(or_pool(gn.rec[pg], a.pool) + LY.dense + (lane & 15) * 64 + (lane >> 4) * 16);
-            sparse_chunks(gn, a.pool, tot, S.soff[b ^ 1][1], S.soff[b ^ 1][2], S.soff[b ^ 1][3], lane,
-                          sreg0, sreg1);
+            for (int pg = 0; pg < GRP; ++pg) dreg[pg] = ld16(gn.base[pg] + koff);
+            sparse_chunks(gn, used, lane, sreg0, sreg1);
             gnn = make_group(a, blk_lane, p_begin, g0 + 2 * GRP, p_end, L, h, 0);
-            hreg = head_chunk(gnn, a.pool, lane);
+            hreg = head_chunk(gnn, lane, hoff);
         }
         wave_sync();
         // sparse part
@@ -635,11 +625,12 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
         wave_sync();
         gc = gn;
         gn = gnn;
+        fits_c = fits_n;
     }
 
     // the first value group's heads go out before the softmax
     gc = make_group(a, blk_lane, p_begin, p_begin, p_end, L, h, 1);
-    hreg = head_chunk(gc, a.pool, lane);
+    hreg = head_chunk(gc, lane, hoff);
 
     // ---- softmax over the range ----------------------------------------------------
 #pragma unroll
@@ -675,23 +666,23 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
 #pragma unroll
     for (int hd = 0; hd < G; ++hd) pb[hd] = 0.0f;
     {
-        const int tot = group_layout(S, 0, gc, lane);
+        const int used = group_layout(S, 0, gc, lane, fits_c);
         wave_sync();
 #pragma unroll
-        for (int pg = 0; pg < GRP; ++pg) dreg[pg] = ld16(or_pool(gc.rec[pg], a.pool) + LY.dense + lane * 16);
-        sparse_chunks(gc, a.pool, tot, S.soff[0][1], S.soff[0][2], S.soff[0][3], lane, sreg0, sreg1);
+        for (int pg = 0; pg < GRP; ++pg) dreg[pg] = ld16(gc.base[pg] + voff);
+        sparse_chunks(gc, used, lane, sreg0, sreg1);
     }
     gn = make_group(a, blk_lane, p_begin, p_begin + GRP, p_end, L, h, 1);
-    hreg = head_chunk(gn, a.pool, lane);
+    hreg = head_chunk(gn, lane, hoff);
     b = 0;
     for (int g0 = p_begin; g0 < p_end; g0 += GRP, b ^= 1) {
         const int tok0 = (g0 - p_begin) * P;
-        const bool staged = S.soff[b][GRP] <= SPL;
+        const bool staged = fits_c;
 #pragma unroll
         for (int pg = 0; pg < GRP; ++pg) *reinterpret_cast<uint4*>(&S.dense[pg][lane * 16]) = dreg[pg];
         if (staged) {
-            *reinterpret_cast<uint4*>(&S.sparse[16 * lane]) = sreg0;
-            *reinterpret_cast<uint4*>(&S.sparse[16 * (lane + 64)]) = sreg1;
+            *reinterpret_cast<uint4*>(&S.sparse[stg]) = sreg0;
+            *reinterpret_cast<uint4*>(&S.sparse[stg + 256]) = sreg1;
         }
         // fixed-point coefficients p*Delta, p*Gp of the group's tokens (lane = token), one
         // shift per head; correction tables (scaled by p when one head reads them)
@@ -738,18 +729,17 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
         }
         // next group: heads -> layout -> issue its loads
         Grp gnn = gn;
+        fits_n = true;
         if (gn.npg > 0) {
             if (lane < GRP * HCH) *reinterpret_cast<uint4*>(&S.head[b ^ 1][0][16 * lane]) = hreg;
             wave_sync();
-            const int tot = group_layout(S, b ^ 1, gn, lane);
+            const int used = group_layout(S, b ^ 1, gn, lane, fits_n);
             wave_sync();
 #pragma unroll
-            for (int pg = 0; pg < GRP; ++pg)
-                dreg[pg] = ld16(or_pool(gn.rec[pg], a.pool) + LY.dense + lane * 16);
-            sparse_chunks(gn, a.pool, tot, S.soff[b ^ 1][1], S.soff[b ^ 1][2], S.soff[b ^ 1][3], lane,
-                          sreg0, sreg1);
+            for (int pg = 0; pg < GRP; ++pg) dreg[pg] = ld16(gn.base[pg] + voff);
+            sparse_chunks(gn, used, lane, sreg0, sreg1);
             gnn = make_group(a, blk_lane, p_begin, g0 + 2 * GRP, p_end, L, h, 1);
-            hreg = head_chunk(gnn, a.pool, lane);
+            hreg = head_chunk(gnn, lane, hoff);
         }
         wave_sync();
         v4i gacc[8];
@@ -805,6 +795,7 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
         }
         gc = gn;
         gn = gnn;
+        fits_c = fits_n;
     }
 
 #pragma unroll
