@@ -103,6 +103,18 @@ __device__ __forceinline__ float wave_max(float v) {
 __device__ __forceinline__ float wave_sum(float v) {
     return wave_reduce(v, 0.0f, [](float a, float b) { return a + b; });
 }
+// Maximum of non-negative floats (their bit patterns order as unsigned integers); lanes
+// shifted in from outside a row read 0.
+__device__ __forceinline__ float wave_max_nonneg(float v) {
+    uint32_t x = __builtin_bit_cast(uint32_t, v);
+    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, true));
+    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, true));
+    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, true));
+    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, true));
+    const uint32_t r = max(max((uint32_t)__builtin_amdgcn_readlane((int)x, 15), (uint32_t)__builtin_amdgcn_readlane((int)x, 31)),
+                           max((uint32_t)__builtin_amdgcn_readlane((int)x, 47), (uint32_t)__builtin_amdgcn_readlane((int)x, 63)));
+    return __builtin_bit_cast(float, r);
+}
 __device__ __forceinline__ int wave_max_i(int v) {
     return wave_reduce(v, (int)0x80000000, [](int a, int b) { return max(a, b); });
 }
@@ -493,7 +505,7 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
         const float x0 = h2f(qp[lane]), x1 = h2f(qp[lane + 64]);
         S.q[hd][lane] = x0;
         S.q[hd][lane + 64] = x1;
-        const float mx = wave_max(fmaxf(fabsf(x0), fabsf(x1)));
+        const float mx = wave_max_nonneg(fmaxf(fabsf(x0), fabsf(x1)));
         const float sum = wave_sum(x0 + x1);
         const int sh = fix_shift(mx);
         S.qi[hd][lane] = (int)rintf(ldexpf(x0, sh));
@@ -566,32 +578,47 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
             token_table(S, lane, T, 1.0f);
         }
         wave_sync();
-        // dense part on the matrix cores; stage the group in LDS
+        // dense part on the matrix cores: one accumulator per page and the pages' MFMAs
+        // interleaved, so that no MFMA waits on the one before it; stage the group in LDS
+        {
+            v4i acc[GRP][NRS];
 #pragma unroll
-        for (int pg = 0; pg < GRP; ++pg) {
-            const uint4 dv = dreg[pg];
-            v4i acc[NRS];
+            for (int pg = 0; pg < GRP; ++pg)
 #pragma unroll
-            for (int rs = 0; rs < NRS; ++rs) acc[rs] = v4i{0, 0, 0, 0};
+                for (int rs = 0; rs < NRS; ++rs) acc[pg][rs] = v4i{0, 0, 0, 0};
 #pragma unroll
             for (int m = 0; m < 4; ++m) {
-                const uint32_t dw = m == 0 ? dv.x : m == 1 ? dv.y : m == 2 ? dv.z : dv.w;
-                const v4i B = features(dw);
 #pragma unroll
-                for (int rs = 0; rs < NRS; ++rs) acc[rs] = mfma(afk[rs][m], B, acc[rs]);
+                for (int pg = 0; pg < GRP; ++pg) {
+                    const uint4 dv = dreg[pg];
+                    const v4i B = features(m == 0 ? dv.x : m == 1 ? dv.y : m == 2 ? dv.z : dv.w);
+#pragma unroll
+                    for (int rs = 0; rs < NRS; ++rs) acc[pg][rs] = mfma(afk[rs][m], B, acc[pg][rs]);
+                }
             }
-            *reinterpret_cast<uint4*>(&S.dense[pg][(lane & 15) * 64 + (lane >> 4) * 16]) = dv;
-            const int t = lane & 15, grp4 = lane >> 4;
-            const float4 tc = S.tokc[pg * P + t];
-            const int nv = gc.nval[pg];
 #pragma unroll
-            for (int rs = 0; rs < NRS; ++rs) {
-                const float v = limbs(acc[rs]);
-                const float o = __shfl_xor(v, 16, 64);
-                const int hd = rs * 2 + (grp4 >> 1);
-                if ((grp4 & 1) == 0 && hd < G && pg < gc.npg) {
-                    const float dot = fmaf(tc.x, ssum[hd], fmaf(tc.y, v, tc.z * o) * sfix[hd]);
-                    sc[hd * cap + tok0 + pg * P + t] = (t < nv) ? dot : -INFINITY;
+            for (int pg = 0; pg < GRP; ++pg)
+                *reinterpret_cast<uint4*>(&S.dense[pg][(lane & 15) * 64 + (lane >> 4) * 16]) = dreg[pg];
+            // Lane (t + 16*grp4) holds rows 4*grp4 .. 4*grp4+3 of column t: the U (grp4
+            // even) or H (grp4 odd) limbs of head rs*2 + grp4/2.  Rows 1 and 3 reach rows 0
+            // and 2 by a row swap.
+            const int t = lane & 15, grp4 = lane >> 4;
+            const bool hi = (grp4 >> 1) != 0;
+#pragma unroll
+            for (int pg = 0; pg < GRP; ++pg) {
+                const float4 tc = S.tokc[pg * P + t];
+                const bool valid = t < gc.nval[pg];
+#pragma unroll
+                for (int rs = 0; rs < NRS; ++rs) {
+                    const float v = limbs(acc[pg][rs]);
+                    const int vb = __builtin_bit_cast(int, v);
+                    const float o = __builtin_bit_cast(float, (int)__builtin_amdgcn_permlane16_swap(vb, vb, false, false)[1]);
+                    const int hd = rs * 2 + (hi ? 1 : 0);
+                    const float s1 = hi ? ssum[min(rs * 2 + 1, G - 1)] : ssum[rs * 2];
+                    const float s2 = hi ? sfix[min(rs * 2 + 1, G - 1)] : sfix[rs * 2];
+                    const float dot = fmaf(tc.x, s1, fmaf(tc.y, v, tc.z * o) * s2);
+                    if ((grp4 & 1) == 0 && hd < G && pg < gc.npg)
+                        sc[hd * cap + tok0 + pg * P + t] = valid ? dot : -INFINITY;
                 }
             }
         }
@@ -701,7 +728,7 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
                 const float cx = vt ? p * T.dm : 0.0f;
                 const float gx = vt ? p * T.gp : 0.0f;
                 if (vt) pb[hd] = fmaf(p, T.base, pb[hd]);
-                const int sh = fix_shift(wave_max(fmaxf(fabsf(cx), fabsf(gx))));
+                const int sh = fix_shift(wave_max_nonneg(fmaxf(fabsf(cx), fabsf(gx))));
                 vsh[hd] = sh;
                 // Weights of token pair lane/2 (even lane: its own C, G and the odd
                 // partner's): 128 (C_e u_e + C_o u_o + G_e h_e + G_o h_o) over the features
@@ -717,10 +744,12 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
             // table is scaled by 2^fsh, chosen so that 64 tokens' largest corrections
             // stay below 2^30 in magnitude.
             const float w = vt ? (G == 1 ? p0 : 1.0f) : 0.0f;
-            const float bound = w * (fmaxf(fmaxf(fabsf(T.b_il - T.base), fabsf(T.b_ol - T.base)),
-                                           fmaxf(fabsf(T.b_ih - T.base), fabsf(T.b_oh - T.base))) +
-                                     15.0f * fmaxf(fabsf(T.kd_i), fabsf(T.kd_o)) + fabsf(T.gp));
-            const float gb = wave_max(bound);
+            // (invalid tokens' metadata is arbitrary: they contribute 0, never NaN)
+            const float bound = vt ? w * (fmaxf(fmaxf(fabsf(T.b_il - T.base), fabsf(T.b_ol - T.base)),
+                                                fmaxf(fabsf(T.b_ih - T.base), fabsf(T.b_oh - T.base))) +
+                                          15.0f * fmaxf(fabsf(T.kd_i), fabsf(T.kd_o)) + fabsf(T.gp))
+                                   : 0.0f;
+            const float gb = wave_max_nonneg(bound);
             int ge = 0;
             if (gb > 0.0f) frexpf(gb, &ge);
             fsh = gb > 0.0f ? 24 - ge : 0;
