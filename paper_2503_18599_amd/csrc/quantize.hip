@@ -26,16 +26,38 @@ __device__ inline uint16_t float_to_half_bits(float f) {
     return __half_as_ushort(__float2half_rn(f));
 }
 
+// Wave reductions: a DPP shift-scan within each row of 16 lanes leaves the row's result
+// in its lane 15; the four row results combine through readlane (no LDS round trips).
+template <typename Op>
+__device__ inline float wave_reduce(float v, float ident, Op op) {
+    const int id = __float_as_int(ident);
+    v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(id, __float_as_int(v), 0x111, 0xf, 0xf, false)));
+    v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(id, __float_as_int(v), 0x112, 0xf, 0xf, false)));
+    v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(id, __float_as_int(v), 0x114, 0xf, 0xf, false)));
+    v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(id, __float_as_int(v), 0x118, 0xf, 0xf, false)));
+    const int x = __float_as_int(v);
+    return op(op(__int_as_float(__builtin_amdgcn_readlane(x, 15)), __int_as_float(__builtin_amdgcn_readlane(x, 31))),
+              op(__int_as_float(__builtin_amdgcn_readlane(x, 47)), __int_as_float(__builtin_amdgcn_readlane(x, 63))));
+}
+
 __device__ inline float wave_min(float v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v = fminf(v, __shfl_xor(v, o, 64));
-    return v;
+    return wave_reduce(v, INFINITY, [](float p, float q) { return fminf(p, q); });
 }
 
 __device__ inline float wave_max(float v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-    return v;
+    return wave_reduce(v, -INFINITY, [](float p, float q) { return fmaxf(p, q); });
+}
+
+// Inclusive prefix sum over the wave (DPP row scan, then the rows' totals).
+__device__ inline int wave_incl_scan(int x, int lane) {
+    x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false);
+    x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false);
+    x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false);
+    x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false);
+    const int r0 = __builtin_amdgcn_readlane(x, 15), r1 = __builtin_amdgcn_readlane(x, 31);
+    const int r2 = __builtin_amdgcn_readlane(x, 47);
+    const int row = lane >> 4;
+    return x + (row == 0 ? 0 : row == 1 ? r0 : row == 2 ? r0 + r1 : r0 + r1 + r2);
 }
 
 template <int D>
@@ -45,6 +67,7 @@ __global__ __launch_bounds__(1024) void quantize_kernel(QuantArgs a) {
 
     __shared__ uint8_t s_counts[kPage][NC];
     __shared__ uint8_t s_vnib[kPage][D];
+    __shared__ __align__(16) uint8_t s_krow[kPage][D / 2];
 
     const int s = blockIdx.y;
     const int h = blockIdx.z >> 1;
@@ -137,12 +160,21 @@ __global__ __launch_bounds__(1024) void quantize_kernel(QuantArgs a) {
     }
     __syncthreads();
 
-    if (active) {
-        // sparse start of this slot: counts of earlier slots (older ones live in the record)
-        int base = 0;
-        for (int t = 0; t < slot; ++t)
+    // sparse start of this slot: the counts of the earlier slots (slots before this call's
+    // first one live in the record), as a prefix sum with lane = slot
+    int base = 0;
+    {
+        int cnt = 0;
+        if (lane < kPage) {
+#pragma unroll
             for (int c = 0; c < NC; ++c)
-                base += (t < slot0) ? rec[LY.counts + t * NC + c] : s_counts[t][c];
+                cnt += (lane < slot0) ? rec[LY.counts + lane * NC + c]
+                                      : (lane < slot0 + nslots ? s_counts[lane][c] : 0);
+        }
+        const int incl = wave_incl_scan(cnt, lane);
+        base = __shfl(incl - cnt, slot < kPage ? slot : 0, 64);
+    }
+    if (active) {
         const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
         int off = base;
 #pragma unroll
@@ -161,12 +193,12 @@ __global__ __launch_bounds__(1024) void quantize_kernel(QuantArgs a) {
             *reinterpret_cast<uint16_t*>(rec + LY.meta + slot * 12 + lane * 2) = hb;
         }
         if (which == 0) {
-            // K: token-major, element j at byte slot*D/2 + j/2, low nibble = even j
+            // K: token-major, element j at byte slot*D/2 + j/2, low nibble = even j; the
+            // row is assembled in LDS and leaves in dwords below
 #pragma unroll
             for (int c = 0; c < NC; ++c) {
-                const int hi_n = __shfl_down((int)nib[c], 1, 64);
-                if ((lane & 1) == 0)
-                    rec[LY.dense + slot * (D / 2) + (c * 64 + lane) / 2] = (uint8_t)(nib[c] | (hi_n << 4));
+                const int hi_n = __builtin_amdgcn_update_dpp(0, (int)nib[c], 0x101, 0xf, 0xf, false);   // lane + 1
+                if ((lane & 1) == 0) s_krow[slot][(c * 64 + lane) / 2] = (uint8_t)(nib[c] | (hi_n << 4));
             }
         } else {
 #pragma unroll
@@ -175,13 +207,19 @@ __global__ __launch_bounds__(1024) void quantize_kernel(QuantArgs a) {
     }
     __syncthreads();
 
-    if (which == 1) {
-        // V: channel-major, element j of slot t at byte j*P/2 + t/2, low nibble = even t.
+    if (which == 0) {
+        // K rows of this call's slots: one contiguous, 4-byte aligned range
+        const uint32_t* src = reinterpret_cast<const uint32_t*>(&s_krow[slot0][0]);
+        uint32_t* dst = reinterpret_cast<uint32_t*>(rec + LY.dense + slot0 * (D / 2));
+        for (int i = threadIdx.x; i < nslots * (D / 8); i += blockDim.x) dst[i] = src[i];
+    } else {
+        // V: channel-major, element j of slot t at byte j*P/2 + t/2, low nibble = even t;
+        // consecutive threads write consecutive bytes of a channel row.
         const int p_lo = slot0 >> 1, p_hi = (slot0 + nslots - 1) >> 1;
         const int npairs = p_hi - p_lo + 1;
         for (int i = threadIdx.x; i < npairs * D; i += blockDim.x) {
-            const int j = i % D;
-            const int p = p_lo + i / D;
+            const int j = i / npairs;
+            const int p = p_lo + i % npairs;
             const int te = 2 * p, to = 2 * p + 1;
             const bool has_e = te >= slot0 && te < slot0 + nslots;
             const bool has_o = to >= slot0 && to < slot0 + nslots;
