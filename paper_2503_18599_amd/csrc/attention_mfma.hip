@@ -332,82 +332,122 @@ __device__ __forceinline__ uint32_t off_of(const Smem<G>& S, const void* p) {
     return (uint32_t)(reinterpret_cast<const char*>(p) - reinterpret_cast<const char*>(&S));
 }
 
-// Walks each lane's bucket and adds every entry's q-weighted correction (true value
-// minus middle reading) to its token's score.  Staged entries are read four at a time
-// from one aligned dword pair; the four corrections of a block are independent, and
-// entries past the bucket contribute zero.
-template <int G, bool STAGED>
+// Walks each lane's buckets and adds every entry's q-weighted correction (true value
+// minus middle reading) to its token's score.  A lane owns NB buckets, one in each of
+// the page pairs pp0, pp0 + 2, ..., walked side by side so that their LDS loads overlap.
+// Staged entries are read four at a time from one aligned dword pair, one block ahead of
+// their use; the corrections of a block are independent, and entries past a bucket
+// contribute zero.
+template <int G, bool STAGED, int NB>
 __device__ __forceinline__ void key_corrections(Smem<G>& S, float* sc, int cap, float scale, int b,
-                                                const Grp& gr, int pp, int tok0, int lane) {
-    const Bucket k = bucket_of(S, b, gr, pp, lane);
-    const uint32_t tbo = off_of(S, &S.tab[0][k.tg][0]);
-    const uint32_t drow = off_of(S, &S.dense[k.pg][k.t * 64 + k.c * 32]);
-    const uint32_t qc = off_of(S, &S.q[0][k.c * 64]);
-    float corr[G];
+                                                const Grp& gr, int pp0, int tok0, int lane) {
+    Bucket k[NB];
+    uint32_t tbo[NB], drow[NB];
+    float corr[NB][G];
+    int mc = 0;
 #pragma unroll
-    for (int hd = 0; hd < G; ++hd) corr[hd] = 0.0f;
-    const int maxc = wave_max_i(k.cnt);
+    for (int nb = 0; nb < NB; ++nb) {
+        k[nb] = bucket_of(S, b, gr, pp0 + 2 * nb, lane);
+        tbo[nb] = off_of(S, &S.tab[0][k[nb].tg][0]);
+        drow[nb] = off_of(S, &S.dense[k[nb].pg][k[nb].t * 64 + k[nb].c * 32]);
+        mc = max(mc, k[nb].cnt);
+#pragma unroll
+        for (int hd = 0; hd < G; ++hd) corr[nb][hd] = 0.0f;
+    }
+    const uint32_t qc = off_of(S, &S.q[0][((lane >> 4) & 1) * 64]);
+    const int maxc = wave_max_i(mc);
     // The entry in bits o..o+7 of ent: index j (6 bits), class (2 bits).  Every slot is
     // computed; slots past the bucket get a zero weight (no branches).
-    auto slot = [&](uint32_t ent, int o, bool valid) {
-        const uint32_t dw = lds_at<uint32_t>(S, drow | (shr(ent, o + 1) & 0x1cu));
+    auto slot = [&](int nb, uint32_t ent, int o, bool valid) {
+        const uint32_t dw = lds_at<uint32_t>(S, drow[nb] | (shr(ent, o + 1) & 0x1cu));
         const uint32_t n = __builtin_amdgcn_ubfe(dw, ((ent >> o) & 0xffu) << 2, 4);
-        const float delta = entry_delta(S, tbo, ent, o, n);
+        const float delta = entry_delta(S, tbo[nb], ent, o, n);
         const uint32_t qo = qc | (shr(ent, o - 2) & 0xfcu);
 #pragma unroll
         for (int hd = 0; hd < G; ++hd) {
             const float q = lds_at<float>(S, qo + hd * D * 4);
-            corr[hd] = fmaf(valid ? q : 0.0f, delta, corr[hd]);
+            corr[nb][hd] = fmaf(valid ? q : 0.0f, delta, corr[nb][hd]);
         }
     };
     if (STAGED) {
-        const int pos = k.pg * SSLOT + k.st;
-        const uint32_t* w = reinterpret_cast<const uint32_t*>(&S.sparse[pos & ~3]);
-        const uint32_t sh = pos & 3;
-        uint32_t cur = w[0];
+        const uint32_t* w[NB];
+        uint32_t sh[NB], cur[NB], nxt[NB], ent[NB];
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+            const int pos = k[nb].pg * SSLOT + k[nb].st;
+            w[nb] = reinterpret_cast<const uint32_t*>(&S.sparse[pos & ~3]);
+            sh[nb] = pos & 3;
+            cur[nb] = w[nb][0];
+            nxt[nb] = w[nb][1];
+        }
         const int full = maxc & ~3;
         for (int kk = 0; kk < full; kk += 4) {
-            const uint32_t nxt = w[(kk >> 2) + 1];
-            const uint32_t ent = __builtin_amdgcn_alignbyte(nxt, cur, sh);
-            cur = nxt;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) slot(ent, 8 * i, kk + i < k.cnt);
+            for (int nb = 0; nb < NB; ++nb) {
+                ent[nb] = __builtin_amdgcn_alignbyte(nxt[nb], cur[nb], sh[nb]);
+                cur[nb] = nxt[nb];
+                nxt[nb] = w[nb][(kk >> 2) + 2];
+            }
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) slot(nb, ent[nb], 8 * i, kk + i < k[nb].cnt);
         }
         // the last 1-3 slots (the wave's longest bucket decides how many)
         const int rem = maxc - full;
         if (rem > 0) {
-            const uint32_t ent = __builtin_amdgcn_alignbyte(w[(full >> 2) + 1], cur, sh);
-            slot(ent, 0, full < k.cnt);
-            if (rem > 1) slot(ent, 8, full + 1 < k.cnt);
-            if (rem > 2) slot(ent, 16, full + 2 < k.cnt);
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) {
+                ent[nb] = __builtin_amdgcn_alignbyte(nxt[nb], cur[nb], sh[nb]);
+                slot(nb, ent[nb], 0, full < k[nb].cnt);
+            }
+            if (rem > 1)
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb) slot(nb, ent[nb], 8, full + 1 < k[nb].cnt);
+            if (rem > 2)
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb) slot(nb, ent[nb], 16, full + 2 < k[nb].cnt);
         }
     } else {
-        const uint8_t* r = pick4(k.pg, gr.rec[0], gr.rec[1], gr.rec[2], gr.rec[3]);
-        const uint8_t* spp = r ? r + LY.sparse + k.st : nullptr;
-        for (int kk = 0; kk < maxc; ++kk)
-            if (kk < k.cnt) slot(spp[kk], 0, true);
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+            const uint8_t* r = pick4(k[nb].pg, gr.rec[0], gr.rec[1], gr.rec[2], gr.rec[3]);
+            const uint8_t* spp = r ? r + LY.sparse + k[nb].st : nullptr;
+            for (int kk = 0; kk < maxc; ++kk)
+                if (kk < k[nb].cnt) slot(nb, spp[kk], 0, true);
+        }
     }
 #pragma unroll
-    for (int hd = 0; hd < G; ++hd) {
-        const float o = corr[hd] + __shfl_xor(corr[hd], 16, 64);
-        if (k.c == 0 && k.vt) sc[hd * cap + tok0 + k.tg] += scale * o;
-    }
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int hd = 0; hd < G; ++hd) {
+            const float o = corr[nb][hd] + __shfl_xor(corr[nb][hd], 16, 64);
+            if (k[nb].c == 0 && k[nb].vt) sc[hd * cap + tok0 + k[nb].tg] += scale * o;
+        }
 }
 
 // Same walk for values: each entry adds p_t * (true value - middle reading) to its
 // channel.  With one head the probability is already folded into the table and Gp.
-template <int G, bool STAGED>
+template <int G, bool STAGED, int NB>
 __device__ __forceinline__ void value_corrections(Smem<G>& S, const float* sc, int cap, int b,
-                                                  const Grp& gr, int pp, int tok0, int lane) {
-    const Bucket k = bucket_of(S, b, gr, pp, lane);
-    const uint32_t tbo = off_of(S, &S.tab[0][k.tg][0]);
-    float pt[G];
+                                                  const Grp& gr, int pp0, int tok0, int lane) {
+    Bucket k[NB];
+    uint32_t tbo[NB], dcol[NB];
+    float pt[NB][G];
+    int mc = 0;
 #pragma unroll
-    for (int hd = 0; hd < G; ++hd) pt[hd] = (G > 1 && k.vt) ? sc[hd * cap + tok0 + k.tg] : 1.0f;
-    const uint32_t dcol = off_of(S, &S.dense[k.pg][(k.t >> 3) * 4 + k.c * 512]);
-    const uint32_t nsh = (k.t & 7) * 4;
-    const uint32_t occ = off_of(S, &S.oci[0][k.c * 64]);
-    const int maxc = wave_max_i(k.cnt);
+    for (int nb = 0; nb < NB; ++nb) {
+        k[nb] = bucket_of(S, b, gr, pp0 + 2 * nb, lane);
+        tbo[nb] = off_of(S, &S.tab[0][k[nb].tg][0]);
+        dcol[nb] = off_of(S, &S.dense[k[nb].pg][(k[nb].t >> 3) * 4 + k[nb].c * 512]);
+        mc = max(mc, k[nb].cnt);
+#pragma unroll
+        for (int hd = 0; hd < G; ++hd)
+            pt[nb][hd] = (G > 1 && k[nb].vt) ? sc[hd * cap + tok0 + k[nb].tg] : 1.0f;
+    }
+    const uint32_t nsh = (lane & 7) * 4;
+    const uint32_t occ = off_of(S, &S.oci[0][((lane >> 4) & 1) * 64]);
+    const int maxc = wave_max_i(mc);
     // Every slot is computed and added; slots past the bucket add zero (no branches).
     // The loads of a block's slots come first, then its LDS additions, so that the
     // additions do not serialise the loads behind them.
@@ -415,15 +455,15 @@ __device__ __forceinline__ void value_corrections(Smem<G>& S, const float* sc, i
         uint32_t addr;
         int v[G];
     };
-    auto slot = [&](uint32_t ent, int o, bool valid) {
-        const uint32_t dw = lds_at<uint32_t>(S, dcol | (shr(ent, o - 3) & 0x1f8u));
+    auto slot = [&](int nb, uint32_t ent, int o, bool valid) {
+        const uint32_t dw = lds_at<uint32_t>(S, dcol[nb] | (shr(ent, o - 3) & 0x1f8u));
         const uint32_t n = __builtin_amdgcn_ubfe(dw, nsh, 4);
-        const float delta = entry_delta(S, tbo, ent, o, n);
+        const float delta = entry_delta(S, tbo[nb], ent, o, n);
         Upd u;
         u.addr = occ | (shr(ent, o - 2) & 0xfcu);
 #pragma unroll
         for (int hd = 0; hd < G; ++hd) {
-            const int v = (int)(G == 1 ? delta : pt[hd] * delta);
+            const int v = (int)(G == 1 ? delta : pt[nb][hd] * delta);
             u.v[hd] = valid ? v : 0;
         }
         return u;
@@ -433,37 +473,62 @@ __device__ __forceinline__ void value_corrections(Smem<G>& S, const float* sc, i
         for (int hd = 0; hd < G; ++hd) atomicAdd(&const_cast<int&>(lds_at<int>(S, u.addr + hd * D * 4)), u.v[hd]);
     };
     if (STAGED) {
-        const int pos = k.pg * SSLOT + k.st;
-        const uint32_t* w = reinterpret_cast<const uint32_t*>(&S.sparse[pos & ~3]);
-        const uint32_t sh = pos & 3;
-        uint32_t cur = w[0];
+        const uint32_t* w[NB];
+        uint32_t sh[NB], cur[NB], nxt[NB], ent[NB];
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+            const int pos = k[nb].pg * SSLOT + k[nb].st;
+            w[nb] = reinterpret_cast<const uint32_t*>(&S.sparse[pos & ~3]);
+            sh[nb] = pos & 3;
+            cur[nb] = w[nb][0];
+            nxt[nb] = w[nb][1];
+        }
         const int full = maxc & ~3;
         for (int kk = 0; kk < full; kk += 4) {
-            const uint32_t nxt = w[(kk >> 2) + 1];
-            const uint32_t ent = __builtin_amdgcn_alignbyte(nxt, cur, sh);
-            cur = nxt;
-            Upd u[4];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) u[i] = slot(ent, 8 * i, kk + i < k.cnt);
+            for (int nb = 0; nb < NB; ++nb) {
+                ent[nb] = __builtin_amdgcn_alignbyte(nxt[nb], cur[nb], sh[nb]);
+                cur[nb] = nxt[nb];
+                nxt[nb] = w[nb][(kk >> 2) + 2];
+            }
+            Upd u[NB][4];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) apply(u[i]);
+            for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) u[nb][i] = slot(nb, ent[nb], 8 * i, kk + i < k[nb].cnt);
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) apply(u[nb][i]);
         }
         // the last 1-3 slots (the wave's longest bucket decides how many)
         const int rem = maxc - full;
         if (rem > 0) {
-            const uint32_t ent = __builtin_amdgcn_alignbyte(w[(full >> 2) + 1], cur, sh);
-            Upd u0 = slot(ent, 0, full < k.cnt), u1 = u0, u2 = u0;
-            if (rem > 1) u1 = slot(ent, 8, full + 1 < k.cnt);
-            if (rem > 2) u2 = slot(ent, 16, full + 2 < k.cnt);
-            apply(u0);
-            if (rem > 1) apply(u1);
-            if (rem > 2) apply(u2);
+            Upd u[NB][3];
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) {
+                ent[nb] = __builtin_amdgcn_alignbyte(nxt[nb], cur[nb], sh[nb]);
+                u[nb][0] = slot(nb, ent[nb], 0, full < k[nb].cnt);
+                u[nb][1] = u[nb][0];
+                u[nb][2] = u[nb][0];
+                if (rem > 1) u[nb][1] = slot(nb, ent[nb], 8, full + 1 < k[nb].cnt);
+                if (rem > 2) u[nb][2] = slot(nb, ent[nb], 16, full + 2 < k[nb].cnt);
+            }
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) {
+                apply(u[nb][0]);
+                if (rem > 1) apply(u[nb][1]);
+                if (rem > 2) apply(u[nb][2]);
+            }
         }
     } else {
-        const uint8_t* r = pick4(k.pg, gr.rec[0], gr.rec[1], gr.rec[2], gr.rec[3]);
-        const uint8_t* spp = r ? r + LY.sparse + k.st : nullptr;
-        for (int kk = 0; kk < maxc; ++kk)
-            if (kk < k.cnt) apply(slot(spp[kk], 0, true));
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+            const uint8_t* r = pick4(k[nb].pg, gr.rec[0], gr.rec[1], gr.rec[2], gr.rec[3]);
+            const uint8_t* spp = r ? r + LY.sparse + k[nb].st : nullptr;
+            for (int kk = 0; kk < maxc; ++kk)
+                if (kk < k[nb].cnt) apply(slot(nb, spp[kk], 0, true));
+        }
     }
 }
 
@@ -642,13 +707,10 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
         }
         wave_sync();
         // sparse part
-#pragma unroll
-        for (int pp = 0; pp < GRP; pp += 2) {
-            if (staged)
-                key_corrections<G, true>(S, sc, cap, a.scale, b, gc, pp, tok0, lane);
-            else
-                key_corrections<G, false>(S, sc, cap, a.scale, b, gc, pp, tok0, lane);
-        }
+        if (staged)
+            key_corrections<G, true, GRP / 2>(S, sc, cap, a.scale, b, gc, 0, tok0, lane);
+        else
+            key_corrections<G, false, GRP / 2>(S, sc, cap, a.scale, b, gc, 0, tok0, lane);
         wave_sync();
         gc = gn;
         gn = gnn;
@@ -803,12 +865,12 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
                     gacc[nt] = mfma(av, features(dw), gacc[nt]);
                 }
             }
-            if (staged)
-                value_corrections<G, true>(S, sc, cap, b, gc, pp, tok0, lane);
-            else
-                value_corrections<G, false>(S, sc, cap, b, gc, pp, tok0, lane);
-            wave_sync();
         }
+        if (staged)
+            value_corrections<G, true, GRP / 2>(S, sc, cap, b, gc, 0, tok0, lane);
+        else
+            value_corrections<G, false, GRP / 2>(S, sc, cap, b, gc, 0, tok0, lane);
+        wave_sync();
         // fold the group's integer sums into the fp32 outputs
 #pragma unroll
         for (int hd = 0; hd < G; ++hd) {
