@@ -162,14 +162,16 @@ __device__ __forceinline__ Tok token_consts(const uint8_t* meta, const float* th
     return T;
 }
 
-// The kernel runs one wave per workgroup.  LDS operations of a wave execute in order,
-// so handing data between its lanes through LDS needs only the LDS counter to drain and
-// a compiler fence; a workgroup barrier would also wait for every global load in flight
-// and stall the prefetch pipeline.
+// The kernel runs one wave per workgroup.  The LDS operations of a wave execute in
+// issue order, so handing data between its lanes through LDS needs no wait at all: only
+// wavefront-scope fences, which keep the compiler from moving memory operations across
+// the hand-over and emit no instructions.  (A workgroup barrier would wait for every
+// global load in flight and stall the prefetch pipeline; draining the LDS counter would
+// stall on every outstanding LDS operation.)
 __device__ __forceinline__ void wave_sync() {
-    __atomic_signal_fence(__ATOMIC_SEQ_CST);
-    __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0); vmcnt and expcnt left open
-    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
 __device__ __forceinline__ uint4 ld16(const uint8_t* p) {
@@ -179,30 +181,45 @@ __device__ __forceinline__ uint4 ld16(const uint8_t* p) {
 // The correction slots build LDS addresses by OR-ing entry bits into aligned bases, so
 // the first members sit at offsets that are multiples of their sizes: tab at 0 (bits
 // 10-11 select the class, bit 3 the nibble half), dense at 4096 (a page per 1024 bytes;
-// K rows of 64 bytes, V channel rows of 8 bytes), q and oci 256-aligned.
+// K rows of 64 bytes, V channel rows of 8 bytes), q and oci 512-aligned.
+//
+// Buffers live only in the phase that needs them share storage, which keeps the wave's
+// LDS small enough for more waves per CU: the fixed-point query (qi) is read only
+// before the key pass and sits in the table's space; q (key pass) shares with oci (value
+// pass); tokc (key pass) shares with wv and oc (value pass).
 template <int G>
 struct Smem {
-    __align__(16) float2 tab[4][GT][2];       // correction table [COO class][token][nibble bit 3]
-    __align__(16) uint8_t dense[GRP][PSTR];   // K: token rows of 64 bytes; V: channel rows of 8
-    __align__(16) float q[G][D];
-    __align__(16) int oci[G][D];              // value corrections of one group, fixed point
-    int qi[G][D];
+    __align__(16) uint8_t tab_[4 * GT * 2 * 8];   // tab float2 [COO class][token][nibble bit 3]; qi
+    __align__(16) uint8_t dense[GRP][PSTR];       // K: token rows of 64 bytes; V: channel rows of 8
+    __align__(16) uint8_t qo_[G * D * 4];         // q float [G][D] (keys); oci int [G][D] (values)
+    __align__(16) uint8_t tw_[(G * D * 4 + G * GT * 8) > GT * 16 ? (G * D * 4 + G * GT * 8) : GT * 16];
     float pbase[G];
     float m[G], l[G];
-    __align__(16) uint8_t head[2][GRP][HB];   // record heads of the current / next group
-    int start[2][GRP][P];                     // offset of each slot's COO bytes in its page
-    __align__(16) uint8_t sparse[SPL + 80];   // page p's COO bytes at p*SSLOT; + slack for
-                                              // whole-dword reads past a bucket
-    __align__(16) float4 tokc[GT];            // base, Delta, Gp of the group's tokens
-    __align__(16) uint4 wv[G][GT / 2];        // value-pass weights of token pairs: 4 features, 4 limbs
-    float oc[G][D];                           // value corrections
+    __align__(16) uint8_t head[2][GRP][HB];       // record heads of the current / next group
+    int start[2][GRP][P];                         // offset of each slot's COO bytes in its page
+    __align__(16) uint8_t sparse[SPL + 80];       // page p's COO bytes at p*SSLOT; + slack for
+                                                  // whole-dword reads past a bucket
+
+    // correction table [COO class][token][nibble bit 3]
+    __device__ float2 (&tab())[4][GT][2] { return *reinterpret_cast<float2 (*)[4][GT][2]>(tab_); }
+    // query in fixed point (before the key pass)
+    __device__ int (&qi())[G][D] { return *reinterpret_cast<int (*)[G][D]>(tab_); }
+    // query in fp32 (key pass)
+    __device__ float (&q())[G][D] { return *reinterpret_cast<float (*)[G][D]>(qo_); }
+    // value corrections of one group, fixed point (value pass)
+    __device__ int (&oci())[G][D] { return *reinterpret_cast<int (*)[G][D]>(qo_); }
+    // base, Delta, Gp of the group's tokens (key pass)
+    __device__ float4 (&tokc())[GT] { return *reinterpret_cast<float4 (*)[GT]>(tw_); }
+    // value corrections (value pass)
+    __device__ float (&oc())[G][D] { return *reinterpret_cast<float (*)[G][D]>(tw_); }
+    // value-pass weights of token pairs: 4 features, 4 limbs (value pass)
+    __device__ uint4 (&wv())[G][GT / 2] { return *reinterpret_cast<uint4 (*)[G][GT / 2]>(tw_ + G * D * 4); }
 };
 
 // Wave-uniform description of a group of consecutive pages of one sequence.
 struct Grp {
-    const uint8_t* rec[GRP];
-    const uint8_t* base[GRP];   // rec, or a valid stand-in record for missing pages
-    int nval[GRP];   // valid slots per page (0 when the page is outside the range)
+    const uint8_t* base[GRP];   // the page's record, or a valid stand-in record when absent
+    int nval[GRP];              // valid slots per page (0 when absent or outside the range)
     int npg;
 };
 
@@ -213,16 +230,15 @@ __device__ __forceinline__ Grp make_group(const AttnArgs& a, int blk_lane, int p
     gr.npg = max(0, min(GRP, p_end - g0));
 #pragma unroll
     for (int pg = 0; pg < GRP; ++pg) {
-        gr.rec[pg] = nullptr;
+        gr.base[pg] = a.pool;
         gr.nval[pg] = 0;
         if (pg < gr.npg) {
             const int blk = __builtin_amdgcn_readlane(blk_lane, g0 + pg - p_begin);
             if (blk >= 0 && blk < a.num_blocks) {
-                gr.rec[pg] = a.pool + (((int64_t)blk * a.H + h) * 2 + which) * a.stride;
+                gr.base[pg] = a.pool + (((int64_t)blk * a.H + h) * 2 + which) * a.stride;
                 gr.nval[pg] = max(0, min(P, L - (g0 + pg) * P));
             }
         }
-        gr.base[pg] = gr.rec[pg] ? gr.rec[pg] : a.pool;
     }
     return gr;
 }
@@ -280,7 +296,7 @@ __device__ __forceinline__ void token_table(Smem<G>& S, int tg, const Tok& T, fl
     const float y[4] = {T.kd_i, T.kd_o, T.kd_i, T.kd_o};
 #pragma unroll
     for (int cls = 0; cls < 4; ++cls)
-        *reinterpret_cast<float4*>(&S.tab[cls][tg][0]) =
+        *reinterpret_cast<float4*>(&S.tab()[cls][tg][0]) =
             make_float4(w * x[cls], w * y[cls], w * (x[cls] - T.gp), w * y[cls]);
 }
 
@@ -324,8 +340,9 @@ __device__ __forceinline__ float entry_delta(Smem<G>& S, uint32_t tbo, uint32_t 
     return fmaf((float)n, kv.y, kv.x);
 }
 
-static_assert(offsetof(Smem<1>, dense) == 4096 && offsetof(Smem<4>, q) == 8192 &&
-              offsetof(Smem<4>, oci) == 8192 + 4 * 512, "LDS layout the correction addressing relies on");
+static_assert(offsetof(Smem<1>, dense) == 4096 && offsetof(Smem<1>, qo_) == 8192 &&
+              offsetof(Smem<4>, qo_) == 8192 && sizeof(Smem<1>::tab_) >= sizeof(int) * 4 * D,
+              "LDS layout the correction addressing relies on");
 
 template <int G>
 __device__ __forceinline__ uint32_t off_of(const Smem<G>& S, const void* p) {
@@ -348,13 +365,13 @@ __device__ __forceinline__ void key_corrections(Smem<G>& S, float* sc, int cap, 
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
         k[nb] = bucket_of(S, b, gr, pp0 + 2 * nb, lane);
-        tbo[nb] = off_of(S, &S.tab[0][k[nb].tg][0]);
+        tbo[nb] = off_of(S, &S.tab()[0][k[nb].tg][0]);
         drow[nb] = off_of(S, &S.dense[k[nb].pg][k[nb].t * 64 + k[nb].c * 32]);
         mc = max(mc, k[nb].cnt);
 #pragma unroll
         for (int hd = 0; hd < G; ++hd) corr[nb][hd] = 0.0f;
     }
-    const uint32_t qc = off_of(S, &S.q[0][((lane >> 4) & 1) * 64]);
+    const uint32_t qc = off_of(S, &S.q()[0][((lane >> 4) & 1) * 64]);
     const int maxc = wave_max_i(mc);
     // The entry in bits o..o+7 of ent: index j (6 bits), class (2 bits).  Every slot is
     // computed; slots past the bucket get a zero weight (no branches).
@@ -388,10 +405,43 @@ __device__ __forceinline__ void key_corrections(Smem<G>& S, float* sc, int cap, 
                 cur[nb] = nxt[nb];
                 nxt[nb] = w[nb][(kk >> 2) + 2];
             }
+            // three phases, kept apart so that a block's reads issue together: the nibble
+            // dwords and queries, then the table rows, then the accumulation
+            uint32_t dw[NB][4];
+            float qv[NB][4][G];
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) slot(nb, ent[nb], 8 * i, kk + i < k[nb].cnt);
+                for (int i = 0; i < 4; ++i) {
+                    const int o = 8 * i;
+                    dw[nb][i] = lds_at<uint32_t>(S, drow[nb] | (shr(ent[nb], o + 1) & 0x1cu));
+                    const uint32_t qo = qc | (shr(ent[nb], o - 2) & 0xfcu);
+#pragma unroll
+                    for (int hd = 0; hd < G; ++hd) qv[nb][i][hd] = lds_at<float>(S, qo + hd * D * 4);
+                }
+            __builtin_amdgcn_sched_barrier(0);
+            float2 kv[NB][4];
+            uint32_t nn[NB][4];
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int o = 8 * i;
+                    nn[nb][i] = __builtin_amdgcn_ubfe(dw[nb][i], ((ent[nb] >> o) & 0xffu) << 2, 4);
+                    const uint32_t ta = (tbo[nb] | (shr(ent[nb], o - 4) & 0xc00u)) | (nn[nb][i] & 8u);
+                    kv[nb][i] = lds_at<float2>(S, ta);
+                }
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float delta = fmaf((float)nn[nb][i], kv[nb][i].y, kv[nb][i].x);
+                    const bool valid = kk + i < k[nb].cnt;
+#pragma unroll
+                    for (int hd = 0; hd < G; ++hd)
+                        corr[nb][hd] = fmaf(valid ? qv[nb][i][hd] : 0.0f, delta, corr[nb][hd]);
+                }
         }
         // the last 1-3 slots (the wave's longest bucket decides how many)
         const int rem = maxc - full;
@@ -411,8 +461,8 @@ __device__ __forceinline__ void key_corrections(Smem<G>& S, float* sc, int cap, 
     } else {
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
-            const uint8_t* r = pick4(k[nb].pg, gr.rec[0], gr.rec[1], gr.rec[2], gr.rec[3]);
-            const uint8_t* spp = r ? r + LY.sparse + k[nb].st : nullptr;
+            // (a bucket of an absent page is empty)
+            const uint8_t* spp = pick4(k[nb].pg, gr.base[0], gr.base[1], gr.base[2], gr.base[3]) + LY.sparse + k[nb].st;
             for (int kk = 0; kk < maxc; ++kk)
                 if (kk < k[nb].cnt) slot(nb, spp[kk], 0, true);
         }
@@ -438,7 +488,7 @@ __device__ __forceinline__ void value_corrections(Smem<G>& S, const float* sc, i
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
         k[nb] = bucket_of(S, b, gr, pp0 + 2 * nb, lane);
-        tbo[nb] = off_of(S, &S.tab[0][k[nb].tg][0]);
+        tbo[nb] = off_of(S, &S.tab()[0][k[nb].tg][0]);
         dcol[nb] = off_of(S, &S.dense[k[nb].pg][(k[nb].t >> 3) * 4 + k[nb].c * 512]);
         mc = max(mc, k[nb].cnt);
 #pragma unroll
@@ -446,7 +496,7 @@ __device__ __forceinline__ void value_corrections(Smem<G>& S, const float* sc, i
             pt[nb][hd] = (G > 1 && k[nb].vt) ? sc[hd * cap + tok0 + k[nb].tg] : 1.0f;
     }
     const uint32_t nsh = (lane & 7) * 4;
-    const uint32_t occ = off_of(S, &S.oci[0][((lane >> 4) & 1) * 64]);
+    const uint32_t occ = off_of(S, &S.oci()[0][((lane >> 4) & 1) * 64]);
     const int maxc = wave_max_i(mc);
     // Every slot is computed and added; slots past the bucket add zero (no branches).
     // The loads of a block's slots come first, then its LDS additions, so that the
@@ -524,8 +574,8 @@ __device__ __forceinline__ void value_corrections(Smem<G>& S, const float* sc, i
     } else {
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
-            const uint8_t* r = pick4(k[nb].pg, gr.rec[0], gr.rec[1], gr.rec[2], gr.rec[3]);
-            const uint8_t* spp = r ? r + LY.sparse + k[nb].st : nullptr;
+            // (a bucket of an absent page is empty)
+            const uint8_t* spp = pick4(k[nb].pg, gr.base[0], gr.base[1], gr.base[2], gr.base[3]) + LY.sparse + k[nb].st;
             for (int kk = 0; kk < maxc; ++kk)
                 if (kk < k[nb].cnt) apply(slot(nb, spp[kk], 0, true));
         }
@@ -533,7 +583,7 @@ __device__ __forceinline__ void value_corrections(Smem<G>& S, const float* sc, i
 }
 
 template <int G>
-__global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 : 1))) void attn_mfma_kernel(AttnArgs a) {
     constexpr int NRS = (G + 1) / 2;        // key-pass MFMA row sets (8 rows per head)
     __shared__ Smem<G> S;
     extern __shared__ float sc[];           // [G][cap]: scores, then probabilities
@@ -568,13 +618,13 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
     for (int hd = 0; hd < G; ++hd) {
         const uint16_t* qp = a.q + ((int64_t)s * a.Hq + h * G + hd) * D;
         const float x0 = h2f(qp[lane]), x1 = h2f(qp[lane + 64]);
-        S.q[hd][lane] = x0;
-        S.q[hd][lane + 64] = x1;
+        S.q()[hd][lane] = x0;
+        S.q()[hd][lane + 64] = x1;
         const float mx = wave_max_nonneg(fmaxf(fabsf(x0), fabsf(x1)));
         const float sum = wave_sum(x0 + x1);
         const int sh = fix_shift(mx);
-        S.qi[hd][lane] = (int)rintf(ldexpf(x0, sh));
-        S.qi[hd][lane + 64] = (int)rintf(ldexpf(x1, sh));
+        S.qi()[hd][lane] = (int)rintf(ldexpf(x0, sh));
+        S.qi()[hd][lane + 64] = (int)rintf(ldexpf(x1, sh));
         // score = scale * (base * sum(q) + (Delta * U + Gp * H) * 2^-(shift + 7))
         ssum[hd] = a.scale * sum;
         sfix[hd] = ldexpf(a.scale, -(sh + 7));
@@ -597,7 +647,7 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
 #pragma unroll
                     for (int bb = 0; bb < 4; ++bb) {
                         const int pr = g4 * 16 + m * 4 + bb;
-                        const int qe = S.qi[hd][2 * pr], qo = S.qi[hd][2 * pr + 1];
+                        const int qe = S.qi()[hd][2 * pr], qo = S.qi()[hd][2 * pr + 1];
                         const int w0 = type ? 0 : 8 * qo;
                         const int w1 = type ? 0 : 128 * qe - 8 * qo;
                         const int w2 = type ? -qo : -16 * qo;
@@ -635,14 +685,6 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
     for (int g0 = p_begin; g0 < p_end; g0 += GRP, b ^= 1) {
         const int tok0 = (g0 - p_begin) * P;
         const bool staged = fits_c;
-        // token constants of the group (lane = token) and the key correction tables
-        {
-            const int pg = lane >> 4, t = lane & 15;
-            const Tok T = token_consts(&S.head[b][pg][LY.meta + 12 * t], tk);
-            S.tokc[lane] = make_float4(T.base, T.dm, T.gp, 0.0f);
-            token_table(S, lane, T, 1.0f);
-        }
-        wave_sync();
         // dense part on the matrix cores: one accumulator per page and the pages' MFMAs
         // interleaved, so that no MFMA waits on the one before it; stage the group in LDS
         {
@@ -664,6 +706,18 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
 #pragma unroll
             for (int pg = 0; pg < GRP; ++pg)
                 *reinterpret_cast<uint4*>(&S.dense[pg][(lane & 15) * 64 + (lane >> 4) * 16]) = dreg[pg];
+            // the next group's dense bytes go out as soon as these are consumed
+#pragma unroll
+            for (int pg = 0; pg < GRP; ++pg) dreg[pg] = ld16(gn.base[pg] + koff);
+            // token constants of the group (lane = token) and the key correction tables,
+            // while the MFMAs drain
+            {
+                const int pg = lane >> 4, t = lane & 15;
+                const Tok T = token_consts(&S.head[b][pg][LY.meta + 12 * t], tk);
+                S.tokc()[lane] = make_float4(T.base, T.dm, T.gp, 0.0f);
+                token_table(S, lane, T, 1.0f);
+            }
+            wave_sync();
             // Lane (t + 16*grp4) holds rows 4*grp4 .. 4*grp4+3 of column t: the U (grp4
             // even) or H (grp4 odd) limbs of head rs*2 + grp4/2.  Rows 1 and 3 reach rows 0
             // and 2 by a row swap.
@@ -671,7 +725,7 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
             const bool hi = (grp4 >> 1) != 0;
 #pragma unroll
             for (int pg = 0; pg < GRP; ++pg) {
-                const float4 tc = S.tokc[pg * P + t];
+                const float4 tc = S.tokc()[pg * P + t];
                 const bool valid = t < gc.nval[pg];
 #pragma unroll
                 for (int rs = 0; rs < NRS; ++rs) {
@@ -699,8 +753,6 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
             wave_sync();
             const int used = group_layout(S, b ^ 1, gn, lane, fits_n);
             wave_sync();
-#pragma unroll
-            for (int pg = 0; pg < GRP; ++pg) dreg[pg] = ld16(gn.base[pg] + koff);
             sparse_chunks(gn, used, lane, sreg0, sreg1);
             gnn = make_group(a, blk_lane, p_begin, g0 + 2 * GRP, p_end, L, h, 0);
             hreg = head_chunk(gnn, lane, hoff);
@@ -738,10 +790,10 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
             S.m[hd] = mx;
             S.l[hd] = sum;
         }
-        S.oc[hd][lane] = 0.0f;
-        S.oc[hd][lane + 64] = 0.0f;
-        S.oci[hd][lane] = 0;
-        S.oci[hd][lane + 64] = 0;
+        S.oc()[hd][lane] = 0.0f;
+        S.oc()[hd][lane + 64] = 0.0f;
+        S.oci()[hd][lane] = 0;
+        S.oci()[hd][lane + 64] = 0;
     }
     if (lane < GRP * HCH) *reinterpret_cast<uint4*>(&S.head[0][0][16 * lane]) = hreg;
     wave_sync();
@@ -769,6 +821,9 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
         const bool staged = fits_c;
 #pragma unroll
         for (int pg = 0; pg < GRP; ++pg) *reinterpret_cast<uint4*>(&S.dense[pg][lane * 16]) = dreg[pg];
+        // the next group's dense bytes go out as soon as these are staged
+#pragma unroll
+        for (int pg = 0; pg < GRP; ++pg) dreg[pg] = ld16(gn.base[pg] + voff);
         if (staged) {
             *reinterpret_cast<uint4*>(&S.sparse[stg]) = sreg0;
             *reinterpret_cast<uint4*>(&S.sparse[stg + 256]) = sreg1;
@@ -799,7 +854,7 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
                 const int co = __builtin_amdgcn_update_dpp(0, ce, 0x101, 0xf, 0xf, false);   // row_shl:1
                 const int go = __builtin_amdgcn_update_dpp(0, ge, 0x101, 0xf, 0xf, false);
                 if ((lane & 1) == 0)
-                    S.wv[hd][lane >> 1] = make_uint4(enc(8 * co), enc(128 * ce - 8 * co), enc(-(go + 16 * co)),
+                    S.wv()[hd][lane >> 1] = make_uint4(enc(8 * co), enc(128 * ce - 8 * co), enc(-(go + 16 * co)),
                                                      enc(16 * ge + go + 16 * co));
             }
             // Value corrections accumulate as integers (LDS float atomics are slow): the
@@ -826,8 +881,6 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
             wave_sync();
             const int used = group_layout(S, b ^ 1, gn, lane, fits_n);
             wave_sync();
-#pragma unroll
-            for (int pg = 0; pg < GRP; ++pg) dreg[pg] = ld16(gn.base[pg] + voff);
             sparse_chunks(gn, used, lane, sreg0, sreg1);
             gnn = make_group(a, blk_lane, p_begin, g0 + 2 * GRP, p_end, L, h, 1);
             hreg = head_chunk(gnn, lane, hoff);
@@ -844,7 +897,7 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
                 const int row = lane & 15, hdr = row >> 2, g4 = lane >> 4, r = row & 3;
                 v4i av = v4i{0, 0, 0, 0};
                 if (hdr < G) {
-                    const uint4* wp = &S.wv[hdr][(pp >> 1) * 16 + g4 * 4];
+                    const uint4* wp = &S.wv()[hdr][(pp >> 1) * 16 + g4 * 4];
                     const uint4 w0 = wp[0], w1 = wp[1], w2 = wp[2], w3 = wp[3];
                     const uint32_t sel = (uint32_t)r | ((uint32_t)(r + 4) << 8);
                     auto col = [&](uint32_t a0, uint32_t a1, uint32_t a2, uint32_t a3) {
@@ -866,6 +919,13 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
                 }
             }
         }
+        // the dense sums leave the accumulators before the correction walk, which then has
+        // their registers
+        if (hq < G) {
+            const int e = pick4(hq, vsh[0], vsh[G > 1 ? 1 : 0], vsh[G > 2 ? 2 : 0], vsh[G > 3 ? 3 : 0]) + 7;
+#pragma unroll
+            for (int nt = 0; nt < 8; ++nt) oacc[nt] += ldexpf(limbs(gacc[nt]), -e);
+        }
         if (staged)
             value_corrections<G, true, GRP / 2>(S, sc, cap, b, gc, 0, tok0, lane);
         else
@@ -874,15 +934,10 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
         // fold the group's integer sums into the fp32 outputs
 #pragma unroll
         for (int hd = 0; hd < G; ++hd) {
-            S.oc[hd][lane] += ldexpf((float)S.oci[hd][lane], -fsh);
-            S.oc[hd][lane + 64] += ldexpf((float)S.oci[hd][lane + 64], -fsh);
-            S.oci[hd][lane] = 0;
-            S.oci[hd][lane + 64] = 0;
-        }
-        if (hq < G) {
-            const int e = pick4(hq, vsh[0], vsh[G > 1 ? 1 : 0], vsh[G > 2 ? 2 : 0], vsh[G > 3 ? 3 : 0]) + 7;
-#pragma unroll
-            for (int nt = 0; nt < 8; ++nt) oacc[nt] += ldexpf(limbs(gacc[nt]), -e);
+            S.oc()[hd][lane] += ldexpf((float)S.oci()[hd][lane], -fsh);
+            S.oc()[hd][lane + 64] += ldexpf((float)S.oci()[hd][lane + 64], -fsh);
+            S.oci()[hd][lane] = 0;
+            S.oci()[hd][lane + 64] = 0;
         }
         gc = gn;
         gn = gnn;
@@ -901,7 +956,7 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
 #pragma unroll
         for (int nt = 0; nt < 8; ++nt) {
             const int j = nt * 16 + (lane & 15);
-            const float o = S.pbase[hq] + oacc[nt] + S.oc[hq][j];
+            const float o = S.pbase[hq] + oacc[nt] + S.oc()[hq][j];
             if (a.n_splits == 1) {
                 a.out[row * D + j] = (l > 0.0f) ? o / l : 0.0f;
             } else {
