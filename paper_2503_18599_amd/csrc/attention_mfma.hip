@@ -44,7 +44,7 @@ constexpr int GRP = 4;                     // pages per group (two correction pa
 constexpr int GT = GRP * P;                // tokens per group
 constexpr int PSTR = 1024;                 // LDS stride of a page's dense bytes
 constexpr int SPCAP = P * D;               // sparse capacity of one record
-constexpr int SSLOT = 512;                 // staged COO bytes per page (larger pages: read from HBM)
+constexpr int SSLOT = 448;                 // staged COO bytes per page (larger pages: read from HBM)
 constexpr int SPL = GRP * SSLOT;           // group sparse bytes staged in LDS
 
 static_assert(LY.meta == 32 && LY.dense == HB && LY.sparse == 1248, "record layout");
@@ -195,8 +195,8 @@ struct Smem {
     __align__(16) uint8_t tw_[(G * D * 4 + G * GT * 8) > GT * 16 ? (G * D * 4 + G * GT * 8) : GT * 16];
     float pbase[G];
     float m[G], l[G];
-    __align__(16) uint8_t head[2][GRP][HB];       // record heads of the current / next group
-    int start[2][GRP][P];                         // offset of each slot's COO bytes in its page
+    __align__(16) uint8_t head[GRP][HB];          // record heads of a group
+    int start[GRP][P];                            // offset of each slot's COO bytes in its page
     __align__(16) uint8_t sparse[SPL + 80];       // page p's COO bytes at p*SSLOT; + slack for
                                                   // whole-dword reads past a bucket
 
@@ -265,12 +265,12 @@ __device__ __forceinline__ uint4 head_chunk(const Grp& gr, int lane, uint32_t ho
 // COO bytes used by the lane's page (lane >> 4) and whether every page fits its staging
 // slot.
 template <int G>
-__device__ __forceinline__ int group_layout(Smem<G>& S, int b, const Grp& gr, int lane, bool& fits) {
+__device__ __forceinline__ int group_layout(Smem<G>& S, const Grp& gr, int lane, bool& fits) {
     const int pg = lane >> 4, t = lane & 15;
     const int nv = pick4(pg, gr.nval[0], gr.nval[1], gr.nval[2], gr.nval[3]);
-    const int tot = (t < nv) ? (int)S.head[b][pg][2 * t] + (int)S.head[b][pg][2 * t + 1] : 0;
+    const int tot = (t < nv) ? (int)S.head[pg][2 * t] + (int)S.head[pg][2 * t + 1] : 0;
     const int incl = row_scan16(tot);
-    S.start[b][pg][t] = incl - tot;
+    S.start[pg][t] = incl - tot;
     const int u0 = __builtin_amdgcn_readlane(incl, 15), u1 = __builtin_amdgcn_readlane(incl, 31);
     const int u2 = __builtin_amdgcn_readlane(incl, 47), u3 = __builtin_amdgcn_readlane(incl, 63);
     fits = max(max(u0, u1), max(u2, u3)) <= SSLOT;
@@ -307,7 +307,7 @@ struct Bucket {
 };
 
 template <int G>
-__device__ __forceinline__ Bucket bucket_of(Smem<G>& S, int b, const Grp& gr, int pp, int lane) {
+__device__ __forceinline__ Bucket bucket_of(Smem<G>& S, const Grp& gr, int pp, int lane) {
     Bucket k;
     k.c = (lane >> 4) & 1;
     k.t = lane & 15;
@@ -315,9 +315,9 @@ __device__ __forceinline__ Bucket bucket_of(Smem<G>& S, int b, const Grp& gr, in
     k.tg = k.pg * P + k.t;
     const int nv = pick4(k.pg, gr.nval[0], gr.nval[1], gr.nval[2], gr.nval[3]);
     k.vt = k.t < nv;
-    const int c0 = k.vt ? (int)S.head[b][k.pg][2 * k.t] : 0;
-    const int c1 = k.vt ? (int)S.head[b][k.pg][2 * k.t + 1] : 0;
-    k.st = k.vt ? S.start[b][k.pg][k.t] + (k.c ? c0 : 0) : 0;
+    const int c0 = k.vt ? (int)S.head[k.pg][2 * k.t] : 0;
+    const int c1 = k.vt ? (int)S.head[k.pg][2 * k.t + 1] : 0;
+    k.st = k.vt ? S.start[k.pg][k.t] + (k.c ? c0 : 0) : 0;
     // a 64-value chunk has at most 64 entries; larger counts are not a valid record
     k.cnt = max(0, min(min(k.c ? c1 : c0, 64), SPCAP - k.st));
     return k;
@@ -351,20 +351,20 @@ __device__ __forceinline__ uint32_t off_of(const Smem<G>& S, const void* p) {
 
 // Walks each lane's buckets and adds every entry's q-weighted correction (true value
 // minus middle reading) to its token's score.  A lane owns NB buckets, one in each of
-// the page pairs pp0, pp0 + 2, ..., walked side by side so that their LDS loads overlap.
+// the page pairs 0, 2, ..., walked side by side so that their LDS loads overlap.
 // Staged entries are read four at a time from one aligned dword pair, one block ahead of
 // their use; the corrections of a block are independent, and entries past a bucket
 // contribute zero.
 template <int G, bool STAGED, int NB>
-__device__ __forceinline__ void key_corrections(Smem<G>& S, float* sc, int cap, float scale, int b,
-                                                const Grp& gr, int pp0, int tok0, int lane) {
+__device__ __forceinline__ void key_corrections(Smem<G>& S, float* sc, int cap, float scale,
+                                                const Bucket (&kb)[NB], const Grp& gr, int tok0, int lane) {
     Bucket k[NB];
     uint32_t tbo[NB], drow[NB];
     float corr[NB][G];
     int mc = 0;
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
-        k[nb] = bucket_of(S, b, gr, pp0 + 2 * nb, lane);
+        k[nb] = kb[nb];
         tbo[nb] = off_of(S, &S.tab()[0][k[nb].tg][0]);
         drow[nb] = off_of(S, &S.dense[k[nb].pg][k[nb].t * 64 + k[nb].c * 32]);
         mc = max(mc, k[nb].cnt);
@@ -479,15 +479,15 @@ __device__ __forceinline__ void key_corrections(Smem<G>& S, float* sc, int cap, 
 // Same walk for values: each entry adds p_t * (true value - middle reading) to its
 // channel.  With one head the probability is already folded into the table and Gp.
 template <int G, bool STAGED, int NB>
-__device__ __forceinline__ void value_corrections(Smem<G>& S, const float* sc, int cap, int b,
-                                                  const Grp& gr, int pp0, int tok0, int lane) {
+__device__ __forceinline__ void value_corrections(Smem<G>& S, const float* sc, int cap,
+                                                  const Bucket (&kb)[NB], const Grp& gr, int tok0, int lane) {
     Bucket k[NB];
     uint32_t tbo[NB], dcol[NB];
     float pt[NB][G];
     int mc = 0;
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
-        k[nb] = bucket_of(S, b, gr, pp0 + 2 * nb, lane);
+        k[nb] = kb[nb];
         tbo[nb] = off_of(S, &S.tab()[0][k[nb].tg][0]);
         dcol[nb] = off_of(S, &S.dense[k[nb].pg][(k[nb].t >> 3) * 4 + k[nb].c * 512]);
         mc = max(mc, k[nb].cnt);
@@ -629,7 +629,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         ssum[hd] = a.scale * sum;
         sfix[hd] = ldexpf(a.scale, -(sh + 7));
     }
-    if (lane < GRP * HCH) *reinterpret_cast<uint4*>(&S.head[0][0][16 * lane]) = hreg;
+    if (lane < GRP * HCH) *reinterpret_cast<uint4*>(&S.head[0][16 * lane]) = hreg;
     wave_sync();
 
     // Key-pass A operand: row = 8*(head%2) + 4*type + limb, type 0 -> sum q u, 1 -> sum q h.
@@ -671,9 +671,11 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
     const uint32_t koff = (uint32_t)LY.dense + (uint32_t)((lane & 15) * 64 + (lane >> 4) * 16);
     const uint32_t voff = (uint32_t)LY.dense + (uint32_t)lane * 16u;
     const uint32_t stg = (uint32_t)((lane >> 4) * SSLOT + (lane & 15) * 16);   // LDS staging slot
+    // (a staged page fits its slot, so its second chunk row is needed only within it)
+    const bool stg1_in = 256 + (lane & 15) * 16 < SSLOT;
     bool fits_c, fits_n;
     {
-        const int used = group_layout(S, 0, gc, lane, fits_c);
+        const int used = group_layout(S, gc, lane, fits_c);
         wave_sync();
 #pragma unroll
         for (int pg = 0; pg < GRP; ++pg) dreg[pg] = ld16(gc.base[pg] + koff);
@@ -681,8 +683,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
     }
     Grp gn = make_group(a, blk_lane, p_begin, p_begin + GRP, p_end, L, h, 0);
     hreg = head_chunk(gn, lane, hoff);
-    int b = 0;
-    for (int g0 = p_begin; g0 < p_end; g0 += GRP, b ^= 1) {
+    for (int g0 = p_begin; g0 < p_end; g0 += GRP) {
         const int tok0 = (g0 - p_begin) * P;
         const bool staged = fits_c;
         // dense part on the matrix cores: one accumulator per page and the pages' MFMAs
@@ -713,7 +714,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
             // while the MFMAs drain
             {
                 const int pg = lane >> 4, t = lane & 15;
-                const Tok T = token_consts(&S.head[b][pg][LY.meta + 12 * t], tk);
+                const Tok T = token_consts(&S.head[pg][LY.meta + 12 * t], tk);
                 S.tokc()[lane] = make_float4(T.base, T.dm, T.gp, 0.0f);
                 token_table(S, lane, T, 1.0f);
             }
@@ -743,15 +744,20 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         }
         if (staged) {
             *reinterpret_cast<uint4*>(&S.sparse[stg]) = sreg0;
-            *reinterpret_cast<uint4*>(&S.sparse[stg + 256]) = sreg1;
+            if (stg1_in) *reinterpret_cast<uint4*>(&S.sparse[stg + 256]) = sreg1;
         }
-        // next group: heads -> layout -> issue its dense/sparse and the heads after it
+        // the walk's buckets leave the head buffer before the next group's heads replace it
+        Bucket kb[GRP / 2];
+#pragma unroll
+        for (int nb = 0; nb < GRP / 2; ++nb) kb[nb] = bucket_of(S, gc, 2 * nb, lane);
+        wave_sync();
+        // next group: heads -> layout -> issue its sparse bytes and the heads after it
         Grp gnn = gn;
         fits_n = true;
         if (gn.npg > 0) {
-            if (lane < GRP * HCH) *reinterpret_cast<uint4*>(&S.head[b ^ 1][0][16 * lane]) = hreg;
+            if (lane < GRP * HCH) *reinterpret_cast<uint4*>(&S.head[0][16 * lane]) = hreg;
             wave_sync();
-            const int used = group_layout(S, b ^ 1, gn, lane, fits_n);
+            const int used = group_layout(S, gn, lane, fits_n);
             wave_sync();
             sparse_chunks(gn, used, lane, sreg0, sreg1);
             gnn = make_group(a, blk_lane, p_begin, g0 + 2 * GRP, p_end, L, h, 0);
@@ -760,9 +766,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         wave_sync();
         // sparse part
         if (staged)
-            key_corrections<G, true, GRP / 2>(S, sc, cap, a.scale, b, gc, 0, tok0, lane);
+            key_corrections<G, true, GRP / 2>(S, sc, cap, a.scale, kb, gc, tok0, lane);
         else
-            key_corrections<G, false, GRP / 2>(S, sc, cap, a.scale, b, gc, 0, tok0, lane);
+            key_corrections<G, false, GRP / 2>(S, sc, cap, a.scale, kb, gc, tok0, lane);
         wave_sync();
         gc = gn;
         gn = gnn;
@@ -795,7 +801,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         S.oci()[hd][lane] = 0;
         S.oci()[hd][lane + 64] = 0;
     }
-    if (lane < GRP * HCH) *reinterpret_cast<uint4*>(&S.head[0][0][16 * lane]) = hreg;
+    if (lane < GRP * HCH) *reinterpret_cast<uint4*>(&S.head[0][16 * lane]) = hreg;
     wave_sync();
 
     // ---- pass 2: values ------------------------------------------------------------
@@ -807,7 +813,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
 #pragma unroll
     for (int hd = 0; hd < G; ++hd) pb[hd] = 0.0f;
     {
-        const int used = group_layout(S, 0, gc, lane, fits_c);
+        const int used = group_layout(S, gc, lane, fits_c);
         wave_sync();
 #pragma unroll
         for (int pg = 0; pg < GRP; ++pg) dreg[pg] = ld16(gc.base[pg] + voff);
@@ -815,8 +821,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
     }
     gn = make_group(a, blk_lane, p_begin, p_begin + GRP, p_end, L, h, 1);
     hreg = head_chunk(gn, lane, hoff);
-    b = 0;
-    for (int g0 = p_begin; g0 < p_end; g0 += GRP, b ^= 1) {
+    for (int g0 = p_begin; g0 < p_end; g0 += GRP) {
         const int tok0 = (g0 - p_begin) * P;
         const bool staged = fits_c;
 #pragma unroll
@@ -826,7 +831,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         for (int pg = 0; pg < GRP; ++pg) dreg[pg] = ld16(gn.base[pg] + voff);
         if (staged) {
             *reinterpret_cast<uint4*>(&S.sparse[stg]) = sreg0;
-            *reinterpret_cast<uint4*>(&S.sparse[stg + 256]) = sreg1;
+            if (stg1_in) *reinterpret_cast<uint4*>(&S.sparse[stg + 256]) = sreg1;
         }
         // fixed-point coefficients p*Delta, p*Gp of the group's tokens (lane = token), one
         // shift per head; correction tables (scaled by p when one head reads them)
@@ -836,7 +841,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
             const int pg = lane >> 4, t = lane & 15;
             const int nv = pick4(pg, gc.nval[0], gc.nval[1], gc.nval[2], gc.nval[3]);
             const bool vt = t < nv;
-            const Tok T = token_consts(&S.head[b][pg][LY.meta + 12 * t], tv);
+            const Tok T = token_consts(&S.head[pg][LY.meta + 12 * t], tv);
             float p0 = 0.0f;
 #pragma unroll
             for (int hd = 0; hd < G; ++hd) {
@@ -873,13 +878,18 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
             const float ws = ldexpf(w, fsh);
             token_table(S, lane, T, ws);
         }
-        // next group: heads -> layout -> issue its loads
+        // the walk's buckets leave the head buffer before the next group's heads replace it
+        Bucket kb[GRP / 2];
+#pragma unroll
+        for (int nb = 0; nb < GRP / 2; ++nb) kb[nb] = bucket_of(S, gc, 2 * nb, lane);
+        wave_sync();
+        // next group: heads -> layout -> issue its sparse bytes and the heads after it
         Grp gnn = gn;
         fits_n = true;
         if (gn.npg > 0) {
-            if (lane < GRP * HCH) *reinterpret_cast<uint4*>(&S.head[b ^ 1][0][16 * lane]) = hreg;
+            if (lane < GRP * HCH) *reinterpret_cast<uint4*>(&S.head[0][16 * lane]) = hreg;
             wave_sync();
-            const int used = group_layout(S, b ^ 1, gn, lane, fits_n);
+            const int used = group_layout(S, gn, lane, fits_n);
             wave_sync();
             sparse_chunks(gn, used, lane, sreg0, sreg1);
             gnn = make_group(a, blk_lane, p_begin, g0 + 2 * GRP, p_end, L, h, 1);
@@ -927,9 +937,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
             for (int nt = 0; nt < 8; ++nt) oacc[nt] += ldexpf(limbs(gacc[nt]), -e);
         }
         if (staged)
-            value_corrections<G, true, GRP / 2>(S, sc, cap, b, gc, 0, tok0, lane);
+            value_corrections<G, true, GRP / 2>(S, sc, cap, kb, gc, tok0, lane);
         else
-            value_corrections<G, false, GRP / 2>(S, sc, cap, b, gc, 0, tok0, lane);
+            value_corrections<G, false, GRP / 2>(S, sc, cap, kb, gc, tok0, lane);
         wave_sync();
         // fold the group's integer sums into the fp32 outputs
 #pragma unroll
