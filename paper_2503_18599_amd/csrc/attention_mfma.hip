@@ -39,7 +39,7 @@ constexpr int D = 128;
 constexpr int P = kPage;
 constexpr Layout LY = make_layout(P, D);   // counts 0, meta 32, dense 224, sparse 1248
 constexpr int HB = 224;                    // counts + meta bytes at the start of a record
-constexpr int HCH = HB / 16;               // 16-byte chunks of a record head
+constexpr int CB = 32;                     // COO count bytes at the start of a record
 constexpr int GRP = 4;                     // pages per group (two correction pairs)
 constexpr int GT = GRP * P;                // tokens per group
 constexpr int PSTR = 1024;                 // LDS stride of a page's dense bytes
@@ -142,10 +142,13 @@ struct Tok {
     float b_il, b_ol, b_ih, b_oh, kd_i, kd_o;
 };
 
-__device__ __forceinline__ Tok token_consts(const uint8_t* meta, const float* th) {
-    const uint32_t w0 = *reinterpret_cast<const uint32_t*>(meta);
-    const uint32_t w1 = *reinterpret_cast<const uint32_t*>(meta + 4);
-    const uint32_t w2 = *reinterpret_cast<const uint32_t*>(meta + 8);
+// The token's 12 metadata bytes (three fp16 pairs Min, Delta: inner, middle, outer).
+struct Meta {
+    uint32_t w0, w1, w2;
+};
+
+__device__ __forceinline__ Tok token_consts(const Meta& mt, const float* th) {
+    const uint32_t w0 = mt.w0, w1 = mt.w1, w2 = mt.w2;
     const float mi = h2f(w0 & 0xffff), di = h2f(w0 >> 16);
     const float mm = h2f(w1 & 0xffff), dm = h2f(w1 >> 16);
     const float mo = h2f(w2 & 0xffff), dd = h2f(w2 >> 16);
@@ -195,7 +198,7 @@ struct Smem {
     __align__(16) uint8_t tw_[(G * D * 4 + G * GT * 8) > GT * 16 ? (G * D * 4 + G * GT * 8) : GT * 16];
     float pbase[G];
     float m[G], l[G];
-    __align__(16) uint8_t head[GRP][HB];          // record heads of a group
+    __align__(16) uint8_t head[GRP][CB];          // COO counts of a group's records
     int start[GRP][P];                            // offset of each slot's COO bytes in its page
     __align__(16) uint8_t sparse[SPL + 80];       // page p's COO bytes at p*SSLOT; + slack for
                                                   // whole-dword reads past a bucket
@@ -254,11 +257,19 @@ __device__ __forceinline__ T pick4(int i, T a0, T a1, T a2, T a3) {
 // every consumer masks by the page's valid-slot count.  A lane's page is a fixed lane
 // range, so its base pointer is a branch-free select of the group's uniform pointers.
 
-// One 16-byte chunk of the group's record heads: lanes 14p .. 14p+13 read page p; lanes
-// 56..63 re-read chunk 0 of page 3.  hoff = 16 * (lane % 14) for lanes < 56, else 0.
-__device__ __forceinline__ uint4 head_chunk(const Grp& gr, int lane, uint32_t hoff) {
-    const int pg = (lane >= HCH) + (lane >= 2 * HCH) + (lane >= 3 * HCH);
-    return ld16(pick4(pg, gr.base[0], gr.base[1], gr.base[2], gr.base[3]) + hoff);
+// One 16-byte chunk of the group's COO counts: lane l < 8 reads chunk l & 1 of page
+// l >> 1; the other lanes re-read the first chunk.
+__device__ __forceinline__ uint4 count_chunk(const Grp& gr, int lane) {
+    const int l = lane < 2 * GRP ? lane : 0;
+    return ld16(pick4(l >> 1, gr.base[0], gr.base[1], gr.base[2], gr.base[3]) + (uint32_t)(l & 1) * 16u);
+}
+
+// The metadata of the lane's token (lane = 16 * page + slot).  Stays in registers until
+// the group's token constants are formed.
+__device__ __forceinline__ Meta meta_words(const Grp& gr, int lane) {
+    const uint8_t* r = pick4(lane >> 4, gr.base[0], gr.base[1], gr.base[2], gr.base[3]);
+    const uint32_t* m = reinterpret_cast<const uint32_t*>(r + LY.meta + 12 * (lane & 15));
+    return Meta{m[0], m[1], m[2]};
 }
 
 // Start of each slot's COO bytes in its page, from group buffer b's counts.  Returns the
@@ -607,10 +618,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         tv[i] = fin(a.thr[(h * 2 + 1) * 4 + i]);
     }
 
-    // the first key group's heads are needed before anything else
+    // the first key group's counts and metadata are needed before anything else
     Grp gc = make_group(a, blk_lane, p_begin, p_begin, p_end, L, h, 0);
-    const uint32_t hoff = lane < GRP * HCH ? (uint32_t)(lane % HCH) * 16u : 0u;
-    uint4 hreg = head_chunk(gc, lane, hoff);
+    uint4 hreg = count_chunk(gc, lane);
+    Meta mreg = meta_words(gc, lane);
 
     // ---- query in fp32 and in fixed point -----------------------------------------
     float ssum[G], sfix[G];
@@ -629,7 +640,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         ssum[hd] = a.scale * sum;
         sfix[hd] = ldexpf(a.scale, -(sh + 7));
     }
-    if (lane < GRP * HCH) *reinterpret_cast<uint4*>(&S.head[0][16 * lane]) = hreg;
+    if (lane < 2 * GRP) *reinterpret_cast<uint4*>(&S.head[0][16 * lane]) = hreg;
     wave_sync();
 
     // Key-pass A operand: row = 8*(head%2) + 4*type + limb, type 0 -> sum q u, 1 -> sum q h.
@@ -682,7 +693,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         sparse_chunks(gc, used, lane, sreg0, sreg1);
     }
     Grp gn = make_group(a, blk_lane, p_begin, p_begin + GRP, p_end, L, h, 0);
-    hreg = head_chunk(gn, lane, hoff);
+    hreg = count_chunk(gn, lane);
     for (int g0 = p_begin; g0 < p_end; g0 += GRP) {
         const int tok0 = (g0 - p_begin) * P;
         const bool staged = fits_c;
@@ -713,8 +724,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
             // token constants of the group (lane = token) and the key correction tables,
             // while the MFMAs drain
             {
-                const int pg = lane >> 4, t = lane & 15;
-                const Tok T = token_consts(&S.head[pg][LY.meta + 12 * t], tk);
+                const Tok T = token_consts(mreg, tk);
                 S.tokc()[lane] = make_float4(T.base, T.dm, T.gp, 0.0f);
                 token_table(S, lane, T, 1.0f);
             }
@@ -755,13 +765,14 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         Grp gnn = gn;
         fits_n = true;
         if (gn.npg > 0) {
-            if (lane < GRP * HCH) *reinterpret_cast<uint4*>(&S.head[0][16 * lane]) = hreg;
+            if (lane < 2 * GRP) *reinterpret_cast<uint4*>(&S.head[0][16 * lane]) = hreg;
             wave_sync();
             const int used = group_layout(S, gn, lane, fits_n);
             wave_sync();
             sparse_chunks(gn, used, lane, sreg0, sreg1);
+            mreg = meta_words(gn, lane);
             gnn = make_group(a, blk_lane, p_begin, g0 + 2 * GRP, p_end, L, h, 0);
-            hreg = head_chunk(gnn, lane, hoff);
+            hreg = count_chunk(gnn, lane);
         }
         wave_sync();
         // sparse part
@@ -777,7 +788,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
 
     // the first value group's heads go out before the softmax
     gc = make_group(a, blk_lane, p_begin, p_begin, p_end, L, h, 1);
-    hreg = head_chunk(gc, lane, hoff);
+    hreg = count_chunk(gc, lane);
+    mreg = meta_words(gc, lane);
 
     // ---- softmax over the range ----------------------------------------------------
 #pragma unroll
@@ -801,7 +813,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         S.oci()[hd][lane] = 0;
         S.oci()[hd][lane + 64] = 0;
     }
-    if (lane < GRP * HCH) *reinterpret_cast<uint4*>(&S.head[0][16 * lane]) = hreg;
+    if (lane < 2 * GRP) *reinterpret_cast<uint4*>(&S.head[0][16 * lane]) = hreg;
     wave_sync();
 
     // ---- pass 2: values ------------------------------------------------------------
@@ -820,7 +832,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         sparse_chunks(gc, used, lane, sreg0, sreg1);
     }
     gn = make_group(a, blk_lane, p_begin, p_begin + GRP, p_end, L, h, 1);
-    hreg = head_chunk(gn, lane, hoff);
+    hreg = count_chunk(gn, lane);
     for (int g0 = p_begin; g0 < p_end; g0 += GRP) {
         const int tok0 = (g0 - p_begin) * P;
         const bool staged = fits_c;
@@ -841,7 +853,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
             const int pg = lane >> 4, t = lane & 15;
             const int nv = pick4(pg, gc.nval[0], gc.nval[1], gc.nval[2], gc.nval[3]);
             const bool vt = t < nv;
-            const Tok T = token_consts(&S.head[pg][LY.meta + 12 * t], tv);
+            const Tok T = token_consts(mreg, tv);
             float p0 = 0.0f;
 #pragma unroll
             for (int hd = 0; hd < G; ++hd) {
@@ -887,13 +899,14 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         Grp gnn = gn;
         fits_n = true;
         if (gn.npg > 0) {
-            if (lane < GRP * HCH) *reinterpret_cast<uint4*>(&S.head[0][16 * lane]) = hreg;
+            if (lane < 2 * GRP) *reinterpret_cast<uint4*>(&S.head[0][16 * lane]) = hreg;
             wave_sync();
             const int used = group_layout(S, gn, lane, fits_n);
             wave_sync();
             sparse_chunks(gn, used, lane, sreg0, sreg1);
+            mreg = meta_words(gn, lane);
             gnn = make_group(a, blk_lane, p_begin, g0 + 2 * GRP, p_end, L, h, 1);
-            hreg = head_chunk(gnn, lane, hoff);
+            hreg = count_chunk(gnn, lane);
         }
         wave_sync();
         v4i gacc[8];
