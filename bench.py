@@ -35,6 +35,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", type=int, default=3, help="1..5 (3 = batch-256 Llama-2-13B layer)")
+    ap.add_argument("--window", type=int, default=0,
+                    help="sliding window in tokens (0: attend over the whole sequence)")
     ap.add_argument("--cpu-sample-seqs", type=int, default=128)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -121,14 +123,15 @@ def main():
     max_len = int(lens.max())
     scale = float(np.float32(1.0 / math.sqrt(d)))
     out = torch.empty(n, Hq, d, dtype=torch.float32, device=dev)
-    ws_bytes = B.attention_workspace_bytes(n, Hq, H, d, max_len)
+    win = max(0, args.window)
+    ws_bytes = B.attention_workspace_bytes(n, Hq, H, d, max_len, win)
     ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
 
     def step(ev=None):
         B.quantize_kv(cache, k_new, v_new, bt, start, cu1, 1)
         if ev is not None:
             ev[0].record()
-        B.decode_attention(cache, q, bt, lens_d, max_len, scale, out=out, workspace=ws)
+        B.decode_attention(cache, q, bt, lens_d, max_len, scale, out=out, workspace=ws, window=win)
         if ev is not None:
             ev[1].record()
 
@@ -161,21 +164,26 @@ def main():
     stride = cache.stride
     rec = cache.pool.view(nblk, H, 2, stride)
     counts = rec[:, :, :, : P * nc].reshape(nblk, H, 2, P, nc).to(torch.int32).sum(-1)  # [blk,H,2,P]
+    # (only the keys a query sees: with a sliding window, the last `win` of each sequence)
     valid = torch.zeros(nblk, P, dtype=torch.bool)
+    seen = [min(int(L), win) if win else int(L) for L in lens]
+    n_pages_read = 0
     for s in range(n):
         L = int(lens[s])
-        for pg in range((L + P - 1) // P):
-            m = min(P, L - pg * P)
-            valid[int(bt_cpu[s, pg]), :m] = True
+        lo = L - seen[s]
+        for pg in range(lo // P, (L + P - 1) // P):
+            t0_, t1_ = max(lo - pg * P, 0), min(P, L - pg * P)
+            valid[int(bt_cpu[s, pg]), t0_:t1_] = True
+            n_pages_read += 1
     n_out = int((counts * valid.to(dev)[:, None, None, :]).sum())
-    n_vec = int(lens.sum()) * H * 2
+    n_vec = sum(seen) * H * 2
     kv_bytes = n_vec * (d // 2 + nc + 12) + n_out
-    aux_bytes = n * Hq * d * (2 + 4) + sum((int(L) + P - 1) // P for L in lens) * 4 + n * 4
+    aux_bytes = n * Hq * d * (2 + 4) + n_pages_read * 4 + n * 4
     aux_bytes += 2 * ws_bytes          # split partials: written once, read once by the combine
     alg_bytes = kv_bytes + aux_bytes
     achieved = alg_bytes / attn_avg_s / 1e9
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": stored_traffic(w.name),
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": stored_traffic(w.name) if not win else None,
                 "bytes_per_launch": alg_bytes, "kernel_us": round(attn_avg_s * 1e6, 2),
                 "outlier_fraction": round(n_out / (n_vec * d), 4)}
 
@@ -210,7 +218,7 @@ def main():
         for _ in range(3):   # median of three steps (re-quantizing the same slot is idempotent)
             t0 = time.perf_counter()
             oracle.quantize_kv(pool_s, off, P, H, d, thr_np, kn, vn, bt_s, pre, np.arange(S + 1, dtype=np.int32))
-            want = oracle.decode_attention(pool_s, off, P, H, d, thr_np, qs, bt_s, lens_s, scale)
+            want = oracle.decode_attention(pool_s, off, P, H, d, thr_np, qs, bt_s, lens_s, scale, window=win)
             times.append(time.perf_counter() - t0)
         cpu_s = sorted(times)[1]
         cpu = {"value": round(S / cpu_s, 2), "unit": "tokens/s", "cores": oracle.max_threads(),
@@ -238,7 +246,9 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{w.name}: batch {n}, {Hq} query / {H} KV heads, head_dim {d}, "
                                f"context {w.ctx_min}..{w.ctx} incl. the new token, 16-token pages, "
-                               f"shuffled block table; step = quantize 1 token/seq + attention",
+                               f"shuffled block table"
+                               + (f", sliding window {win}" if win else "")
+                               + "; step = quantize 1 token/seq + attention",
                    "global_batch": n, "seq_len": max_len, "parallelism": "single GPU"},
         "roofline": roofline,
         "cpu_baseline": cpu,

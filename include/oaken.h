@@ -156,6 +156,27 @@ int oaken_decode_attention(const oaken_cache* cache, const void* q, int32_t n_q_
                            float softmax_scale, float* out, void* workspace,
                            size_t workspace_bytes, void* stream);
 
+/*
+ * Sliding-window decode attention (the Mistral and Mixtral models of Sec. 6.1 attend
+ * over a sliding window).  Same as oaken_decode_attention, except that sequence s
+ * attends only over its last sliding_window keys:
+ *   t in [max(0, seq_lens[s] - sliding_window), seq_lens[s]).
+ * sliding_window = 0 means the whole sequence (oaken_decode_attention itself);
+ * negative values are rejected.  Keys outside the window are neither read nor
+ * weighted; pages wholly before the window are skipped.  workspace:
+ * oaken_attention_workspace_bytes_window(..., sliding_window) bytes, which depends
+ * on the window (the split plan covers only the pages a window can span).
+ */
+size_t oaken_attention_workspace_bytes_window(int32_t n_seqs, int32_t n_q_heads, int32_t n_kv_heads,
+                                              int32_t head_dim, int32_t max_seq_len,
+                                              int32_t sliding_window);
+
+int oaken_decode_attention_window(const oaken_cache* cache, const void* q, int32_t n_q_heads,
+                                  const int32_t* block_table, int32_t max_blocks_per_seq,
+                                  const int32_t* seq_lens, int32_t n_seqs, int32_t max_seq_len,
+                                  int32_t sliding_window, float softmax_scale, float* out,
+                                  void* workspace, size_t workspace_bytes, void* stream);
+
 /* Static description of a status code. */
 const char* oaken_status_string(int status);
 

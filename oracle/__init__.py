@@ -56,7 +56,7 @@ def _load():
     lib.oaken_ref_dequantize_slot.argtypes = [P, i32, i32, i32, i32, P, P, P]
     lib.oaken_ref_dequantize_slot.restype = None
     lib.oaken_ref_decode_attention.argtypes = [P, i32, i32, i32, i32, i64, P, P, i32, P, i32, P,
-                                               i32, f32, P]
+                                               i32, i32, f32, P]
     lib.oaken_ref_decode_attention.restype = i32
     lib.oaken_ref_calibrate.argtypes = [P, P, i32, i32, i32, i32, f32, f32, P]
     lib.oaken_ref_calibrate.restype = i32
@@ -150,8 +150,10 @@ def dequantize_slot(pool, P, H, d, thresholds, blk, h, which, slot, return_group
     return (out, grp) if return_groups else out
 
 
-def decode_attention(pool, num_blocks, P, H, d, thresholds, q, block_table, seq_lens, scale):
-    """fp64 softmax(q K^T scale) V over the dequantized cache; returns fp32 [n_seqs, Hq, d]."""
+def decode_attention(pool, num_blocks, P, H, d, thresholds, q, block_table, seq_lens, scale, window=0):
+    """fp64 softmax(q K^T scale) V over the dequantized cache; returns fp32 [n_seqs, Hq, d].
+
+    window > 0 restricts sequence s to its last `window` keys (sliding-window attention)."""
     lay = layout(P, d)
     thr = np.ascontiguousarray(np.asarray(thresholds, np.float32))
     qb = _bits16(q)
@@ -161,7 +163,7 @@ def decode_attention(pool, num_blocks, P, H, d, thresholds, q, block_table, seq_
     out = np.zeros((n_seqs, Hq, d), np.float32)
     rc = _load().oaken_ref_decode_attention(_ptr(pool), num_blocks, P, H, d, lay["stride"],
                                             _ptr(thr), _ptr(qb), Hq, _ptr(bt), bt.shape[1],
-                                            _ptr(sl), n_seqs, float(scale), _ptr(out))
+                                            _ptr(sl), n_seqs, int(window), float(scale), _ptr(out))
     if rc != 0:
         raise ValueError("oracle decode_attention: invalid arguments")
     return out

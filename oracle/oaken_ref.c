@@ -316,12 +316,16 @@ void oaken_ref_dequantize_slot(const uint8_t* rec, int which, int P, int d, int 
 /* Decode attention over the dequantized cache (Sec. 2.1: the new query is   */
 /* multiplied with every cached key, softmax, then weighted sum of values).  */
 /* Query head h reads KV head h / (Hq / H).  fp64 throughout.               */
+/* With a sliding window W > 0 (the Mistral/Mixtral models of Sec. 6.1) the  */
+/* query at position L-1 sees only keys t with L-W <= t < L; W <= 0 means    */
+/* the whole sequence.                                                       */
 /* ------------------------------------------------------------------------ */
 
 int oaken_ref_decode_attention(const uint8_t* pool, int num_blocks, int P, int H, int d,
                                int64_t stride, const float* thr, const uint16_t* q, int Hq,
                                const int32_t* block_table, int max_blocks,
-                               const int32_t* seq_lens, int n_seqs, float scale, float* out)
+                               const int32_t* seq_lens, int n_seqs, int window, float scale,
+                               float* out)
 {
     if (Hq % H != 0) return -1;
     const int G = Hq / H;
@@ -330,6 +334,7 @@ int oaken_ref_decode_attention(const uint8_t* pool, int num_blocks, int P, int H
     for (int s = 0; s < n_seqs; ++s)
         for (int h = 0; h < H; ++h) {
             const int Ls = seq_lens[s];
+            const int t0 = (window > 0 && Ls > window) ? Ls - window : 0;   /* first key seen */
             double* kv = (double*)malloc(sizeof(double) * d);
             double* sc = (double*)malloc(sizeof(double) * (size_t)Ls * G);
             double* acc = (double*)calloc((size_t)G * d, sizeof(double));
@@ -338,7 +343,7 @@ int oaken_ref_decode_attention(const uint8_t* pool, int num_blocks, int P, int H
                 for (int j = 0; j < d; ++j)
                     qd[gq * d + j] = oaken_ref_half_to_float(q[((int64_t)s * Hq + h * G + gq) * d + j]);
             int ok = Ls >= 1 && (Ls + P - 1) / P <= max_blocks;
-            for (int t = 0; ok && t < Ls; ++t) {
+            for (int t = t0; ok && t < Ls; ++t) {
                 int blk = block_table[(int64_t)s * max_blocks + t / P];
                 if (blk < 0 || blk >= num_blocks) { ok = 0; break; }
                 const uint8_t* rec = pool + (((int64_t)blk * H + h) * 2 + 0) * stride;
@@ -352,16 +357,16 @@ int oaken_ref_decode_attention(const uint8_t* pool, int num_blocks, int P, int H
             if (ok) {
                 for (int gq = 0; gq < G; ++gq) {
                     double m = -INFINITY;
-                    for (int t = 0; t < Ls; ++t) if (sc[(int64_t)gq * Ls + t] > m) m = sc[(int64_t)gq * Ls + t];
+                    for (int t = t0; t < Ls; ++t) if (sc[(int64_t)gq * Ls + t] > m) m = sc[(int64_t)gq * Ls + t];
                     double l = 0.0;
-                    for (int t = 0; t < Ls; ++t) {
+                    for (int t = t0; t < Ls; ++t) {
                         double p = exp(sc[(int64_t)gq * Ls + t] - m);
                         sc[(int64_t)gq * Ls + t] = p;
                         l += p;
                     }
-                    for (int t = 0; t < Ls; ++t) sc[(int64_t)gq * Ls + t] /= l;
+                    for (int t = t0; t < Ls; ++t) sc[(int64_t)gq * Ls + t] /= l;
                 }
-                for (int t = 0; t < Ls; ++t) {
+                for (int t = t0; t < Ls; ++t) {
                     int blk = block_table[(int64_t)s * max_blocks + t / P];
                     const uint8_t* rec = pool + (((int64_t)blk * H + h) * 2 + 1) * stride;
                     oaken_ref_dequantize_slot(rec, 1, P, d, t % P, thr + (h * 2 + 1) * 4, kv, NULL);

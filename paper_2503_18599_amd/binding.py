@@ -62,6 +62,11 @@ def lib():
     L.oaken_decode_attention.argtypes = [ctypes.POINTER(_CacheStruct), P, i32, P, i32, P, i32, i32,
                                          f32, P, P, sz, P]
     L.oaken_decode_attention.restype = ctypes.c_int
+    L.oaken_attention_workspace_bytes_window.argtypes = [i32, i32, i32, i32, i32, i32]
+    L.oaken_attention_workspace_bytes_window.restype = sz
+    L.oaken_decode_attention_window.argtypes = [ctypes.POINTER(_CacheStruct), P, i32, P, i32, P, i32, i32,
+                                                i32, f32, P, P, sz, P]
+    L.oaken_decode_attention_window.restype = ctypes.c_int
     L.oaken_status_string.argtypes = [ctypes.c_int]
     L.oaken_status_string.restype = ctypes.c_char_p
     L.oaken_last_error.argtypes = []
@@ -160,25 +165,35 @@ def quantize_kv(cache: Cache, k_new: torch.Tensor, v_new: torch.Tensor, block_ta
         n_seqs, n_tokens, int(max_new_per_seq), _stream()))
 
 
-def attention_workspace_bytes(n_seqs, n_q_heads, n_kv_heads, head_dim, max_seq_len) -> int:
+def attention_workspace_bytes(n_seqs, n_q_heads, n_kv_heads, head_dim, max_seq_len, window: int = 0) -> int:
+    if window:
+        return int(lib().oaken_attention_workspace_bytes_window(n_seqs, n_q_heads, n_kv_heads, head_dim,
+                                                                max_seq_len, int(window)))
     return int(lib().oaken_attention_workspace_bytes(n_seqs, n_q_heads, n_kv_heads, head_dim, max_seq_len))
 
 
 def decode_attention(cache: Cache, q: torch.Tensor, block_table: torch.Tensor, seq_lens: torch.Tensor,
                      max_seq_len: int, scale: float, out: torch.Tensor | None = None,
-                     workspace: torch.Tensor | None = None) -> torch.Tensor:
-    """fp16 q [n_seqs][Hq][d] -> fp32 out [n_seqs][Hq][d]."""
+                     workspace: torch.Tensor | None = None, window: int = 0) -> torch.Tensor:
+    """fp16 q [n_seqs][Hq][d] -> fp32 out [n_seqs][Hq][d].  window > 0: sliding-window
+    attention over each sequence's last `window` keys."""
     n_seqs, Hq, d = q.shape
     if d != cache.head_dim or seq_lens.numel() != n_seqs or block_table.shape[0] != n_seqs:
         raise ValueError("q / seq_lens / block_table shapes disagree")
     if out is None:
         out = torch.empty(n_seqs, Hq, d, dtype=torch.float32, device=q.device)
-    ws_bytes = attention_workspace_bytes(n_seqs, Hq, cache.n_kv_heads, d, max_seq_len)
+    ws_bytes = attention_workspace_bytes(n_seqs, Hq, cache.n_kv_heads, d, max_seq_len, window)
     if ws_bytes and (workspace is None or workspace.numel() < ws_bytes):
         workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
     ws_ptr = workspace.data_ptr() if (ws_bytes and workspace is not None) else None
-    _check(lib().oaken_decode_attention(
-        cache.struct, _dev(q, torch.float16, "q"), Hq, _dev(block_table, torch.int32, "block_table"),
-        block_table.shape[1], _dev(seq_lens, torch.int32, "seq_lens"), n_seqs, int(max_seq_len),
-        float(scale), _dev(out, torch.float32, "out"), ws_ptr, ws_bytes, _stream()))
+    if window:
+        _check(lib().oaken_decode_attention_window(
+            cache.struct, _dev(q, torch.float16, "q"), Hq, _dev(block_table, torch.int32, "block_table"),
+            block_table.shape[1], _dev(seq_lens, torch.int32, "seq_lens"), n_seqs, int(max_seq_len),
+            int(window), float(scale), _dev(out, torch.float32, "out"), ws_ptr, ws_bytes, _stream()))
+    else:
+        _check(lib().oaken_decode_attention(
+            cache.struct, _dev(q, torch.float16, "q"), Hq, _dev(block_table, torch.int32, "block_table"),
+            block_table.shape[1], _dev(seq_lens, torch.int32, "seq_lens"), n_seqs, int(max_seq_len),
+            float(scale), _dev(out, torch.float32, "out"), ws_ptr, ws_bytes, _stream()))
     return out

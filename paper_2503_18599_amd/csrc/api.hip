@@ -3,6 +3,7 @@
 #include "oaken.h"
 #include "oaken_internal.h"
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -27,6 +28,14 @@ int ok() {
 }
 
 bool supported_dim(int32_t d) { return d == 64 || d == 128; }
+
+// Tokens the split plan must cover per sequence: a window of W keys can straddle
+// (W - 1) / P + 2 pages.
+int32_t attention_span(int32_t max_seq_len, int32_t window) {
+    if (window <= 0) return max_seq_len;
+    const int64_t pages = (int64_t)(window - 1) / oaken::kPage + 2;
+    return (int32_t)std::min<int64_t>(max_seq_len, pages * oaken::kPage);
+}
 
 int check_cache(const oaken_cache* c) {
     if (!c) return fail(OAKEN_ERR_INVALID_ARG, "cache is NULL");
@@ -79,10 +88,17 @@ size_t oaken_calibrate_workspace_bytes(int32_t n_runs, int32_t n_kv_heads) {
 
 size_t oaken_attention_workspace_bytes(int32_t n_seqs, int32_t n_q_heads, int32_t n_kv_heads,
                                        int32_t head_dim, int32_t max_seq_len) {
+    return oaken_attention_workspace_bytes_window(n_seqs, n_q_heads, n_kv_heads, head_dim, max_seq_len, 0);
+}
+
+size_t oaken_attention_workspace_bytes_window(int32_t n_seqs, int32_t n_q_heads, int32_t n_kv_heads,
+                                              int32_t head_dim, int32_t max_seq_len,
+                                              int32_t sliding_window) {
     if (n_seqs <= 0 || n_q_heads <= 0 || n_kv_heads <= 0 || n_q_heads % n_kv_heads != 0 ||
         !supported_dim(head_dim) || max_seq_len <= 0)
         return 0;
-    const oaken::SplitPlan sp = oaken::plan_splits(n_seqs, n_q_heads, n_kv_heads, head_dim, max_seq_len);
+    const oaken::SplitPlan sp = oaken::plan_splits(n_seqs, n_q_heads, n_kv_heads, head_dim,
+                                                   attention_span(max_seq_len, sliding_window));
     if (sp.n_splits <= 1) return 0;
     return (size_t)n_seqs * n_q_heads * sp.n_splits * (head_dim + 2) * sizeof(float);
 }
@@ -157,6 +173,16 @@ int oaken_decode_attention(const oaken_cache* cache, const void* q, int32_t n_q_
                            const int32_t* seq_lens, int32_t n_seqs, int32_t max_seq_len,
                            float softmax_scale, float* out, void* workspace,
                            size_t workspace_bytes, void* stream) {
+    return oaken_decode_attention_window(cache, q, n_q_heads, block_table, max_blocks_per_seq, seq_lens,
+                                         n_seqs, max_seq_len, 0, softmax_scale, out, workspace,
+                                         workspace_bytes, stream);
+}
+
+int oaken_decode_attention_window(const oaken_cache* cache, const void* q, int32_t n_q_heads,
+                                  const int32_t* block_table, int32_t max_blocks_per_seq,
+                                  const int32_t* seq_lens, int32_t n_seqs, int32_t max_seq_len,
+                                  int32_t sliding_window, float softmax_scale, float* out,
+                                  void* workspace, size_t workspace_bytes, void* stream) {
     int st = check_cache(cache);
     if (st != OAKEN_OK) return st;
     if (!q || !block_table || !seq_lens || !out)
@@ -171,12 +197,13 @@ int oaken_decode_attention(const oaken_cache* cache, const void* q, int32_t n_q_
     if ((int64_t)max_blocks_per_seq * oaken::kPage < max_seq_len)
         return fail(OAKEN_ERR_INVALID_ARG, "block table too narrow for max_seq_len");
     if (!std::isfinite(softmax_scale)) return fail(OAKEN_ERR_INVALID_ARG, "softmax_scale not finite");
-    const size_t need = oaken_attention_workspace_bytes(n_seqs, n_q_heads, cache->n_kv_heads,
-                                                        cache->head_dim, max_seq_len);
+    if (sliding_window < 0) return fail(OAKEN_ERR_INVALID_ARG, "sliding_window must be >= 0");
+    const size_t need = oaken_attention_workspace_bytes_window(n_seqs, n_q_heads, cache->n_kv_heads,
+                                                               cache->head_dim, max_seq_len, sliding_window);
     if (need > 0 && (!workspace || workspace_bytes < need))
         return fail(OAKEN_ERR_WORKSPACE, "attention workspace %zu < %zu bytes", workspace_bytes, need);
-    const oaken::SplitPlan sp = oaken::plan_splits(n_seqs, n_q_heads, cache->n_kv_heads,
-                                                   cache->head_dim, max_seq_len);
+    const oaken::SplitPlan sp = oaken::plan_splits(n_seqs, n_q_heads, cache->n_kv_heads, cache->head_dim,
+                                                   attention_span(max_seq_len, sliding_window));
     oaken::AttnArgs a{};
     a.pool = static_cast<const uint8_t*>(cache->pool);
     a.thr = cache->thresholds;
@@ -194,6 +221,7 @@ int oaken_decode_attention(const oaken_cache* cache, const void* q, int32_t n_q_
     a.max_seq_len = max_seq_len;
     a.pages_per_split = sp.pages_per_split;
     a.n_splits = sp.n_splits;
+    a.window = sliding_window;
     a.scale = softmax_scale;
     return hip_status(oaken::launch_attention(a, cache->head_dim, static_cast<hipStream_t>(stream)),
                       "attention launch");

@@ -101,7 +101,9 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
     int L = a.seq_lens[s];
     L = max(0, min(L, min(a.max_seq_len, a.max_blocks * kPage)));
     const int n_pages = (L + kPage - 1) / kPage;
-    const int p_begin = split * a.pages_per_split;
+    // a sliding window hides keys before lo; the ranges start at its first page
+    const int lo = (a.window > 0 && L > a.window) ? L - a.window : 0;
+    const int p_begin = lo / kPage + split * a.pages_per_split;
     const int p_end = min(n_pages, p_begin + a.pages_per_split);
     const int n_tok = max(0, min(L, p_end * kPage) - p_begin * kPage);
     const int tok_cap = a.pages_per_split * kPage;
@@ -136,7 +138,7 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
 #pragma unroll
             for (int o = 8; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
             const int tok = (p - p_begin) * kPage + t;
-            const bool valid = ok && (p * kPage + t) < L;
+            const bool valid = ok && (p * kPage + t) < L && (p * kPage + t) >= lo;
             if (part == 0) s_scores[g * tok_cap + tok] = valid ? v * a.scale : -INFINITY;
         }
         __syncthreads();

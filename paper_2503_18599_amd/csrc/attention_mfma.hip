@@ -603,7 +603,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
     const int split = blockIdx.x, h = blockIdx.y, s = blockIdx.z;
     const int L = max(0, min(a.seq_lens[s], min(a.max_seq_len, a.max_blocks * P)));
     const int n_pages = (L + P - 1) / P;
-    const int p_begin = split * a.pages_per_split;
+    // a sliding window hides keys before lo; the ranges start at its first page
+    const int lo = (a.window > 0 && L > a.window) ? L - a.window : 0;
+    const int p_begin = lo / P + split * a.pages_per_split;
     const int p_end = min(n_pages, p_begin + a.pages_per_split);
     const int cap = a.pages_per_split * P;
     const int n_tok = max(0, min(L, p_end * P) - p_begin * P);
@@ -737,7 +739,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
 #pragma unroll
             for (int pg = 0; pg < GRP; ++pg) {
                 const float4 tc = S.tokc()[pg * P + t];
-                const bool valid = t < gc.nval[pg];
+                const bool valid = t < gc.nval[pg] && (g0 + pg) * P + t >= lo;
 #pragma unroll
                 for (int rs = 0; rs < NRS; ++rs) {
                     const float v = limbs(acc[pg][rs]);

@@ -57,6 +57,7 @@ struct AttnArgs {
     int64_t stride;
     int32_t num_blocks, H, Hq, max_blocks, n_seqs, max_seq_len;
     int32_t pages_per_split, n_splits;
+    int32_t window;               // sliding window in tokens (<= 0: the whole sequence)
     float scale;
 };
 

@@ -8,7 +8,8 @@ A sample of sequences is checked against the oracle:
 - their page records (counts, scales, nibbles, COO bytes) bit for bit;
 - their attention outputs within |gpu - ref| <= 2e-3 + 1e-2 |ref|.
 
-The sample includes the shortest and the longest sequence when lengths vary.
+The sample includes the shortest and the longest sequence when lengths vary.  The
+Mistral-shaped workload is also checked under Mistral-7B's 4096-token sliding window.
 """
 import math
 
@@ -44,8 +45,8 @@ def _sample(lens: torch.Tensor, n: int):
     return sorted(picks)
 
 
-@pytest.mark.parametrize("cid,n_sample", [(3, 6), (4, 6), (5, 2)])
-def test_full_size_sampled_parity(B, ref, cid, n_sample):
+@pytest.mark.parametrize("cid,n_sample,window", [(3, 6, 0), (4, 6, 4096), (5, 2, 0)])
+def test_full_size_sampled_parity(B, ref, cid, n_sample, window):
     w = synth.WORKLOADS[cid]
     H, Hq, d = w.n_kv_heads, w.n_q_heads, w.head_dim
     n = w.n_seqs
@@ -122,9 +123,18 @@ def test_full_size_sampled_parity(B, ref, cid, n_sample):
                     n_checked += 1
     assert n_checked == sum(nb_s) * H * 2
 
-    want_out = ref.decode_attention(pool_s, off, P, H, d, thr_np, np16(q)[sample], bt_s,
-                                    np.array([int(lens[s]) for s in sample], np.int32), scale)
+    lens_s = np.array([int(lens[s]) for s in sample], np.int32)
+    want_out = ref.decode_attention(pool_s, off, P, H, d, thr_np, np16(q)[sample], bt_s, lens_s, scale)
     ok, max_abs, max_rel = attention_tolerance(out[sample], want_out)
     print(f"workload {w.name}: {S} sequences, {n_checked} records bit-exact, "
           f"attention max_abs={max_abs:.3e} max_rel={max_rel:.3e}")
     assert ok, (max_abs, max_rel)
+
+    if window:
+        # the same cache under the model's sliding window
+        out_w = B.decode_attention(cache, q, bt, lens.to(DEV), int(lens.max()), scale, window=window)
+        want_w = ref.decode_attention(pool_s, off, P, H, d, thr_np, np16(q)[sample], bt_s, lens_s, scale,
+                                      window=window)
+        ok, max_abs, max_rel = attention_tolerance(out_w.cpu().numpy()[sample], want_w)
+        print(f"  window {window}: attention max_abs={max_abs:.3e} max_rel={max_rel:.3e}")
+        assert ok, (max_abs, max_rel)

@@ -170,6 +170,43 @@ def test_attention_single_token_and_ragged(B, ref):
     assert ok, (max_abs, max_rel)
 
 
+@pytest.mark.parametrize("name,window", [("tiny", 1), ("tiny", 5), ("llama2-7b", 17), ("llama2-13b", 1000),
+                                         ("mistral-gqa", 16), ("mistral-gqa", 513), ("llama3-32k", 2049),
+                                         ("llama2-13b-wide", 20)])
+def test_attention_sliding_window(B, ref, name, window):
+    """Sliding-window attention (keys L-W .. L-1) against the oracle: windows shorter than
+    a page, straddling page boundaries, and longer than some of the sequences."""
+    case = _case(ref, name)
+    pool_ref = case.oracle_pool(ref)
+    cache, bt = _gpu_cache(B, case)
+    q = synth.queries(case.w)
+    scale = float(np.float32(1.0 / math.sqrt(case.d)))
+    want = ref.decode_attention(pool_ref, case.num_blocks, 16, case.H, case.d, case.thr, np16(q),
+                                case.bt.numpy(), case.lens.numpy(), scale, window=window)
+    got = B.decode_attention(cache, q.to(DEV), bt, case.lens.to(DEV), int(case.lens.max()), scale, window=window)
+    ok, max_abs, max_rel = attention_tolerance(got.cpu().numpy(), want)
+    print(f"{name} window {window}: max_abs={max_abs:.3e} max_rel={max_rel:.3e}")
+    assert ok, (max_abs, max_rel)
+
+
+def test_attention_sliding_window_ragged(B, ref):
+    """Windows of 1, 15, 16, 17 and L tokens over lengths that are page multiples and
+    ragged; max_seq_len larger than every length."""
+    w = synth.scaled(synth.WORKLOADS[4], n_seqs=6)
+    case = Case(w, lens=[1, 16, 17, 31, 64, 250])
+    case.calibrate_oracle(ref)
+    pool_ref = case.oracle_pool(ref)
+    cache, bt = _gpu_cache(B, case)
+    q = synth.queries(case.w)
+    for window in (1, 15, 16, 17, 250):
+        want = ref.decode_attention(pool_ref, case.num_blocks, 16, case.H, case.d, case.thr, np16(q),
+                                    case.bt.numpy(), case.lens.numpy(), 0.088, window=window)
+        got = B.decode_attention(cache, q.to(DEV), bt, case.lens.to(DEV), case.max_blocks * 16, 0.088,
+                                 window=window)
+        ok, max_abs, max_rel = attention_tolerance(got.cpu().numpy(), want)
+        assert ok, (window, max_abs, max_rel)
+
+
 @pytest.mark.parametrize("mode", ["all-outliers", "no-inner", "mixed"])
 def test_attention_edge_thresholds(B, ref, mode):
     """Attention over extreme COO loads: every value an outlier (the largest page groups,

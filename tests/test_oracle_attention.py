@@ -181,3 +181,33 @@ def test_record_field_layout(ref):
                         byte, high = j * P // 2 + t // 2, t & 1
                     b = int(rec[lay["dense"] + byte])
                     assert ((b >> 4) if high else (b & 15)) == (int(r["code"][j]) & 15)
+
+
+def test_sliding_window_pins(ref):
+    """Sliding window W (the Mistral/Mixtral models of Sec. 6.1): the query at position L-1
+    sees keys L-W .. L-1.  Pinned three ways:
+    - W >= L is the full attention;
+    - W = 1 returns the last token's dequantized value;
+    - quantization is per token, so windowed attention over L tokens equals plain
+      attention over a fresh cache holding only the last W tokens (relocation)."""
+    rng = np.random.default_rng(41)
+    H, d, Hq = 2, 64, 4
+    lens = [53, 40, 7]
+    pool, total, bt, thr, k, v, cu = _build(ref, rng, 3, H, d, lens)
+    q = rng.standard_normal((3, Hq, d)).astype(np.float16)
+    full = ref.decode_attention(pool, total, P, H, d, thr, q, bt, lens, 0.125)
+    assert np.array_equal(ref.decode_attention(pool, total, P, H, d, thr, q, bt, lens, 0.125, window=64), full)
+    last = ref.decode_attention(pool, total, P, H, d, thr, q, bt, lens, 0.125, window=1)
+    for s in range(3):
+        for hq in range(Hq):
+            want = _dq(ref, pool, H, d, thr, bt, s, lens[s] - 1, hq // (Hq // H), 1)
+            assert np.array_equal(last[s, hq], want.astype(np.float32))
+    for W in (5, 16, 17, 33):
+        win = ref.decode_attention(pool, total, P, H, d, thr, q, bt, lens, 0.125, window=W)
+        keep = [min(W, L) for L in lens]
+        rows = np.concatenate([np.arange(cu[s + 1] - keep[s], cu[s + 1]) for s in range(3)])
+        pool2, total2, bt2, _, _, _, _ = _build(ref, rng, 3, H, d, keep, thr=thr, k=k[rows], v=v[rows])
+        want = ref.decode_attention(pool2, total2, P, H, d, thr, q, bt2, keep, 0.125)
+        assert np.allclose(win, want, rtol=1e-6, atol=1e-7), W
+        if W < min(lens):
+            assert not np.allclose(win, full, atol=1e-4)
