@@ -40,6 +40,7 @@ constexpr int P = kPage;
 constexpr Layout LY = make_layout(P, D);   // counts 0, meta 32, dense 224, sparse 1248
 constexpr int HB = 224;                    // counts + meta bytes at the start of a record
 constexpr int CB = 32;                     // COO count bytes at the start of a record
+constexpr int cmax(int x, int y) { return x > y ? x : y; }
 constexpr int GRP = 4;                     // pages per group (two correction pairs)
 constexpr int GT = GRP * P;                // tokens per group
 constexpr int PSTR = 1024;                 // LDS stride of a page's dense bytes
@@ -189,13 +190,14 @@ __device__ __forceinline__ uint4 ld16(const uint8_t* p) {
 // Buffers live only in the phase that needs them share storage, which keeps the wave's
 // LDS small enough for more waves per CU: the fixed-point query (qi) is read only
 // before the key pass and sits in the table's space; q (key pass) shares with oci (value
-// pass); tokc (key pass) shares with wv and oc (value pass).
+// pass); tokc (key pass) shares with wv (value pass) and, after the value pass, with the
+// value corrections on their way to the output lanes.
 template <int G>
 struct Smem {
     __align__(16) uint8_t tab_[4 * GT * 2 * 8];   // tab float2 [COO class][token][nibble bit 3]; qi
     __align__(16) uint8_t dense[GRP][PSTR];       // K: token rows of 64 bytes; V: channel rows of 8
     __align__(16) uint8_t qo_[G * D * 4];         // q float [G][D] (keys); oci int [G][D] (values)
-    __align__(16) uint8_t tw_[(G * D * 4 + G * GT * 8) > GT * 16 ? (G * D * 4 + G * GT * 8) : GT * 16];
+    __align__(16) uint8_t tw_[cmax(cmax(GT * 16, G * GT * 8), G * D * 4)];
     float pbase[G];
     float m[G], l[G];
     __align__(16) uint8_t head[GRP][CB];          // COO counts of a group's records
@@ -207,16 +209,16 @@ struct Smem {
     __device__ float2 (&tab())[4][GT][2] { return *reinterpret_cast<float2 (*)[4][GT][2]>(tab_); }
     // query in fixed point (before the key pass)
     __device__ int (&qi())[G][D] { return *reinterpret_cast<int (*)[G][D]>(tab_); }
-    // query in fp32 (key pass)
-    __device__ float (&q())[G][D] { return *reinterpret_cast<float (*)[G][D]>(qo_); }
+    // query in fp32, the heads of a channel side by side (key pass)
+    __device__ float (&q())[D][G] { return *reinterpret_cast<float (*)[D][G]>(qo_); }
     // value corrections of one group, fixed point (value pass)
     __device__ int (&oci())[G][D] { return *reinterpret_cast<int (*)[G][D]>(qo_); }
     // base, Delta, Gp of the group's tokens (key pass)
     __device__ float4 (&tokc())[GT] { return *reinterpret_cast<float4 (*)[GT]>(tw_); }
-    // value corrections (value pass)
-    __device__ float (&oc())[G][D] { return *reinterpret_cast<float (*)[G][D]>(tw_); }
     // value-pass weights of token pairs: 4 features, 4 limbs (value pass)
-    __device__ uint4 (&wv())[G][GT / 2] { return *reinterpret_cast<uint4 (*)[G][GT / 2]>(tw_ + G * D * 4); }
+    __device__ uint4 (&wv())[G][GT / 2] { return *reinterpret_cast<uint4 (*)[G][GT / 2]>(tw_); }
+    // value corrections, handed to the output lanes (after the value pass)
+    __device__ float (&oc())[G][D] { return *reinterpret_cast<float (*)[G][D]>(tw_); }
 };
 
 // Wave-uniform description of a group of consecutive pages of one sequence.
@@ -382,7 +384,8 @@ __device__ __forceinline__ void key_corrections(Smem<G>& S, float* sc, int cap, 
 #pragma unroll
         for (int hd = 0; hd < G; ++hd) corr[nb][hd] = 0.0f;
     }
-    const uint32_t qc = off_of(S, &S.q()[0][((lane >> 4) & 1) * 64]);
+    const uint32_t qc = off_of(S, &S.q()[((lane >> 4) & 1) * 64][0]);
+    constexpr int LG = G == 1 ? 0 : G == 2 ? 1 : 2;   // log2 G: one channel's heads span 4G bytes
     const int maxc = wave_max_i(mc);
     // The entry in bits o..o+7 of ent: index j (6 bits), class (2 bits).  Every slot is
     // computed; slots past the bucket get a zero weight (no branches).
@@ -390,10 +393,10 @@ __device__ __forceinline__ void key_corrections(Smem<G>& S, float* sc, int cap, 
         const uint32_t dw = lds_at<uint32_t>(S, drow[nb] | (shr(ent, o + 1) & 0x1cu));
         const uint32_t n = __builtin_amdgcn_ubfe(dw, ((ent >> o) & 0xffu) << 2, 4);
         const float delta = entry_delta(S, tbo[nb], ent, o, n);
-        const uint32_t qo = qc | (shr(ent, o - 2) & 0xfcu);
+        const uint32_t qo = qc | (shr(ent, o - 2 - LG) & (0xfcu << LG));
 #pragma unroll
         for (int hd = 0; hd < G; ++hd) {
-            const float q = lds_at<float>(S, qo + hd * D * 4);
+            const float q = lds_at<float>(S, qo + hd * 4);
             corr[nb][hd] = fmaf(valid ? q : 0.0f, delta, corr[nb][hd]);
         }
     };
@@ -426,9 +429,17 @@ __device__ __forceinline__ void key_corrections(Smem<G>& S, float* sc, int cap, 
                 for (int i = 0; i < 4; ++i) {
                     const int o = 8 * i;
                     dw[nb][i] = lds_at<uint32_t>(S, drow[nb] | (shr(ent[nb], o + 1) & 0x1cu));
-                    const uint32_t qo = qc | (shr(ent[nb], o - 2) & 0xfcu);
+                    const uint32_t qo = qc | (shr(ent[nb], o - 2 - LG) & (0xfcu << LG));
+                    if constexpr (G == 4) {
+                        const float4 v4 = lds_at<float4>(S, qo);
+                        qv[nb][i][0] = v4.x;
+                        qv[nb][i][G > 1 ? 1 : 0] = v4.y;
+                        qv[nb][i][G > 2 ? 2 : 0] = v4.z;
+                        qv[nb][i][G > 3 ? 3 : 0] = v4.w;
+                    } else {
 #pragma unroll
-                    for (int hd = 0; hd < G; ++hd) qv[nb][i][hd] = lds_at<float>(S, qo + hd * D * 4);
+                        for (int hd = 0; hd < G; ++hd) qv[nb][i][hd] = lds_at<float>(S, qo + hd * 4);
+                    }
                 }
             __builtin_amdgcn_sched_barrier(0);
             float2 kv[NB][4];
@@ -631,8 +642,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
     for (int hd = 0; hd < G; ++hd) {
         const uint16_t* qp = a.q + ((int64_t)s * a.Hq + h * G + hd) * D;
         const float x0 = h2f(qp[lane]), x1 = h2f(qp[lane + 64]);
-        S.q()[hd][lane] = x0;
-        S.q()[hd][lane + 64] = x1;
+        S.q()[lane][hd] = x0;
+        S.q()[lane + 64][hd] = x1;
         const float mx = wave_max_nonneg(fmaxf(fabsf(x0), fabsf(x1)));
         const float sum = wave_sum(x0 + x1);
         const int sh = fix_shift(mx);
@@ -810,8 +821,6 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
             S.m[hd] = mx;
             S.l[hd] = sum;
         }
-        S.oc()[hd][lane] = 0.0f;
-        S.oc()[hd][lane + 64] = 0.0f;
         S.oci()[hd][lane] = 0;
         S.oci()[hd][lane + 64] = 0;
     }
@@ -824,8 +833,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
 #pragma unroll
     for (int nt = 0; nt < 8; ++nt) oacc[nt] = 0.0f;
     float pb[G];
+    float ocr[G][2];   // value corrections of channels lane and lane + 64
 #pragma unroll
-    for (int hd = 0; hd < G; ++hd) pb[hd] = 0.0f;
+    for (int hd = 0; hd < G; ++hd) pb[hd] = ocr[hd][0] = ocr[hd][1] = 0.0f;
     {
         const int used = group_layout(S, gc, lane, fits_c);
         wave_sync();
@@ -959,8 +969,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         // fold the group's integer sums into the fp32 outputs
 #pragma unroll
         for (int hd = 0; hd < G; ++hd) {
-            S.oc()[hd][lane] += ldexpf((float)S.oci()[hd][lane], -fsh);
-            S.oc()[hd][lane + 64] += ldexpf((float)S.oci()[hd][lane + 64], -fsh);
+            ocr[hd][0] += ldexpf((float)S.oci()[hd][lane], -fsh);
+            ocr[hd][1] += ldexpf((float)S.oci()[hd][lane + 64], -fsh);
             S.oci()[hd][lane] = 0;
             S.oci()[hd][lane + 64] = 0;
         }
@@ -973,6 +983,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
     for (int hd = 0; hd < G; ++hd) {
         const float v = wave_sum(pb[hd]);
         if (lane == 0) S.pbase[hd] = v;
+        S.oc()[hd][lane] = ocr[hd][0];
+        S.oc()[hd][lane + 64] = ocr[hd][1];
     }
     wave_sync();
     if (hq < G) {
