@@ -91,6 +91,22 @@ __global__ __launch_bounds__(1024) void quantize_kernel(QuantArgs a) {
     const bool active = wave < nslots;
     const int slot = slot0 + wave;
 
+    // Reads that do not depend on this call's values go out first, so that their latency
+    // overlaps the quantization: the COO counts of the record's earlier slots, and (values,
+    // when the call starts at an odd slot) the bytes the previous token shares with it.
+    int pre_cnt = 0;
+    if (lane < slot0) {
+#pragma unroll
+        for (int c = 0; c < NC; ++c) pre_cnt += rec[LY.counts + lane * NC + c];
+    }
+    uint8_t old_b[D / 64];
+#pragma unroll
+    for (int k = 0; k < D / 64; ++k) old_b[k] = 0;
+    if (which == 1 && (slot0 & 1) && wave == 0) {
+#pragma unroll
+        for (int k = 0; k < D / 64; ++k) old_b[k] = rec[LY.dense + (lane + 64 * k) * (kPage / 2) + (slot0 >> 1)];
+    }
+
     // ---- quantize this wave's vector (Eq. 1-4) -------------------------------------
     const float* th = a.thr + (h * 2 + which) * 4;
     const float lo_o = th[0], lo_i = th[1], hi_i = th[2], hi_o = th[3];
@@ -166,10 +182,12 @@ __global__ __launch_bounds__(1024) void quantize_kernel(QuantArgs a) {
     {
         int cnt = 0;
         if (lane < kPage) {
+            if (lane < slot0) {
+                cnt = pre_cnt;
+            } else if (lane < slot0 + nslots) {
 #pragma unroll
-            for (int c = 0; c < NC; ++c)
-                cnt += (lane < slot0) ? rec[LY.counts + lane * NC + c]
-                                      : (lane < slot0 + nslots ? s_counts[lane][c] : 0);
+                for (int c = 0; c < NC; ++c) cnt += s_counts[lane][c];
+            }
         }
         const int incl = wave_incl_scan(cnt, lane);
         base = __shfl(incl - cnt, slot < kPage ? slot : 0, 64);
@@ -213,23 +231,31 @@ __global__ __launch_bounds__(1024) void quantize_kernel(QuantArgs a) {
         uint32_t* dst = reinterpret_cast<uint32_t*>(rec + LY.dense + slot0 * (D / 2));
         for (int i = threadIdx.x; i < nslots * (D / 8); i += blockDim.x) dst[i] = src[i];
     } else {
-        // V: channel-major, element j of slot t at byte j*P/2 + t/2, low nibble = even t;
-        // consecutive threads write consecutive bytes of a channel row.
+        // V: channel-major, element j of slot t at byte j*P/2 + t/2, low nibble = even t.
+        // The first pair (which may keep an earlier token's even nibble) is written by wave
+        // 0, one channel per lane; the later pairs by all threads, consecutive threads on
+        // consecutive bytes of a channel row.
         const int p_lo = slot0 >> 1, p_hi = (slot0 + nslots - 1) >> 1;
-        const int npairs = p_hi - p_lo + 1;
+        if (wave == 0) {
+            const int te = 2 * p_lo, to = te + 1;
+            const bool has_e = te >= slot0;
+            const bool has_o = to < slot0 + nslots;
+#pragma unroll
+            for (int k = 0; k < D / 64; ++k) {
+                const int j = lane + 64 * k;
+                const uint8_t lo_n = has_e ? s_vnib[te][j] : (uint8_t)(old_b[k] & 0x0f);
+                const uint8_t hi_n = has_o ? (uint8_t)(s_vnib[to][j] << 4) : (uint8_t)0;
+                rec[LY.dense + j * (kPage / 2) + p_lo] = (uint8_t)(lo_n | hi_n);
+            }
+        }
+        const int npairs = p_hi - p_lo;   // pairs after the first
         for (int i = threadIdx.x; i < npairs * D; i += blockDim.x) {
             const int j = i / npairs;
-            const int p = p_lo + i % npairs;
+            const int p = p_lo + 1 + i % npairs;
             const int te = 2 * p, to = 2 * p + 1;
-            const bool has_e = te >= slot0 && te < slot0 + nslots;
-            const bool has_o = to >= slot0 && to < slot0 + nslots;
-            uint8_t* dst = rec + LY.dense + j * (kPage / 2) + p;
-            if (has_e && has_o)
-                *dst = (uint8_t)(s_vnib[te][j] | (s_vnib[to][j] << 4));
-            else if (has_e)
-                *dst = s_vnib[te][j];
-            else
-                *dst = (uint8_t)((*dst & 0x0f) | (s_vnib[to][j] << 4));
+            const bool has_o = to < slot0 + nslots;
+            rec[LY.dense + j * (kPage / 2) + p] = has_o ? (uint8_t)(s_vnib[te][j] | (s_vnib[to][j] << 4))
+                                                        : s_vnib[te][j];
         }
     }
 }
@@ -238,7 +264,8 @@ __global__ __launch_bounds__(1024) void quantize_kernel(QuantArgs a) {
 
 hipError_t launch_quantize(const QuantArgs& a, int d, int max_new_per_seq, hipStream_t st) {
     const int waves = max(1, min(kPage, max_new_per_seq));
-    const int segs = (max_new_per_seq + kPage - 1) / kPage + 1;   // pages one sequence can touch
+    // pages a run of n tokens can touch: (n + P - 2) / P + 1 (one for a single token)
+    const int segs = (max_new_per_seq + kPage - 2) / kPage + 1;
     dim3 grid(segs, a.n_seqs, a.H * 2);
     dim3 block(64 * waves);
     if (d == 64)
