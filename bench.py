@@ -37,6 +37,8 @@ def parse():
     ap.add_argument("--workload", type=int, default=3, help="1..5 (3 = batch-256 Llama-2-13B layer)")
     ap.add_argument("--window", type=int, default=0,
                     help="sliding window in tokens (0: attend over the whole sequence)")
+    ap.add_argument("--paged", action="store_true",
+                    help="on-demand sparse pages: COO bytes in a separate pool of 256-byte pages")
     ap.add_argument("--cpu-sample-seqs", type=int, default=128)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -97,7 +99,9 @@ def main():
     lens = synth.seq_lengths(w)
     bt_cpu, nblk = synth.block_table(w, lens)
     bt = bt_cpu.to(dev)
-    cache = B.Cache(nblk, H, d, thr)
+    # (on-demand sparse pages: room for two 256-byte pages per record; only what the COO
+    # streams need is taken)
+    cache = B.Cache(nblk, H, d, thr, sparse_pages=2 * nblk * H * 2 if args.paged else 0)
     log(f"pool {cache.pool.numel() / 2**30:.2f} GiB, {nblk} pages")
     chunk = 16
     t0 = time.time()
@@ -113,6 +117,17 @@ def main():
         del k, v
     torch.cuda.synchronize()
     log(f"prefill-quantized {int(lens.sum()) - n} tokens in {time.time() - t0:.1f}s")
+    capacity = None
+    if args.paged:
+        free, overflow = cache.sparse_status()
+        if overflow:
+            raise SystemExit("sparse page pool overflowed")
+        used_pages = cache.sparse_pages - free
+        capacity = {"dense_pool_bytes": cache.pool.numel(), "sparse_pages_used": used_pages,
+                    "pool_bytes": cache.pool.numel() + used_pages * B.SPARSE_PAGE_BYTES,
+                    "fixed_record_pool_bytes": nblk * H * 2 * B.record_bytes(d)}
+        log(f"sparse pages used: {used_pages}; pool {capacity['pool_bytes'] / 2**30:.2f} GiB "
+            f"vs {capacity['fixed_record_pool_bytes'] / 2**30:.2f} GiB with fixed records")
 
     k_new = synth.new_token_values(w, "k", 0, dev)
     v_new = synth.new_token_values(w, "v", 0, dev)
@@ -178,12 +193,14 @@ def main():
     n_out = int((counts * valid.to(dev)[:, None, None, :]).sum())
     n_vec = sum(seen) * H * 2
     kv_bytes = n_vec * (d // 2 + nc + 12) + n_out
+    if args.paged:
+        kv_bytes += n_pages_read * H * 2 * 8   # each record's first two sparse page ids
     aux_bytes = n * Hq * d * (2 + 4) + n_pages_read * 4 + n * 4
     aux_bytes += 2 * ws_bytes          # split partials: written once, read once by the combine
     alg_bytes = kv_bytes + aux_bytes
     achieved = alg_bytes / attn_avg_s / 1e9
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": stored_traffic(w.name) if not win else None,
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": stored_traffic(w.name) if not (win or args.paged) else None,
                 "bytes_per_launch": alg_bytes, "kernel_us": round(attn_avg_s * 1e6, 2),
                 "outlier_fraction": round(n_out / (n_vec * d), 4)}
 
@@ -248,10 +265,12 @@ def main():
                                f"context {w.ctx_min}..{w.ctx} incl. the new token, 16-token pages, "
                                f"shuffled block table"
                                + (f", sliding window {win}" if win else "")
+                               + (", on-demand 256-byte sparse pages" if args.paged else "")
                                + "; step = quantize 1 token/seq + attention",
                    "global_batch": n, "seq_len": max_len, "parallelism": "single GPU"},
         "roofline": roofline,
         "cpu_baseline": cpu,
+        **({"capacity": capacity} if capacity else {}),
         "parity_sample": parity,
         "attention_source": source_hash(),
     }

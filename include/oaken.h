@@ -57,6 +57,25 @@
  * pool + ((b * n_kv_heads + h) * 2 + w) * record_stride.
  * Tokens are appended in position order (Sec. 5.2, MMU); writing slot t of a page
  * invalidates any later slot of that page.
+ *
+ * On-demand sparse pages (the dense and sparse management tables of Sec. 5.2: the
+ * sparse matrices vary in size, so their pages are taken as needed).  A cache whose
+ * sparse_pool is not NULL keeps each record's COO bytes in a separate pool of
+ * OAKEN_SPARSE_PAGE_BYTES-byte sparse pages, taken from a free list as a record's COO
+ * stream grows:
+ *   counts, meta, dense   as above
+ *   table   offset dense + P*d/2         int32 [P*d / OAKEN_SPARSE_PAGE_BYTES]: sparse
+ *           page holding bytes [256 i, 256 i + 256) of the record's COO stream (the
+ *           stream is laid out as in the fixed record); entries i >= ceil(used / 256),
+ *           used = sum of the record's counts, are unused
+ *   stride  align128(table + 4 * P*d / OAKEN_SPARSE_PAGE_BYTES)
+ * oaken_record_bytes_paged gives that stride.  The free list (sparse_free, int32):
+ *   [0] number of free pages n, [1] overflow flag, [2 .. 2+n) the free page ids.
+ * oaken_quantize_kv pops pages from it (atomically) and writes their ids into the
+ * record's table.  When the list runs dry it sets the overflow flag, and that
+ * record's missing pages are left unwritten: the cache contents are then undefined
+ * until the pages are released or the pool is reset (attention still only reads
+ * inside the pools).  oaken_sparse_release returns retired blocks' pages.
  */
 #ifndef OAKEN_H
 #define OAKEN_H
@@ -76,19 +95,48 @@ typedef enum {
     OAKEN_ERR_HIP = 4            /* the HIP runtime rejected a launch */
 } oaken_status;
 
+#define OAKEN_SPARSE_PAGE_BYTES 256
+
 /* One layer's quantized KV cache: host struct describing device buffers. */
 typedef struct oaken_cache {
     int32_t num_blocks;          /* physical pages in the pool */
     int32_t block_size;          /* tokens per page P; must be 16 */
     int32_t n_kv_heads;          /* KV heads H */
     int32_t head_dim;            /* d: 64 or 128 */
-    int64_t record_stride;       /* must equal oaken_record_bytes(block_size, head_dim) */
+    int64_t record_stride;       /* oaken_record_bytes(block_size, head_dim), or
+                                    oaken_record_bytes_paged(...) with sparse pages */
     void* pool;                  /* device, num_blocks * n_kv_heads * 2 * record_stride bytes */
     const float* thresholds;     /* device fp32 [n_kv_heads][2 (K, V)][4] = lo_o, lo_i, hi_i, hi_o */
+    /* On-demand sparse pages; NULL sparse_pool selects the fixed records. */
+    void* sparse_pool;           /* device, sparse_pages * OAKEN_SPARSE_PAGE_BYTES bytes */
+    int32_t* sparse_free;        /* device, oaken_sparse_free_list_bytes(sparse_pages) bytes */
+    int32_t sparse_pages;        /* pages in sparse_pool (>= 1 when sparse_pool is set) */
 } oaken_cache;
 
 /* Bytes of one page record (see layout above); -1 if (block_size, head_dim) is unsupported. */
 int64_t oaken_record_bytes(int32_t block_size, int32_t head_dim);
+
+/* Bytes of one record with on-demand sparse pages; -1 if unsupported. */
+int64_t oaken_record_bytes_paged(int32_t block_size, int32_t head_dim);
+
+/* Bytes of the free list for a pool of sparse_pages pages. */
+size_t oaken_sparse_free_list_bytes(int32_t sparse_pages);
+
+/* Marks every sparse page free and clears the overflow flag (run before first use, and
+   to drop every sequence at once).  Records keep their bytes: reset them by writing
+   their pages again from slot 0.  Enqueued on stream. */
+int oaken_sparse_reset(const oaken_cache* cache, void* stream);
+
+/* Retires blocks: their records (every KV head, K and V) give their sparse pages back
+   to the free list and become empty (counts zeroed).  block_ids: device int32
+   [n_blocks], each < num_blocks, no repeats.  Must not run concurrently with a
+   quantize call on the same cache (order them on one stream).  Enqueued on stream. */
+int oaken_sparse_release(const oaken_cache* cache, const int32_t* block_ids, int32_t n_blocks,
+                         void* stream);
+
+/* Host copies of the free-page count and the overflow flag.  Synchronizes stream. */
+int oaken_sparse_status(const oaken_cache* cache, int32_t* free_pages, int32_t* overflowed,
+                        void* stream);
 
 /* Host array out[5] = byte offsets of counts, meta, dense, sparse, and the stride.
    Returns OAKEN_OK or OAKEN_ERR_UNSUPPORTED / OAKEN_ERR_INVALID_ARG. */

@@ -34,6 +34,9 @@ class _CacheStruct(ctypes.Structure):
         ("record_stride", ctypes.c_int64),
         ("pool", ctypes.c_void_p),
         ("thresholds", ctypes.c_void_p),
+        ("sparse_pool", ctypes.c_void_p),
+        ("sparse_free", ctypes.c_void_p),
+        ("sparse_pages", ctypes.c_int32),
     ]
 
 
@@ -49,6 +52,16 @@ def lib():
     P, i32, i64, f32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_size_t
     L.oaken_record_bytes.argtypes = [i32, i32]
     L.oaken_record_bytes.restype = i64
+    L.oaken_record_bytes_paged.argtypes = [i32, i32]
+    L.oaken_record_bytes_paged.restype = i64
+    L.oaken_sparse_free_list_bytes.argtypes = [i32]
+    L.oaken_sparse_free_list_bytes.restype = sz
+    L.oaken_sparse_reset.argtypes = [ctypes.POINTER(_CacheStruct), P]
+    L.oaken_sparse_reset.restype = ctypes.c_int
+    L.oaken_sparse_release.argtypes = [ctypes.POINTER(_CacheStruct), P, i32, P]
+    L.oaken_sparse_release.restype = ctypes.c_int
+    L.oaken_sparse_status.argtypes = [ctypes.POINTER(_CacheStruct), ctypes.POINTER(i32), ctypes.POINTER(i32), P]
+    L.oaken_sparse_status.restype = ctypes.c_int
     L.oaken_record_layout.argtypes = [i32, i32, P]
     L.oaken_record_layout.restype = ctypes.c_int
     L.oaken_calibrate_workspace_bytes.argtypes = [i32, i32]
@@ -100,6 +113,13 @@ def record_bytes(head_dim: int, block_size: int = PAGE) -> int:
     return int(lib().oaken_record_bytes(block_size, head_dim))
 
 
+def record_bytes_paged(head_dim: int, block_size: int = PAGE) -> int:
+    return int(lib().oaken_record_bytes_paged(block_size, head_dim))
+
+
+SPARSE_PAGE_BYTES = 256
+
+
 def record_layout(head_dim: int, block_size: int = PAGE) -> dict:
     out = (ctypes.c_int64 * 5)()
     _check(lib().oaken_record_layout(block_size, head_dim, out))
@@ -107,11 +127,16 @@ def record_layout(head_dim: int, block_size: int = PAGE) -> dict:
 
 
 class Cache:
-    """One layer's quantized KV cache: a uint8 page pool plus fp32 thresholds [H][2][4]."""
+    """One layer's quantized KV cache: a uint8 page pool plus fp32 thresholds [H][2][4].
+
+    sparse_pages > 0 keeps the COO bytes in a separate pool of that many 256-byte sparse
+    pages, taken on demand (the records then hold a sparse page table instead of their
+    worst-case COO capacity)."""
 
     def __init__(self, num_blocks: int, n_kv_heads: int, head_dim: int, thresholds: torch.Tensor,
-                 pool: torch.Tensor | None = None):
-        stride = record_bytes(head_dim)
+                 pool: torch.Tensor | None = None, sparse_pages: int = 0):
+        self.sparse_pages = int(sparse_pages)
+        stride = record_bytes_paged(head_dim) if self.sparse_pages > 0 else record_bytes(head_dim)
         if stride < 0:
             raise OakenError(2, f"head_dim {head_dim} unsupported")
         nbytes = num_blocks * n_kv_heads * 2 * stride
@@ -124,9 +149,35 @@ class Cache:
         self.pool = pool
         self.thresholds = thresholds.contiguous()
         self.num_blocks, self.n_kv_heads, self.head_dim, self.stride = num_blocks, n_kv_heads, head_dim, stride
+        self.sparse_pool = self.sparse_free = None
+        sp = sf = None
+        if self.sparse_pages > 0:
+            dev = thresholds.device
+            self.sparse_pool = torch.zeros(self.sparse_pages * SPARSE_PAGE_BYTES, dtype=torch.uint8, device=dev)
+            nfree = int(lib().oaken_sparse_free_list_bytes(self.sparse_pages)) // 4
+            self.sparse_free = torch.zeros(nfree, dtype=torch.int32, device=dev)
+            sp = _dev(self.sparse_pool, torch.uint8, "sparse_pool")
+            sf = _dev(self.sparse_free, torch.int32, "sparse_free")
         self._s = _CacheStruct(num_blocks, PAGE, n_kv_heads, head_dim, stride,
                                _dev(self.pool, torch.uint8, "pool"),
-                               _dev(self.thresholds, torch.float32, "thresholds"))
+                               _dev(self.thresholds, torch.float32, "thresholds"), sp, sf, self.sparse_pages)
+        if self.sparse_pages > 0:
+            self.sparse_reset()
+
+    def sparse_reset(self):
+        """Every sparse page free, every record empty."""
+        _check(lib().oaken_sparse_reset(self.struct, _stream()))
+
+    def release(self, block_ids: torch.Tensor):
+        """Retire blocks: their records give their sparse pages back and become empty."""
+        _check(lib().oaken_sparse_release(self.struct, _dev(block_ids, torch.int32, "block_ids"),
+                                          block_ids.numel(), _stream()))
+
+    def sparse_status(self) -> tuple[int, bool]:
+        """(free sparse pages, overflow flag); synchronizes the current stream."""
+        fp, ov = ctypes.c_int32(0), ctypes.c_int32(0)
+        _check(lib().oaken_sparse_status(self.struct, ctypes.byref(fp), ctypes.byref(ov), _stream()))
+        return int(fp.value), bool(ov.value)
 
     @property
     def struct(self):

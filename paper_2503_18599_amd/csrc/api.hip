@@ -45,12 +45,31 @@ int check_cache(const oaken_cache* c) {
         return fail(OAKEN_ERR_UNSUPPORTED, "head_dim %d unsupported (64 or 128)", c->head_dim);
     if (c->num_blocks <= 0 || c->n_kv_heads <= 0)
         return fail(OAKEN_ERR_INVALID_ARG, "num_blocks and n_kv_heads must be positive");
-    const int64_t want = oaken::make_layout(c->block_size, c->head_dim).stride;
+    const bool paged = c->sparse_pool != nullptr;
+    const int64_t want = paged ? oaken::make_layout_paged(c->block_size, c->head_dim).stride
+                               : oaken::make_layout(c->block_size, c->head_dim).stride;
     if (c->record_stride != want)
         return fail(OAKEN_ERR_INVALID_ARG, "record_stride %lld != %lld", (long long)c->record_stride,
                     (long long)want);
     if (!c->pool || !c->thresholds) return fail(OAKEN_ERR_INVALID_ARG, "pool or thresholds is NULL");
+    if (paged && (!c->sparse_free || c->sparse_pages <= 0))
+        return fail(OAKEN_ERR_INVALID_ARG, "sparse pages need a free list and sparse_pages > 0");
     return OAKEN_OK;
+}
+
+oaken::SparseArgs sparse_args(const oaken_cache* c) {
+    const oaken::Layout L = oaken::make_layout_paged(c->block_size, c->head_dim);
+    oaken::SparseArgs a{};
+    a.pool = static_cast<uint8_t*>(c->pool);
+    a.stride = L.stride;
+    a.table = L.sparse;
+    a.num_blocks = c->num_blocks;
+    a.H = c->n_kv_heads;
+    a.cbytes = (int32_t)L.meta;   // counts occupy [0, meta) (padding included)
+    a.tbytes = (int32_t)(4 * ((int64_t)c->block_size * c->head_dim / oaken::kSparsePage));
+    a.sfree = c->sparse_free;
+    a.spages = c->sparse_pages;
+    return a;
 }
 
 int hip_status(hipError_t e, const char* what) {
@@ -65,6 +84,51 @@ extern "C" {
 int64_t oaken_record_bytes(int32_t block_size, int32_t head_dim) {
     if (block_size != oaken::kPage || !supported_dim(head_dim)) return -1;
     return oaken::make_layout(block_size, head_dim).stride;
+}
+
+int64_t oaken_record_bytes_paged(int32_t block_size, int32_t head_dim) {
+    if (block_size != oaken::kPage || !supported_dim(head_dim)) return -1;
+    return oaken::make_layout_paged(block_size, head_dim).stride;
+}
+
+size_t oaken_sparse_free_list_bytes(int32_t sparse_pages) {
+    if (sparse_pages <= 0) return 0;
+    return (size_t)(sparse_pages + 2) * sizeof(int32_t);
+}
+
+int oaken_sparse_reset(const oaken_cache* cache, void* stream) {
+    int st = check_cache(cache);
+    if (st != OAKEN_OK) return st;
+    if (!cache->sparse_pool) return fail(OAKEN_ERR_INVALID_ARG, "cache has no sparse pages");
+    return hip_status(oaken::launch_sparse_reset(sparse_args(cache), static_cast<hipStream_t>(stream)),
+                      "sparse reset launch");
+}
+
+int oaken_sparse_release(const oaken_cache* cache, const int32_t* block_ids, int32_t n_blocks, void* stream) {
+    int st = check_cache(cache);
+    if (st != OAKEN_OK) return st;
+    if (!cache->sparse_pool) return fail(OAKEN_ERR_INVALID_ARG, "cache has no sparse pages");
+    if (n_blocks < 0 || (n_blocks > 0 && !block_ids))
+        return fail(OAKEN_ERR_INVALID_ARG, "block_ids NULL or n_blocks negative");
+    if (n_blocks == 0) return ok();
+    return hip_status(oaken::launch_sparse_release(sparse_args(cache), block_ids, n_blocks,
+                                                   static_cast<hipStream_t>(stream)),
+                      "sparse release launch");
+}
+
+int oaken_sparse_status(const oaken_cache* cache, int32_t* free_pages, int32_t* overflowed, void* stream) {
+    int st = check_cache(cache);
+    if (st != OAKEN_OK) return st;
+    if (!cache->sparse_pool) return fail(OAKEN_ERR_INVALID_ARG, "cache has no sparse pages");
+    if (!free_pages || !overflowed) return fail(OAKEN_ERR_INVALID_ARG, "output pointers are NULL");
+    int32_t h[2] = {0, 0};
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = hipMemcpyAsync(h, cache->sparse_free, sizeof(h), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_status(e, "sparse status copy");
+    *free_pages = h[0];
+    *overflowed = h[1];
+    return ok();
 }
 
 int oaken_record_layout(int32_t block_size, int32_t head_dim, int64_t* out) {
@@ -152,6 +216,9 @@ int oaken_quantize_kv(const oaken_cache* cache, const void* k_new, const void* v
     if (n_tokens == 0 || max_new_per_seq == 0) return ok();
     oaken::QuantArgs a{};
     a.pool = static_cast<uint8_t*>(cache->pool);
+    a.spool = static_cast<uint8_t*>(cache->sparse_pool);
+    a.sfree = cache->sparse_free;
+    a.spages = cache->sparse_pages;
     a.thr = cache->thresholds;
     a.k_new = static_cast<const uint16_t*>(k_new);
     a.v_new = static_cast<const uint16_t*>(v_new);
@@ -198,6 +265,9 @@ int oaken_decode_attention_window(const oaken_cache* cache, const void* q, int32
         return fail(OAKEN_ERR_INVALID_ARG, "block table too narrow for max_seq_len");
     if (!std::isfinite(softmax_scale)) return fail(OAKEN_ERR_INVALID_ARG, "softmax_scale not finite");
     if (sliding_window < 0) return fail(OAKEN_ERR_INVALID_ARG, "sliding_window must be >= 0");
+    if (cache->sparse_pool && !oaken::mfma_attention_supported(cache->head_dim, n_q_heads / cache->n_kv_heads))
+        return fail(OAKEN_ERR_UNSUPPORTED,
+                    "on-demand sparse pages need head_dim 128 and 1, 2 or 4 query heads per KV head");
     const size_t need = oaken_attention_workspace_bytes_window(n_seqs, n_q_heads, cache->n_kv_heads,
                                                                cache->head_dim, max_seq_len, sliding_window);
     if (need > 0 && (!workspace || workspace_bytes < need))
@@ -223,6 +293,8 @@ int oaken_decode_attention_window(const oaken_cache* cache, const void* q, int32
     a.n_splits = sp.n_splits;
     a.window = sliding_window;
     a.scale = softmax_scale;
+    a.spool = static_cast<const uint8_t*>(cache->sparse_pool);
+    a.spages = cache->sparse_pages;
     return hip_status(oaken::launch_attention(a, cache->head_dim, static_cast<hipStream_t>(stream)),
                       "attention launch");
 }

@@ -266,6 +266,12 @@ __device__ __forceinline__ uint4 count_chunk(const Grp& gr, int lane) {
     return ld16(pick4(l >> 1, gr.base[0], gr.base[1], gr.base[2], gr.base[3]) + (uint32_t)(l & 1) * 16u);
 }
 
+// With on-demand sparse pages: the first two entries of the sparse page table of the
+// lane's page (lane >> 4), which hold the bytes a staged page can use.
+__device__ __forceinline__ int2 page_tab(const Grp& gr, int lane) {
+    return *reinterpret_cast<const int2*>(pick4(lane >> 4, gr.base[0], gr.base[1], gr.base[2], gr.base[3]) + LY.sparse);
+}
+
 // The metadata of the lane's token (lane = 16 * page + slot).  Stays in registers until
 // the group's token constants are formed.
 __device__ __forceinline__ Meta meta_words(const Grp& gr, int lane) {
@@ -290,13 +296,42 @@ __device__ __forceinline__ int group_layout(Smem<G>& S, const Grp& gr, int lane,
     return lane < 16 ? u0 : lane < 32 ? u1 : lane < 48 ? u2 : u3;
 }
 
+// Sparse page id from a record table entry (1 + id; 0 = none held), clamped into the
+// pool so that a stale or missing entry can only misread, never fault.
+__device__ __forceinline__ const uint8_t* sparse_page(const AttnArgs& a, int32_t entry) {
+    const int id = entry - 1;
+    return a.spool + (int64_t)((id >= 0 && id < a.spages) ? id : 0) * kSparsePage;
+}
+
 // The lane's two 16-byte chunks of its page's COO bytes: chunks (lane & 15) and
 // (lane & 15) + 16 of page lane >> 4.  Chunks past the page's used bytes re-read chunk 0.
-__device__ __forceinline__ void sparse_chunks(const Grp& gr, int used, int lane, uint4& r0, uint4& r1) {
-    const uint8_t* r = pick4(lane >> 4, gr.base[0], gr.base[1], gr.base[2], gr.base[3]);
+// With on-demand pages the two chunk rows are the record's first two sparse pages.
+template <bool PG>
+__device__ __forceinline__ void sparse_chunks(const AttnArgs& a, const Grp& gr, int2 tab, int used, int lane,
+                                              uint4& r0, uint4& r1) {
     const uint32_t o0 = (uint32_t)(lane & 15) * 16u, o1 = o0 + 256u;
-    r0 = ld16(r + LY.sparse + ((int)o0 < used ? o0 : 0u));
-    r1 = ld16(r + LY.sparse + ((int)o1 < used ? o1 : 0u));
+    if constexpr (PG) {
+        const uint8_t* p0 = sparse_page(a, tab.x);
+        const uint8_t* p1 = sparse_page(a, tab.y);
+        r0 = ld16(p0 + ((int)o0 < used ? o0 : 0u));
+        r1 = ld16((int)o1 < used ? p1 + o0 : p0);
+    } else {
+        const uint8_t* r = pick4(lane >> 4, gr.base[0], gr.base[1], gr.base[2], gr.base[3]);
+        r0 = ld16(r + LY.sparse + ((int)o0 < used ? o0 : 0u));
+        r1 = ld16(r + LY.sparse + ((int)o1 < used ? o1 : 0u));
+    }
+}
+
+// COO byte `off` of page pg's stream, read from HBM (groups whose pages exceed their
+// staging slot).
+template <bool PG>
+__device__ __forceinline__ uint32_t coo_byte(const AttnArgs& a, const Grp& gr, int pg, int off) {
+    const uint8_t* r = pick4(pg, gr.base[0], gr.base[1], gr.base[2], gr.base[3]);
+    if constexpr (PG) {
+        const int32_t entry = reinterpret_cast<const int32_t*>(r + LY.sparse)[off / kSparsePage];
+        return sparse_page(a, entry)[off % kSparsePage];
+    }
+    return r[LY.sparse + off];
 }
 
 // Writes the token's correction table: for COO class cls = COO >> 6 (bit 0 outer,
@@ -368,8 +403,8 @@ __device__ __forceinline__ uint32_t off_of(const Smem<G>& S, const void* p) {
 // Staged entries are read four at a time from one aligned dword pair, one block ahead of
 // their use; the corrections of a block are independent, and entries past a bucket
 // contribute zero.
-template <int G, bool STAGED, int NB>
-__device__ __forceinline__ void key_corrections(Smem<G>& S, float* sc, int cap, float scale,
+template <int G, bool STAGED, int NB, bool PG>
+__device__ __forceinline__ void key_corrections(Smem<G>& S, const AttnArgs& a, float* sc, int cap, float scale,
                                                 const Bucket (&kb)[NB], const Grp& gr, int tok0, int lane) {
     Bucket k[NB];
     uint32_t tbo[NB], drow[NB];
@@ -484,9 +519,14 @@ __device__ __forceinline__ void key_corrections(Smem<G>& S, float* sc, int cap, 
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
             // (a bucket of an absent page is empty)
-            const uint8_t* spp = pick4(k[nb].pg, gr.base[0], gr.base[1], gr.base[2], gr.base[3]) + LY.sparse + k[nb].st;
-            for (int kk = 0; kk < maxc; ++kk)
-                if (kk < k[nb].cnt) slot(nb, spp[kk], 0, true);
+            if constexpr (PG) {
+                for (int kk = 0; kk < maxc; ++kk)
+                    if (kk < k[nb].cnt) slot(nb, coo_byte<PG>(a, gr, k[nb].pg, k[nb].st + kk), 0, true);
+            } else {
+                const uint8_t* spp = pick4(k[nb].pg, gr.base[0], gr.base[1], gr.base[2], gr.base[3]) + LY.sparse + k[nb].st;
+                for (int kk = 0; kk < maxc; ++kk)
+                    if (kk < k[nb].cnt) slot(nb, spp[kk], 0, true);
+            }
         }
     }
 #pragma unroll
@@ -500,8 +540,8 @@ __device__ __forceinline__ void key_corrections(Smem<G>& S, float* sc, int cap, 
 
 // Same walk for values: each entry adds p_t * (true value - middle reading) to its
 // channel.  With one head the probability is already folded into the table and Gp.
-template <int G, bool STAGED, int NB>
-__device__ __forceinline__ void value_corrections(Smem<G>& S, const float* sc, int cap,
+template <int G, bool STAGED, int NB, bool PG>
+__device__ __forceinline__ void value_corrections(Smem<G>& S, const AttnArgs& a, const float* sc, int cap,
                                                   const Bucket (&kb)[NB], const Grp& gr, int tok0, int lane) {
     Bucket k[NB];
     uint32_t tbo[NB], dcol[NB];
@@ -597,14 +637,19 @@ __device__ __forceinline__ void value_corrections(Smem<G>& S, const float* sc, i
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
             // (a bucket of an absent page is empty)
-            const uint8_t* spp = pick4(k[nb].pg, gr.base[0], gr.base[1], gr.base[2], gr.base[3]) + LY.sparse + k[nb].st;
-            for (int kk = 0; kk < maxc; ++kk)
-                if (kk < k[nb].cnt) apply(slot(nb, spp[kk], 0, true));
+            if constexpr (PG) {
+                for (int kk = 0; kk < maxc; ++kk)
+                    if (kk < k[nb].cnt) apply(slot(nb, coo_byte<PG>(a, gr, k[nb].pg, k[nb].st + kk), 0, true));
+            } else {
+                const uint8_t* spp = pick4(k[nb].pg, gr.base[0], gr.base[1], gr.base[2], gr.base[3]) + LY.sparse + k[nb].st;
+                for (int kk = 0; kk < maxc; ++kk)
+                    if (kk < k[nb].cnt) apply(slot(nb, spp[kk], 0, true));
+            }
         }
     }
 }
 
-template <int G>
+template <int G, bool PG>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 : 1))) void attn_mfma_kernel(AttnArgs a) {
     constexpr int NRS = (G + 1) / 2;        // key-pass MFMA row sets (8 rows per head)
     __shared__ Smem<G> S;
@@ -621,6 +666,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
     const int cap = a.pages_per_split * P;
     const int n_tok = max(0, min(L, p_end * P) - p_begin * P);
     const int32_t* btab = a.block_table + (int64_t)s * a.max_blocks;
+    constexpr bool paged = PG;   // on-demand sparse pages
     // block ids of the range, one page per lane (a range spans at most 64 pages)
     const int blk_lane = (p_begin + lane < p_end) ? btab[p_begin + lane] : -1;
 
@@ -634,6 +680,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
     // the first key group's counts and metadata are needed before anything else
     Grp gc = make_group(a, blk_lane, p_begin, p_begin, p_end, L, h, 0);
     uint4 hreg = count_chunk(gc, lane);
+    int2 tab_c = paged ? page_tab(gc, lane) : int2{0, 0};   // (on-demand sparse pages)
     Meta mreg = meta_words(gc, lane);
 
     // ---- query in fp32 and in fixed point -----------------------------------------
@@ -703,10 +750,11 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         wave_sync();
 #pragma unroll
         for (int pg = 0; pg < GRP; ++pg) dreg[pg] = ld16(gc.base[pg] + koff);
-        sparse_chunks(gc, used, lane, sreg0, sreg1);
+        sparse_chunks<PG>(a, gc, tab_c, used, lane, sreg0, sreg1);
     }
     Grp gn = make_group(a, blk_lane, p_begin, p_begin + GRP, p_end, L, h, 0);
     hreg = count_chunk(gn, lane);
+    int2 tab_n = paged ? page_tab(gn, lane) : int2{0, 0};
     for (int g0 = p_begin; g0 < p_end; g0 += GRP) {
         const int tok0 = (g0 - p_begin) * P;
         const bool staged = fits_c;
@@ -776,32 +824,36 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         wave_sync();
         // next group: heads -> layout -> issue its sparse bytes and the heads after it
         Grp gnn = gn;
+        int2 tab_nn = tab_n;
         fits_n = true;
         if (gn.npg > 0) {
             if (lane < 2 * GRP) *reinterpret_cast<uint4*>(&S.head[0][16 * lane]) = hreg;
             wave_sync();
             const int used = group_layout(S, gn, lane, fits_n);
             wave_sync();
-            sparse_chunks(gn, used, lane, sreg0, sreg1);
+            sparse_chunks<PG>(a, gn, tab_n, used, lane, sreg0, sreg1);
             mreg = meta_words(gn, lane);
             gnn = make_group(a, blk_lane, p_begin, g0 + 2 * GRP, p_end, L, h, 0);
             hreg = count_chunk(gnn, lane);
+            if constexpr (PG) tab_nn = page_tab(gnn, lane);
         }
         wave_sync();
         // sparse part
         if (staged)
-            key_corrections<G, true, GRP / 2>(S, sc, cap, a.scale, kb, gc, tok0, lane);
+            key_corrections<G, true, GRP / 2, PG>(S, a, sc, cap, a.scale, kb, gc, tok0, lane);
         else
-            key_corrections<G, false, GRP / 2>(S, sc, cap, a.scale, kb, gc, tok0, lane);
+            key_corrections<G, false, GRP / 2, PG>(S, a, sc, cap, a.scale, kb, gc, tok0, lane);
         wave_sync();
         gc = gn;
         gn = gnn;
+        tab_n = tab_nn;
         fits_c = fits_n;
     }
 
     // the first value group's heads go out before the softmax
     gc = make_group(a, blk_lane, p_begin, p_begin, p_end, L, h, 1);
     hreg = count_chunk(gc, lane);
+    if constexpr (PG) tab_c = page_tab(gc, lane);
     mreg = meta_words(gc, lane);
 
     // ---- softmax over the range ----------------------------------------------------
@@ -841,10 +893,11 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         wave_sync();
 #pragma unroll
         for (int pg = 0; pg < GRP; ++pg) dreg[pg] = ld16(gc.base[pg] + voff);
-        sparse_chunks(gc, used, lane, sreg0, sreg1);
+        sparse_chunks<PG>(a, gc, tab_c, used, lane, sreg0, sreg1);
     }
     gn = make_group(a, blk_lane, p_begin, p_begin + GRP, p_end, L, h, 1);
     hreg = count_chunk(gn, lane);
+    if constexpr (PG) tab_n = page_tab(gn, lane);
     for (int g0 = p_begin; g0 < p_end; g0 += GRP) {
         const int tok0 = (g0 - p_begin) * P;
         const bool staged = fits_c;
@@ -909,16 +962,18 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         wave_sync();
         // next group: heads -> layout -> issue its sparse bytes and the heads after it
         Grp gnn = gn;
+        int2 tab_nn = tab_n;
         fits_n = true;
         if (gn.npg > 0) {
             if (lane < 2 * GRP) *reinterpret_cast<uint4*>(&S.head[0][16 * lane]) = hreg;
             wave_sync();
             const int used = group_layout(S, gn, lane, fits_n);
             wave_sync();
-            sparse_chunks(gn, used, lane, sreg0, sreg1);
+            sparse_chunks<PG>(a, gn, tab_n, used, lane, sreg0, sreg1);
             mreg = meta_words(gn, lane);
             gnn = make_group(a, blk_lane, p_begin, g0 + 2 * GRP, p_end, L, h, 1);
             hreg = count_chunk(gnn, lane);
+            if constexpr (PG) tab_nn = page_tab(gnn, lane);
         }
         wave_sync();
         v4i gacc[8];
@@ -962,9 +1017,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
             for (int nt = 0; nt < 8; ++nt) oacc[nt] += ldexpf(limbs(gacc[nt]), -e);
         }
         if (staged)
-            value_corrections<G, true, GRP / 2>(S, sc, cap, kb, gc, tok0, lane);
+            value_corrections<G, true, GRP / 2, PG>(S, a, sc, cap, kb, gc, tok0, lane);
         else
-            value_corrections<G, false, GRP / 2>(S, sc, cap, kb, gc, tok0, lane);
+            value_corrections<G, false, GRP / 2, PG>(S, a, sc, cap, kb, gc, tok0, lane);
         wave_sync();
         // fold the group's integer sums into the fp32 outputs
 #pragma unroll
@@ -976,6 +1031,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         }
         gc = gn;
         gn = gnn;
+        tab_n = tab_nn;
         fits_c = fits_n;
     }
 
@@ -1010,24 +1066,36 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
 
 }  // namespace
 
-bool mfma_attention_supported(int d, int G) { return d == D && (G == 1 || G == 2 || G == 4); }
-
-int mfma_score_cap() { return 512; }
-
-hipError_t launch_attention_mfma(const AttnArgs& a, hipStream_t st) {
+// The kernel with on-demand sparse pages is compiled in a translation unit of its own
+// (attention_mfma_paged.hip includes this file with OAKEN_ATTN_PAGED_TU defined): in one
+// module with the fixed-record kernel it changes the fixed kernel's register allocation.
+template <bool PG>
+static hipError_t launch_mfma(const AttnArgs& a, hipStream_t st) {
     const int G = a.Hq / a.H;
     if (a.pages_per_split > 64) return hipErrorInvalidValue;
     const size_t shm = (size_t)G * a.pages_per_split * P * sizeof(float);
     dim3 grid(a.n_splits, a.H, a.n_seqs);
     if (G == 1)
-        hipLaunchKernelGGL(attn_mfma_kernel<1>, grid, dim3(64), shm, st, a);
+        hipLaunchKernelGGL((attn_mfma_kernel<1, PG>), grid, dim3(64), shm, st, a);
     else if (G == 2)
-        hipLaunchKernelGGL(attn_mfma_kernel<2>, grid, dim3(64), shm, st, a);
+        hipLaunchKernelGGL((attn_mfma_kernel<2, PG>), grid, dim3(64), shm, st, a);
     else if (G == 4)
-        hipLaunchKernelGGL(attn_mfma_kernel<4>, grid, dim3(64), shm, st, a);
+        hipLaunchKernelGGL((attn_mfma_kernel<4, PG>), grid, dim3(64), shm, st, a);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();
 }
+
+#ifdef OAKEN_ATTN_PAGED_TU
+hipError_t launch_attention_mfma_paged(const AttnArgs& a, hipStream_t st) { return launch_mfma<true>(a, st); }
+#else
+bool mfma_attention_supported(int d, int G) { return d == D && (G == 1 || G == 2 || G == 4); }
+
+int mfma_score_cap() { return 512; }
+
+hipError_t launch_attention_mfma(const AttnArgs& a, hipStream_t st) {
+    return a.spool ? launch_attention_mfma_paged(a, st) : launch_mfma<false>(a, st);
+}
+#endif
 
 }  // namespace oaken

@@ -6,7 +6,8 @@
 
 namespace oaken {
 
-constexpr int kPage = 16;  // tokens per page (block_size)
+constexpr int kPage = 16;         // tokens per page (block_size)
+constexpr int kSparsePage = 256;  // bytes of one on-demand sparse page
 
 // Byte offsets of the fields of one page record (layout in include/oaken.h).
 struct Layout {
@@ -25,6 +26,14 @@ __host__ __device__ constexpr Layout make_layout(int P, int d) {
     return L;
 }
 
+// With on-demand sparse pages the record ends in its sparse page table (int32 ids of
+// the pages holding its COO stream); `sparse` is then the table's offset.
+__host__ __device__ constexpr Layout make_layout_paged(int P, int d) {
+    Layout L = make_layout(P, d);
+    L.stride = round_up(L.sparse + 4 * ((int64_t)P * d / kSparsePage), 128);
+    return L;
+}
+
 struct QuantArgs {
     uint8_t* pool;
     const float* thr;             // [H][2][4]
@@ -35,6 +44,9 @@ struct QuantArgs {
     const int32_t* cu_tokens;     // [n_seqs + 1]
     int64_t stride;
     int32_t num_blocks, H, max_blocks, n_seqs;
+    uint8_t* spool;               // on-demand sparse pages (nullptr: fixed records)
+    int32_t* sfree;               // free list: [0] count, [1] overflow flag, [2..] page ids
+    int32_t spages;
 };
 
 struct CalibArgs {
@@ -59,6 +71,8 @@ struct AttnArgs {
     int32_t pages_per_split, n_splits;
     int32_t window;               // sliding window in tokens (<= 0: the whole sequence)
     float scale;
+    const uint8_t* spool;         // on-demand sparse pages (nullptr: fixed records)
+    int32_t spages;
 };
 
 // Split-K plan used by both the workspace query and the launch.
@@ -68,6 +82,17 @@ struct SplitPlan {
 SplitPlan plan_splits(int32_t n_seqs, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
                       int32_t max_seq_len);
 
+// Sparse page pool maintenance (sparse_pages.hip).
+struct SparseArgs {
+    uint8_t* pool;                // dense records
+    int64_t stride, table;        // record stride; offset of the record's page table
+    int32_t num_blocks, H, cbytes, tbytes;   // counts bytes and table bytes per record
+    int32_t* sfree;
+    int32_t spages;
+};
+hipError_t launch_sparse_reset(const SparseArgs& a, hipStream_t st);
+hipError_t launch_sparse_release(const SparseArgs& a, const int32_t* block_ids, int n_blocks, hipStream_t st);
+
 hipError_t launch_quantize(const QuantArgs& a, int d, int max_new_per_seq, hipStream_t st);
 hipError_t launch_calibrate(const CalibArgs& a, hipStream_t st);
 hipError_t launch_attention(const AttnArgs& a, int d, hipStream_t st);
@@ -76,5 +101,6 @@ hipError_t launch_attention(const AttnArgs& a, int d, hipStream_t st);
 bool mfma_attention_supported(int d, int G);
 int mfma_score_cap();   // tokens per query head in one workgroup's page range
 hipError_t launch_attention_mfma(const AttnArgs& a, hipStream_t st);
+hipError_t launch_attention_mfma_paged(const AttnArgs& a, hipStream_t st);   // on-demand sparse pages
 
 }  // namespace oaken

@@ -60,14 +60,16 @@ __device__ inline int wave_incl_scan(int x, int lane) {
     return x + (row == 0 ? 0 : row == 1 ? r0 : row == 2 ? r0 + r1 : r0 + r1 + r2);
 }
 
-template <int D>
+template <int D, bool PG>
 __global__ __launch_bounds__(1024) void quantize_kernel(QuantArgs a) {
     constexpr int NC = D / 64;           // 64-value chunks per vector
-    constexpr Layout LY = make_layout(kPage, D);
+    constexpr Layout LY = PG ? make_layout_paged(kPage, D) : make_layout(kPage, D);
+    constexpr int NT = kPage * D / kSparsePage;   // sparse pages a record can need
 
     __shared__ uint8_t s_counts[kPage][NC];
     __shared__ uint8_t s_vnib[kPage][D];
     __shared__ __align__(16) uint8_t s_krow[kPage][D / 2];
+    __shared__ int s_tab[NT];            // the record's sparse page ids (on-demand pages)
 
     const int s = blockIdx.y;
     const int h = blockIdx.z >> 1;
@@ -99,6 +101,8 @@ __global__ __launch_bounds__(1024) void quantize_kernel(QuantArgs a) {
 #pragma unroll
         for (int c = 0; c < NC; ++c) pre_cnt += rec[LY.counts + lane * NC + c];
     }
+    // (on-demand pages: the record's page table, for the pages it already holds)
+    const int tab_pre = (PG && lane < NT) ? reinterpret_cast<const int32_t*>(rec + LY.sparse)[lane] : 0;
     uint8_t old_b[D / 64];
 #pragma unroll
     for (int k = 0; k < D / 64; ++k) old_b[k] = 0;
@@ -191,14 +195,53 @@ __global__ __launch_bounds__(1024) void quantize_kernel(QuantArgs a) {
         }
         const int incl = wave_incl_scan(cnt, lane);
         base = __shfl(incl - cnt, slot < kPage ? slot : 0, 64);
+        if constexpr (PG) {
+            // Sparse pages on demand (Sec. 5.2 MMU): the record's COO stream now needs
+            // ceil(new_used / 256) pages; wave 0 pops the ones the record does not hold
+            // yet from the free list and enters them in its table (entry = 1 + page id,
+            // 0 = none held).  An empty list sets the overflow flag and leaves those pages
+            // out (their bytes are not written).
+            const int new_used = __shfl(incl, slot0 + nslots - 1, 64);
+            const int p_new = (new_used + kSparsePage - 1) / kSparsePage;
+            if (wave == 0) {
+                const bool need = lane < p_new && tab_pre == 0;
+                const uint64_t nm = __ballot(need);
+                const int k = __popcll(nm);
+                int t = 0;
+                if (k > 0 && lane == 0) {
+                    t = atomicSub(&a.sfree[0], k);
+                    if (t < k) {              // not enough pages: give the count back
+                        atomicAdd(&a.sfree[0], k);
+                        atomicOr(&a.sfree[1], 1);
+                    }
+                }
+                t = __shfl(t, 0, 64);
+                int entry = tab_pre;
+                if (need && t >= k && t <= a.spages) {   // (a consistent list never exceeds the pool)
+                    const int r = __popcll(nm & ((1ull << lane) - 1ull));
+                    entry = 1 + a.sfree[2 + t - k + r];
+                    reinterpret_cast<int32_t*>(rec + LY.sparse)[lane] = entry;
+                }
+                if (lane < NT) s_tab[lane] = entry - 1;
+            }
+            __syncthreads();
+        }
     }
     if (active) {
         const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
         int off = base;
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
-            if ((omask[c] >> lane) & 1ull)
-                rec[LY.sparse + off + __popcll(omask[c] & below)] = coo[c];
+            if ((omask[c] >> lane) & 1ull) {
+                const int o = off + __popcll(omask[c] & below);
+                if constexpr (PG) {
+                    const int id = s_tab[o / kSparsePage];
+                    if (id >= 0 && id < a.spages)
+                        a.spool[(int64_t)id * kSparsePage + (o % kSparsePage)] = coo[c];
+                } else {
+                    rec[LY.sparse + o] = coo[c];
+                }
+            }
             off += __popcll(omask[c]);
         }
         if (lane < NC) rec[LY.counts + slot * NC + lane] = s_counts[slot][lane];
@@ -268,10 +311,15 @@ hipError_t launch_quantize(const QuantArgs& a, int d, int max_new_per_seq, hipSt
     const int segs = (max_new_per_seq + kPage - 2) / kPage + 1;
     dim3 grid(segs, a.n_seqs, a.H * 2);
     dim3 block(64 * waves);
-    if (d == 64)
-        hipLaunchKernelGGL(quantize_kernel<64>, grid, block, 0, st, a);
+    const bool pg = a.spool != nullptr;
+    if (d == 64 && !pg)
+        hipLaunchKernelGGL((quantize_kernel<64, false>), grid, block, 0, st, a);
+    else if (d == 128 && !pg)
+        hipLaunchKernelGGL((quantize_kernel<128, false>), grid, block, 0, st, a);
+    else if (d == 64)
+        hipLaunchKernelGGL((quantize_kernel<64, true>), grid, block, 0, st, a);
     else if (d == 128)
-        hipLaunchKernelGGL(quantize_kernel<128>, grid, block, 0, st, a);
+        hipLaunchKernelGGL((quantize_kernel<128, true>), grid, block, 0, st, a);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();
