@@ -39,6 +39,10 @@ def parse():
                     help="sliding window in tokens (0: attend over the whole sequence)")
     ap.add_argument("--paged", action="store_true",
                     help="on-demand sparse pages: COO bytes in a separate pool of 256-byte pages")
+    ap.add_argument("--layer", action="store_true",
+                    help="time a full decoder layer's decode step (random bf16 weights) around the cache")
+    ap.add_argument("--layer-batch", type=int, default=0,
+                    help="sequences in the layer step (0: the whole workload batch)")
     ap.add_argument("--cpu-sample-seqs", type=int, default=128)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -67,6 +71,65 @@ def stored_traffic(workload_name: str):
     if d.get("source_hash") != source_hash() or d.get("workload") != workload_name:
         return None
     return d.get("bytes_per_launch")
+
+
+def layer_bench(args, w, cache, bt, lens, dev):
+    """Decode step of a full decoder layer of the workload's shape: per-phase times of the
+    sequential step (HIP events), and the step with the batch in two micro-batches on two
+    streams."""
+    import torch
+
+    from paper_2503_18599_amd import binding as B
+    from paper_2503_18599_amd.layer import PHASES, DecoderLayer
+
+    n = args.layer_batch or w.n_seqs
+    H, Hq, d = w.n_kv_heads, w.n_q_heads, w.head_dim
+    d_model = Hq * d
+    d_ff = {5120: 13824, 4096: 14336}.get(d_model, 4 * d_model)   # Llama-2-13B / Mistral-7B MLP widths
+    layer = DecoderLayer(d_model, Hq, H, d, d_ff, cache, seed=1)
+    x = (torch.randn(n, d_model, generator=torch.Generator().manual_seed(2)) * 0.5).to(torch.bfloat16).to(dev)
+    bt_n, lens_n = bt[:n].contiguous(), lens[:n].to(dev)
+    max_len = int(lens[:n].max())
+    ws = torch.empty(max(1, B.attention_workspace_bytes(n, Hq, H, d, max_len)), dtype=torch.uint8, device=dev)
+    for _ in range(args.warmup):
+        layer.step(x, bt_n, lens_n, max_len, workspace=ws)
+    torch.cuda.synchronize()
+    ev = [{p: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for p in PHASES}
+          for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        layer.step(x, bt_n, lens_n, max_len, events=ev[i], workspace=ws)
+    torch.cuda.synchronize()
+    seq_s = (time.perf_counter() - t0) / args.steps
+    phase_ms = {p: sum(e[p][0].elapsed_time(e[p][1]) for e in ev) / args.steps for p in PHASES}
+    gpu_ms = sum(phase_ms.values())
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    halves = [n // 2, n - n // 2]
+    wss = [torch.empty(max(1, B.attention_workspace_bytes(m, Hq, H, d, max_len)), dtype=torch.uint8, device=dev)
+           for m in halves]
+    for _ in range(args.warmup):
+        layer.step_overlapped(x, bt_n, lens_n, max_len, streams, wss)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        layer.step_overlapped(x, bt_n, lens_n, max_len, streams, wss)
+    torch.cuda.synchronize()
+    ovl_s = (time.perf_counter() - t0) / args.steps
+    log(f"layer step: sequential {seq_s * 1e3:.3f} ms (phases {phase_ms}), two streams {ovl_s * 1e3:.3f} ms")
+    res = {
+        "metric": "decoder-layer decode step tokens/sec (quantize + attention inside a full layer)",
+        "value": round(n / min(seq_s, ovl_s), 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(min(seq_s, ovl_s) * 1e3, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16+f32", "data": "synthetic",
+        "config": {"workload": f"one {w.name} decoder layer (d_model {d_model}, {Hq}/{H} heads, MLP {d_ff}, "
+                               f"random bf16 weights), batch {n}, context {w.ctx_min}..{w.ctx}"
+                               + (", on-demand sparse pages" if args.paged else ""),
+                   "global_batch": n, "seq_len": max_len, "parallelism": "single GPU"},
+        "layer": {"sequential_ms": round(seq_s * 1e3, 4), "two_streams_ms": round(ovl_s * 1e3, 4),
+                  "phase_ms": {p: round(v, 4) for p, v in phase_ms.items()},
+                  "share": {p: round(v / gpu_ms, 4) for p, v in phase_ms.items()}},
+    }
+    print(json.dumps(res), flush=True)
 
 
 def main():
@@ -128,6 +191,9 @@ def main():
                     "fixed_record_pool_bytes": nblk * H * 2 * B.record_bytes(d)}
         log(f"sparse pages used: {used_pages}; pool {capacity['pool_bytes'] / 2**30:.2f} GiB "
             f"vs {capacity['fixed_record_pool_bytes'] / 2**30:.2f} GiB with fixed records")
+
+    if args.layer:
+        return layer_bench(args, w, cache, bt, lens, dev)
 
     k_new = synth.new_token_values(w, "k", 0, dev)
     v_new = synth.new_token_values(w, "v", 0, dev)
