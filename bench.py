@@ -43,6 +43,8 @@ def parse():
                     help="time a full decoder layer's decode step (random bf16 weights) around the cache")
     ap.add_argument("--layer-batch", type=int, default=0,
                     help="sequences in the layer step (0: the whole workload batch)")
+    ap.add_argument("--ratio-sweep", action="store_true",
+                    help="group-ratio trade-off: effective bits vs attention error for several (outer, inner) ratios")
     ap.add_argument("--cpu-sample-seqs", type=int, default=128)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -132,9 +134,68 @@ def layer_bench(args, w, cache, bt, lens, dev):
     print(json.dumps(res), flush=True)
 
 
+def ratio_sweep(args):
+    """Group-ratio trade-off (Sec. 6.2, accuracy vs compression ratio) on synthetic data:
+    for each (outer, inner) share, calibrate thresholds, quantize a cache, and report the
+    effective bits per element (from the stored bytes) and the decode-attention error
+    against fp32 attention over the unquantized fp16 keys and values."""
+    import numpy as np
+    import torch
+
+    from paper_2503_18599_amd import binding as B
+    from paper_2503_18599_amd import synth
+
+    dev = "cuda"
+    w = synth.scaled(synth.WORKLOADS[args.workload], n_seqs=32, ctx=1024)
+    H, Hq, d, n = w.n_kv_heads, w.n_q_heads, w.head_dim, w.n_seqs
+    G = Hq // H
+    lens = synth.seq_lengths(w)
+    bt_cpu, nblk = synth.block_table(w, lens)
+    bt = bt_cpu.to(dev)
+    k = [synth.kv_values_seq(w, "k", s, int(lens[s]), dev) for s in range(n)]
+    v = [synth.kv_values_seq(w, "v", s, int(lens[s]), dev) for s in range(n)]
+    kk, vv = torch.cat(k), torch.cat(v)
+    cu = torch.zeros(n + 1, dtype=torch.int32)
+    cu[1:] = torch.cumsum(lens, 0)
+    q = synth.queries(w, 0, dev)
+    scale = float(np.float32(1.0 / math.sqrt(d)))
+    # fp32 reference attention over the raw values
+    ref = []
+    for s in range(n):
+        kt = k[s].float().repeat_interleave(G, 1).permute(1, 2, 0).contiguous()   # [Hq][d][L]
+        vt = v[s].float().repeat_interleave(G, 1).permute(1, 0, 2).contiguous()   # [Hq][L][d]
+        sc = torch.bmm(q[s].float()[:, None, :], kt)[:, 0, :] * scale
+        ref.append(torch.bmm(torch.softmax(sc, -1)[:, None, :], vt)[:, 0, :])
+    ref = torch.stack(ref)
+    kc = synth.calibration_set(w, "k", dev)
+    vc = synth.calibration_set(w, "v", dev)
+    rows = []
+    grid = [(0.0, 0.0), (0.02, 0.03), (0.04, 0.06), (0.0, 0.10), (0.10, 0.0), (0.06, 0.04), (0.06, 0.09), (0.08, 0.12)]
+    for ro, ri in grid:
+        thr = B.calibrate_thresholds(kc, vc, ro, ri)
+        cache = B.Cache(nblk, H, d, thr)
+        B.quantize_kv(cache, kk, vv, bt, torch.zeros(n, dtype=torch.int32, device=dev), cu.to(dev), int(lens.max()))
+        out = B.decode_attention(cache, q, bt, lens.to(dev), int(lens.max()), scale)
+        err = float(((out - ref).norm() / ref.norm()).item())
+        rec = cache.pool.view(nblk, H, 2, cache.stride)
+        n_out = int(rec[:, :, :, :16 * (d // 64)].to(torch.int64).sum())   # the records' COO counts
+        n_el = int(lens.sum()) * H * 2 * d
+        # bits per element: 4-bit code + one COO byte per outlier + 12 B meta and d/64 count bytes per vector
+        bits = 4.0 + 8.0 * n_out / n_el + 8.0 * (12 + d // 64) / d
+        rows.append({"outer": ro, "inner": ri, "outlier_fraction": round(n_out / n_el, 4),
+                     "effective_bits": round(bits, 3), "attention_rel_err": round(err, 5)})
+        log(f"outer {ro:.2f} inner {ri:.2f}: outliers {n_out / n_el:.4f}, {bits:.3f} bits, attention err {err:.5f}")
+    print(json.dumps({"metric": "group-ratio trade-off (effective bits vs decode-attention relative L2 error)",
+                      "config": {"workload": f"{w.name}: {n} sequences x {w.ctx} tokens, {Hq}/{H} heads, d {d}"},
+                      "data": "synthetic", "reference": "fp32 attention over the unquantized fp16 K/V",
+                      "sweep": rows}), flush=True)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.ratio_sweep:
+        return ratio_sweep(args)
     if args.gpus != 1 or world != 1:
         print(json.dumps({"error": "this benchmark runs on exactly one GPU; multi-GPU runs are "
                                    "not part of this build", "n_gpus": args.gpus}))
