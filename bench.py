@@ -45,6 +45,8 @@ def parse():
                     help="sequences in the layer step (0: the whole workload batch)")
     ap.add_argument("--ratio-sweep", action="store_true",
                     help="group-ratio trade-off: effective bits vs attention error for several (outer, inner) ratios")
+    ap.add_argument("--prefill-chunk", type=int, default=0,
+                    help="time chunked-prefill attention for the last N cached tokens of every sequence")
     ap.add_argument("--cpu-sample-seqs", type=int, default=128)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -191,6 +193,54 @@ def ratio_sweep(args):
                       "sweep": rows}), flush=True)
 
 
+def prefill_bench(args, w, cache, bt, lens, dev):
+    """Chunked-prefill attention: the last C cached tokens of every sequence attend causally
+    over their prefixes (each query token reads its own prefix; the query heads of a KV
+    head share the reads)."""
+    import numpy as np
+    import torch
+
+    from paper_2503_18599_amd import binding as B
+
+    n, H, Hq, d = w.n_seqs, w.n_kv_heads, w.n_q_heads, w.head_dim
+    cached = lens - 1                                    # tokens in the cache
+    clen = torch.clamp(cached, max=args.prefill_chunk).to(torch.int32)
+    start = (cached - clen).to(torch.int32)
+    cu = torch.zeros(n + 1, dtype=torch.int32)
+    cu[1:] = torch.cumsum(clen, 0)
+    n_tok = int(cu[-1])
+    q = (torch.randn(n_tok, Hq, d, generator=torch.Generator().manual_seed(3))).to(torch.float16).to(dev)
+    max_len = int(lens.max())
+    scale = float(np.float32(1.0 / math.sqrt(d)))
+    out = torch.empty(n_tok, Hq, d, dtype=torch.float32, device=dev)
+    ws = torch.empty(max(1, int(B.lib().oaken_prefill_attention_workspace_bytes(n_tok, Hq, H, d, max_len, 0))),
+                     dtype=torch.uint8, device=dev)
+    args_d = (bt, start.to(dev), cu.to(dev), max_len, scale)
+    for _ in range(args.warmup):
+        B.prefill_attention(cache, q, *args_d, out=out, workspace=ws)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        B.prefill_attention(cache, q, *args_d, out=out, workspace=ws)
+    e1.record()
+    torch.cuda.synchronize()
+    t = e0.elapsed_time(e1) / args.steps / 1e3
+    # bytes streamed: each query token reads (position + 1) keys and values of every KV head
+    pos1 = torch.cat([torch.arange(int(start[s]) + 1, int(cached[s]) + 1) for s in range(n)]).to(torch.int64)
+    vec = 2 * H * int(pos1.sum())
+    kv_bytes = vec * (d // 2 + d // 64 + 12 + 0.1 * d)   # 10 % outliers: one COO byte each
+    log(f"prefill attention: {n_tok} query tokens in {t * 1e6:.1f} us")
+    res = {"metric": "chunked-prefill attention query tokens/sec", "value": round(n_tok / t, 1), "unit": "tokens/s",
+           "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(t * 1e3, 4),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+           "config": {"workload": f"{w.name}: {n} sequences, chunks of the last {args.prefill_chunk} cached tokens "
+                                  f"({n_tok} query tokens), {Hq}/{H} heads, d {d}, context {w.ctx_min}..{w.ctx}",
+                      "global_batch": n, "seq_len": max_len, "parallelism": "single GPU"},
+           "kv_read_gbs": round(kv_bytes / t / 1e9, 1)}
+    print(json.dumps(res), flush=True)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -255,6 +305,8 @@ def main():
 
     if args.layer:
         return layer_bench(args, w, cache, bt, lens, dev)
+    if args.prefill_chunk:
+        return prefill_bench(args, w, cache, bt, lens, dev)
 
     k_new = synth.new_token_values(w, "k", 0, dev)
     v_new = synth.new_token_values(w, "v", 0, dev)

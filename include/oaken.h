@@ -225,6 +225,28 @@ int oaken_decode_attention_window(const oaken_cache* cache, const void* q, int32
                                   int32_t sliding_window, float softmax_scale, float* out,
                                   void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * Chunked-prefill attention over the quantized cache (prefill reads the KV cache of the
+ * earlier tokens, Sec. 2.1; the sliding window of Sec. 6.1 applies per query).  q: fp16
+ * [n_tokens][n_q_heads][head_dim], the queries of new tokens; rows cu_tokens[s] ..
+ * cu_tokens[s+1]-1 belong to sequence s and sit at positions start_pos[s] + i (the layout
+ * and arrays of oaken_quantize_kv).  The query at position p attends causally over its
+ * sequence's keys max(0, p + 1 - W) .. p (W = sliding_window, 0 = no window), which must
+ * already be in the cache: quantize the chunk's keys and values first.
+ * out: fp32 [n_tokens][n_q_heads][head_dim].  Every p + 1 <= max_seq_len.
+ * Each query reads its own prefix: keys are shared by the query heads of a KV head, not
+ * across the tokens of a chunk.  workspace: oaken_prefill_attention_workspace_bytes(...)
+ * bytes (never 0 for valid sizes: it holds the token-to-sequence map).
+ */
+size_t oaken_prefill_attention_workspace_bytes(int32_t n_tokens, int32_t n_q_heads, int32_t n_kv_heads,
+                                               int32_t head_dim, int32_t max_seq_len, int32_t sliding_window);
+
+int oaken_prefill_attention(const oaken_cache* cache, const void* q, int32_t n_q_heads,
+                            const int32_t* block_table, int32_t max_blocks_per_seq, const int32_t* start_pos,
+                            const int32_t* cu_tokens, int32_t n_seqs, int32_t n_tokens, int32_t max_seq_len,
+                            int32_t sliding_window, float softmax_scale, float* out, void* workspace,
+                            size_t workspace_bytes, void* stream);
+
 /* Static description of a status code. */
 const char* oaken_status_string(int status);
 

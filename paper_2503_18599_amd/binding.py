@@ -62,6 +62,11 @@ def lib():
     L.oaken_sparse_release.restype = ctypes.c_int
     L.oaken_sparse_status.argtypes = [ctypes.POINTER(_CacheStruct), ctypes.POINTER(i32), ctypes.POINTER(i32), P]
     L.oaken_sparse_status.restype = ctypes.c_int
+    L.oaken_prefill_attention_workspace_bytes.argtypes = [i32, i32, i32, i32, i32, i32]
+    L.oaken_prefill_attention_workspace_bytes.restype = sz
+    L.oaken_prefill_attention.argtypes = [ctypes.POINTER(_CacheStruct), P, i32, P, i32, P, P, i32, i32, i32, i32,
+                                          f32, P, P, sz, P]
+    L.oaken_prefill_attention.restype = ctypes.c_int
     L.oaken_record_layout.argtypes = [i32, i32, P]
     L.oaken_record_layout.restype = ctypes.c_int
     L.oaken_calibrate_workspace_bytes.argtypes = [i32, i32]
@@ -247,4 +252,28 @@ def decode_attention(cache: Cache, q: torch.Tensor, block_table: torch.Tensor, s
             cache.struct, _dev(q, torch.float16, "q"), Hq, _dev(block_table, torch.int32, "block_table"),
             block_table.shape[1], _dev(seq_lens, torch.int32, "seq_lens"), n_seqs, int(max_seq_len),
             float(scale), _dev(out, torch.float32, "out"), ws_ptr, ws_bytes, _stream()))
+    return out
+
+
+def prefill_attention(cache: Cache, q: torch.Tensor, block_table: torch.Tensor, start_pos: torch.Tensor,
+                      cu_tokens: torch.Tensor, max_seq_len: int, scale: float, window: int = 0,
+                      out: torch.Tensor | None = None, workspace: torch.Tensor | None = None) -> torch.Tensor:
+    """Chunked-prefill attention: fp16 q [n_tokens][Hq][d] of new tokens (already quantized
+    into the cache) -> fp32 out [n_tokens][Hq][d]; each query attends causally over its
+    sequence's keys up to its own position."""
+    n_tokens, Hq, d = q.shape
+    n_seqs = start_pos.numel()
+    if d != cache.head_dim or cu_tokens.numel() != n_seqs + 1 or block_table.shape[0] != n_seqs:
+        raise ValueError("q / start_pos / cu_tokens / block_table shapes disagree")
+    if out is None:
+        out = torch.empty(n_tokens, Hq, d, dtype=torch.float32, device=q.device)
+    ws_bytes = int(lib().oaken_prefill_attention_workspace_bytes(n_tokens, Hq, cache.n_kv_heads, d,
+                                                                 int(max_seq_len), int(window)))
+    if workspace is None or workspace.numel() < ws_bytes:
+        workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=q.device)
+    _check(lib().oaken_prefill_attention(
+        cache.struct, _dev(q, torch.float16, "q"), Hq, _dev(block_table, torch.int32, "block_table"),
+        block_table.shape[1], _dev(start_pos, torch.int32, "start_pos"), _dev(cu_tokens, torch.int32, "cu_tokens"),
+        n_seqs, n_tokens, int(max_seq_len), int(window), float(scale), _dev(out, torch.float32, "out"),
+        workspace.data_ptr(), ws_bytes, _stream()))
     return out

@@ -77,6 +77,64 @@ int hip_status(hipError_t e, const char* what) {
     return fail(OAKEN_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
+// Attention over n_rows query rows: sequences (seq_lens) or prefill tokens (tok_seq/tok_pos).
+int attention_rows(const oaken_cache* cache, const void* q, int32_t n_q_heads, const int32_t* block_table,
+                   int32_t max_blocks_per_seq, const int32_t* seq_lens, const int32_t* tok_seq,
+                   const int32_t* tok_pos, int32_t n_rows, int32_t max_seq_len, int32_t sliding_window,
+                   float softmax_scale, float* out, void* workspace, size_t workspace_bytes, void* stream) {
+    int st = check_cache(cache);
+    if (st != OAKEN_OK) return st;
+    if (!q || !block_table || !out)
+        return fail(OAKEN_ERR_INVALID_ARG, "a device array argument is NULL");
+    if (n_rows <= 0 || max_seq_len <= 0 || max_blocks_per_seq <= 0 || n_q_heads <= 0)
+        return fail(OAKEN_ERR_INVALID_ARG, "sizes must be positive");
+    if (n_q_heads % cache->n_kv_heads != 0)
+        return fail(OAKEN_ERR_INVALID_ARG, "n_q_heads %d not a multiple of n_kv_heads %d", n_q_heads,
+                    cache->n_kv_heads);
+    if (n_q_heads / cache->n_kv_heads > 8)
+        return fail(OAKEN_ERR_UNSUPPORTED, "more than 8 query heads per KV head");
+    if ((int64_t)max_blocks_per_seq * oaken::kPage < max_seq_len)
+        return fail(OAKEN_ERR_INVALID_ARG, "block table too narrow for max_seq_len");
+    if (!std::isfinite(softmax_scale)) return fail(OAKEN_ERR_INVALID_ARG, "softmax_scale not finite");
+    if (sliding_window < 0) return fail(OAKEN_ERR_INVALID_ARG, "sliding_window must be >= 0");
+    if (cache->sparse_pool && !oaken::mfma_attention_supported(cache->head_dim, n_q_heads / cache->n_kv_heads))
+        return fail(OAKEN_ERR_UNSUPPORTED,
+                    "on-demand sparse pages need head_dim 128 and 1, 2 or 4 query heads per KV head");
+    const size_t need = oaken_attention_workspace_bytes_window(n_rows, n_q_heads, cache->n_kv_heads,
+                                                               cache->head_dim, max_seq_len, sliding_window);
+    if (need > 0 && (!workspace || workspace_bytes < need))
+        return fail(OAKEN_ERR_WORKSPACE, "attention workspace %zu < %zu bytes", workspace_bytes, need);
+    const oaken::SplitPlan sp = oaken::plan_splits(n_rows, n_q_heads, cache->n_kv_heads, cache->head_dim,
+                                                   attention_span(max_seq_len, sliding_window));
+    oaken::AttnArgs a{};
+    a.pool = static_cast<const uint8_t*>(cache->pool);
+    a.thr = cache->thresholds;
+    a.q = static_cast<const uint16_t*>(q);
+    a.block_table = block_table;
+    a.seq_lens = seq_lens;
+    a.tok_seq = tok_seq;
+    a.tok_pos = tok_pos;
+    a.out = out;
+    a.partial = static_cast<float*>(workspace);
+    a.stride = cache->record_stride;
+    a.num_blocks = cache->num_blocks;
+    a.H = cache->n_kv_heads;
+    a.Hq = n_q_heads;
+    a.max_blocks = max_blocks_per_seq;
+    a.n_seqs = n_rows;
+    a.max_seq_len = max_seq_len;
+    a.pages_per_split = sp.pages_per_split;
+    a.n_splits = sp.n_splits;
+    a.window = sliding_window;
+    a.scale = softmax_scale;
+    a.spool = static_cast<const uint8_t*>(cache->sparse_pool);
+    a.spages = cache->sparse_pages;
+    return hip_status(oaken::launch_attention(a, cache->head_dim, static_cast<hipStream_t>(stream)),
+                      "attention launch");
+}
+
+size_t round_up_sz(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
 }  // namespace
 
 extern "C" {
@@ -250,53 +308,48 @@ int oaken_decode_attention_window(const oaken_cache* cache, const void* q, int32
                                   const int32_t* seq_lens, int32_t n_seqs, int32_t max_seq_len,
                                   int32_t sliding_window, float softmax_scale, float* out,
                                   void* workspace, size_t workspace_bytes, void* stream) {
-    int st = check_cache(cache);
-    if (st != OAKEN_OK) return st;
-    if (!q || !block_table || !seq_lens || !out)
-        return fail(OAKEN_ERR_INVALID_ARG, "a device array argument is NULL");
-    if (n_seqs <= 0 || max_seq_len <= 0 || max_blocks_per_seq <= 0 || n_q_heads <= 0)
-        return fail(OAKEN_ERR_INVALID_ARG, "sizes must be positive");
-    if (n_q_heads % cache->n_kv_heads != 0)
-        return fail(OAKEN_ERR_INVALID_ARG, "n_q_heads %d not a multiple of n_kv_heads %d", n_q_heads,
-                    cache->n_kv_heads);
-    if (n_q_heads / cache->n_kv_heads > 8)
-        return fail(OAKEN_ERR_UNSUPPORTED, "more than 8 query heads per KV head");
-    if ((int64_t)max_blocks_per_seq * oaken::kPage < max_seq_len)
-        return fail(OAKEN_ERR_INVALID_ARG, "block table too narrow for max_seq_len");
-    if (!std::isfinite(softmax_scale)) return fail(OAKEN_ERR_INVALID_ARG, "softmax_scale not finite");
-    if (sliding_window < 0) return fail(OAKEN_ERR_INVALID_ARG, "sliding_window must be >= 0");
-    if (cache->sparse_pool && !oaken::mfma_attention_supported(cache->head_dim, n_q_heads / cache->n_kv_heads))
-        return fail(OAKEN_ERR_UNSUPPORTED,
-                    "on-demand sparse pages need head_dim 128 and 1, 2 or 4 query heads per KV head");
-    const size_t need = oaken_attention_workspace_bytes_window(n_seqs, n_q_heads, cache->n_kv_heads,
-                                                               cache->head_dim, max_seq_len, sliding_window);
-    if (need > 0 && (!workspace || workspace_bytes < need))
-        return fail(OAKEN_ERR_WORKSPACE, "attention workspace %zu < %zu bytes", workspace_bytes, need);
-    const oaken::SplitPlan sp = oaken::plan_splits(n_seqs, n_q_heads, cache->n_kv_heads, cache->head_dim,
-                                                   attention_span(max_seq_len, sliding_window));
-    oaken::AttnArgs a{};
-    a.pool = static_cast<const uint8_t*>(cache->pool);
-    a.thr = cache->thresholds;
-    a.q = static_cast<const uint16_t*>(q);
-    a.block_table = block_table;
-    a.seq_lens = seq_lens;
-    a.out = out;
-    a.partial = static_cast<float*>(workspace);
-    a.stride = cache->record_stride;
-    a.num_blocks = cache->num_blocks;
-    a.H = cache->n_kv_heads;
-    a.Hq = n_q_heads;
-    a.max_blocks = max_blocks_per_seq;
-    a.n_seqs = n_seqs;
-    a.max_seq_len = max_seq_len;
-    a.pages_per_split = sp.pages_per_split;
-    a.n_splits = sp.n_splits;
-    a.window = sliding_window;
-    a.scale = softmax_scale;
-    a.spool = static_cast<const uint8_t*>(cache->sparse_pool);
-    a.spages = cache->sparse_pages;
-    return hip_status(oaken::launch_attention(a, cache->head_dim, static_cast<hipStream_t>(stream)),
-                      "attention launch");
+    if (!seq_lens) return fail(OAKEN_ERR_INVALID_ARG, "a device array argument is NULL");
+    return attention_rows(cache, q, n_q_heads, block_table, max_blocks_per_seq, seq_lens, nullptr, nullptr, n_seqs,
+                          max_seq_len, sliding_window, softmax_scale, out, workspace, workspace_bytes, stream);
+}
+
+size_t oaken_prefill_attention_workspace_bytes(int32_t n_tokens, int32_t n_q_heads, int32_t n_kv_heads,
+                                               int32_t head_dim, int32_t max_seq_len, int32_t sliding_window) {
+    if (n_tokens <= 0) return 0;
+    const size_t part = oaken_attention_workspace_bytes_window(n_tokens, n_q_heads, n_kv_heads, head_dim,
+                                                               max_seq_len, sliding_window);
+    if (part == 0 && !(n_q_heads > 0 && n_kv_heads > 0 && n_q_heads % n_kv_heads == 0 && supported_dim(head_dim) &&
+                       max_seq_len > 0))
+        return 0;
+    return round_up_sz(part, 256) + 2 * round_up_sz((size_t)n_tokens * 4, 256);
+}
+
+int oaken_prefill_attention(const oaken_cache* cache, const void* q, int32_t n_q_heads,
+                            const int32_t* block_table, int32_t max_blocks_per_seq, const int32_t* start_pos,
+                            const int32_t* cu_tokens, int32_t n_seqs, int32_t n_tokens, int32_t max_seq_len,
+                            int32_t sliding_window, float softmax_scale, float* out, void* workspace,
+                            size_t workspace_bytes, void* stream) {
+    if (!start_pos || !cu_tokens) return fail(OAKEN_ERR_INVALID_ARG, "a device array argument is NULL");
+    if (n_seqs <= 0 || n_tokens <= 0) return fail(OAKEN_ERR_INVALID_ARG, "n_seqs and n_tokens must be positive");
+    const size_t need = oaken_prefill_attention_workspace_bytes(n_tokens, n_q_heads, cache ? cache->n_kv_heads : 0,
+                                                                cache ? cache->head_dim : 0, max_seq_len,
+                                                                sliding_window);
+    if (need == 0) return fail(OAKEN_ERR_INVALID_ARG, "unsupported sizes");
+    if (!workspace || workspace_bytes < need)
+        return fail(OAKEN_ERR_WORKSPACE, "prefill attention workspace %zu < %zu bytes", workspace_bytes, need);
+    // workspace: [split partials][token -> sequence][token -> position]
+    const size_t part = need - 2 * round_up_sz((size_t)n_tokens * 4, 256);
+    int32_t* tok_seq = reinterpret_cast<int32_t*>(static_cast<uint8_t*>(workspace) + part);
+    int32_t* tok_pos = reinterpret_cast<int32_t*>(static_cast<uint8_t*>(workspace) + part +
+                                                  round_up_sz((size_t)n_tokens * 4, 256));
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    int rc = check_cache(cache);
+    if (rc != OAKEN_OK) return rc;
+    rc = hip_status(oaken::launch_token_map(cu_tokens, start_pos, n_seqs, n_tokens, tok_seq, tok_pos, st),
+                    "token map launch");
+    if (rc != OAKEN_OK) return rc;
+    return attention_rows(cache, q, n_q_heads, block_table, max_blocks_per_seq, nullptr, tok_seq, tok_pos, n_tokens,
+                          max_seq_len, sliding_window, softmax_scale, out, part ? workspace : nullptr, part, stream);
 }
 
 const char* oaken_status_string(int status) {

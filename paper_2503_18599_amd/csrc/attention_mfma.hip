@@ -657,7 +657,11 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
 
     const int lane = threadIdx.x;
     const int split = blockIdx.x, h = blockIdx.y, s = blockIdx.z;
-    const int L = max(0, min(a.seq_lens[s], min(a.max_seq_len, a.max_blocks * P)));
+    // row s: a sequence (decode), or a query token of a prefill chunk, which sees its
+    // sequence's keys up to its own position
+    const int srow = a.tok_seq ? a.tok_seq[s] : s;
+    const int Ls = a.tok_seq ? a.tok_pos[s] + 1 : a.seq_lens[s];
+    const int L = max(0, min(Ls, min(a.max_seq_len, a.max_blocks * P)));
     const int n_pages = (L + P - 1) / P;
     // a sliding window hides keys before lo; the ranges start at its first page
     const int lo = (a.window > 0 && L > a.window) ? L - a.window : 0;
@@ -665,7 +669,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
     const int p_end = min(n_pages, p_begin + a.pages_per_split);
     const int cap = a.pages_per_split * P;
     const int n_tok = max(0, min(L, p_end * P) - p_begin * P);
-    const int32_t* btab = a.block_table + (int64_t)s * a.max_blocks;
+    const int32_t* btab = a.block_table + (int64_t)srow * a.max_blocks;
     constexpr bool paged = PG;   // on-demand sparse pages
     // block ids of the range, one page per lane (a range spans at most 64 pages)
     const int blk_lane = (p_begin + lane < p_end) ? btab[p_begin + lane] : -1;

@@ -73,6 +73,10 @@ struct AttnArgs {
     float scale;
     const uint8_t* spool;         // on-demand sparse pages (nullptr: fixed records)
     int32_t spages;
+    // prefill chunks: row r is a query token of sequence tok_seq[r] at position tok_pos[r]
+    // (nullptr: row r is sequence r, of length seq_lens[r])
+    const int32_t* tok_seq;
+    const int32_t* tok_pos;
 };
 
 // Split-K plan used by both the workspace query and the launch.
@@ -96,6 +100,8 @@ hipError_t launch_sparse_release(const SparseArgs& a, const int32_t* block_ids, 
 hipError_t launch_quantize(const QuantArgs& a, int d, int max_new_per_seq, hipStream_t st);
 hipError_t launch_calibrate(const CalibArgs& a, hipStream_t st);
 hipError_t launch_attention(const AttnArgs& a, int d, hipStream_t st);
+hipError_t launch_token_map(const int32_t* cu_tokens, const int32_t* start_pos, int n_seqs, int n_tokens,
+                            int32_t* tok_seq, int32_t* tok_pos, hipStream_t st);
 
 // Matrix-core decode attention (head_dim 128; 1, 2 or 4 query heads per KV head).
 bool mfma_attention_supported(int d, int G);

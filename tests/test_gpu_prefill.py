@@ -1,0 +1,94 @@
+"""Chunked-prefill attention over the quantized cache: every query token of a chunk
+attends causally over its sequence's keys up to its own position.  The reference is the
+oracle's decode attention evaluated once per query token (its sequence's block table,
+length = position + 1), over the oracle's bit-identical cache."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2503_18599_amd import synth
+from tests.cases import Case, attention_tolerance, np16
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+P = 16
+
+
+@pytest.fixture(scope="module")
+def B():
+    from paper_2503_18599_amd import binding
+    binding.lib()
+    assert torch.cuda.is_available()
+    return binding
+
+
+def _run(B, ref, case, chunk, window=0, paged=False, seed=5):
+    """Cache all tokens (prefix, then the chunk), then prefill attention for the chunk's
+    queries; returns (got, want)."""
+    n, H, Hq, d = case.n_seqs, case.H, case.Hq, case.d
+    lens = case.lens
+    clen = torch.minimum(torch.as_tensor(chunk, dtype=torch.int32).expand(n), lens)   # chunk tokens per sequence
+    start = (lens - clen).to(torch.int32)
+    thr = torch.from_numpy(case.thr).to(DEV)
+    cache = B.Cache(case.num_blocks, H, d, thr, sparse_pages=4 * case.num_blocks * H * 2 if paged else 0)
+    bt = case.bt.to(DEV)
+    B.quantize_kv(cache, case.k.to(DEV), case.v.to(DEV), bt, torch.zeros(n, dtype=torch.int32, device=DEV),
+                  case.cu.to(DEV), int(lens.max()))
+    cu = torch.zeros(n + 1, dtype=torch.int32)
+    cu[1:] = torch.cumsum(clen, 0)
+    n_tok = int(cu[-1])
+    g = torch.Generator().manual_seed(seed)
+    q = torch.randn(n_tok, Hq, d, generator=g).to(torch.float16)
+    scale = float(np.float32(1.0 / math.sqrt(d)))
+    got = B.prefill_attention(cache, q.to(DEV), bt, start.to(DEV), cu.to(DEV), int(lens.max()), scale,
+                              window=window).cpu().numpy()
+    # oracle: one decode-attention row per query token
+    pool = case.oracle_pool(ref)
+    seq = np.concatenate([np.full(int(clen[s]), s) for s in range(n)])
+    pos = np.concatenate([np.arange(int(start[s]), int(lens[s])) for s in range(n)])
+    want = ref.decode_attention(pool, case.num_blocks, P, H, d, case.thr, np16(q), case.bt.numpy()[seq],
+                                (pos + 1).astype(np.int32), scale, window=window)
+    return got, want
+
+
+@pytest.mark.parametrize("cid,kw,chunk,window,paged", [
+    (3, dict(n_seqs=3, ctx=600), 37, 0, False),           # MHA, ragged chunk
+    (4, dict(n_seqs=4, ctx=700, ctx_min=40), 64, 0, False),  # GQA, chunk = whole prompt for short ones
+    (4, dict(n_seqs=4, ctx=700, ctx_min=40), 50, 100, False),  # GQA with a sliding window
+    (2, dict(n_seqs=3, ctx=203), 203, 0, False),          # whole prompts from position 0
+    (1, dict(), 16, 0, False)])
+def test_prefill_attention_matches_oracle(B, ref, cid, kw, chunk, window, paged):
+    case = Case(synth.scaled(synth.WORKLOADS[cid], **kw))
+    case.calibrate_oracle(ref)
+    got, want = _run(B, ref, case, chunk, window, paged)
+    ok, max_abs, max_rel = attention_tolerance(got, want)
+    print(f"{case.w.name} chunk {chunk} window {window}: {got.shape[0]} query tokens, max_abs={max_abs:.3e}")
+    assert ok, (max_abs, max_rel)
+
+
+def test_prefill_attention_paged(B, ref):
+    case = Case(synth.scaled(synth.WORKLOADS[3], n_seqs=3, ctx=600))
+    case.calibrate_oracle(ref)
+    got, want = _run(B, ref, case, 48, paged=True)
+    ok, max_abs, max_rel = attention_tolerance(got, want)
+    assert ok, (max_abs, max_rel)
+
+
+def test_prefill_last_token_is_decode(B, ref):
+    """The last query of a chunk sees the whole sequence: its output is decode attention's."""
+    case = Case(synth.scaled(synth.WORKLOADS[4], n_seqs=4, ctx=300, ctx_min=20))
+    case.calibrate_oracle(ref)
+    n, Hq, d = case.n_seqs, case.Hq, case.d
+    thr = torch.from_numpy(case.thr).to(DEV)
+    cache = B.Cache(case.num_blocks, case.H, d, thr)
+    bt = case.bt.to(DEV)
+    B.quantize_kv(cache, case.k.to(DEV), case.v.to(DEV), bt, torch.zeros(n, dtype=torch.int32, device=DEV),
+                  case.cu.to(DEV), int(case.lens.max()))
+    q = synth.queries(case.w).to(DEV)
+    dec = B.decode_attention(cache, q, bt, case.lens.to(DEV), int(case.lens.max()), 0.09)
+    pre = B.prefill_attention(cache, q, bt, (case.lens - 1).to(torch.int32).to(DEV),
+                              torch.arange(n + 1, dtype=torch.int32).to(DEV), int(case.lens.max()), 0.09)
+    assert torch.allclose(dec, pre, rtol=1e-5, atol=1e-6)
