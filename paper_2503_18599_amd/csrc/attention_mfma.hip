@@ -192,27 +192,39 @@ __device__ __forceinline__ uint4 ld16(const uint8_t* p) {
 // before the key pass and sits in the table's space; q (key pass) shares with oci (value
 // pass); tokc (key pass) shares with wv (value pass) and, after the value pass, with the
 // value corrections on their way to the output lanes.
+//
+// With one query head per KV head the correction walks take one token per lane, and the
+// table is token-major: row tg (64 bytes) holds the four classes at 16-byte slots rotated
+// by bits 1-2 of tg (so that lanes reading one class spread over the banks), each slot
+// the two nibble halves.  The key walk reads the query in fp16 (one byte of offset per
+// entry), and the value walk adds into corrections at an 8-byte stride (the channel's
+// dense offset doubles as its correction offset).
 template <int G>
 struct Smem {
-    __align__(16) uint8_t tab_[4 * GT * 2 * 8];   // tab float2 [COO class][token][nibble bit 3]; qi
+    __align__(16) uint8_t tab_[4 * GT * 2 * 8];   // correction table; qi
     __align__(16) uint8_t dense[GRP][PSTR];       // K: token rows of 64 bytes; V: channel rows of 8
-    __align__(16) uint8_t qo_[G * D * 4];         // q float [G][D] (keys); oci int [G][D] (values)
+    __align__(16) uint8_t qo_[G == 1 ? D * 8 : G * D * 4];   // q (keys); oci (values)
     __align__(16) uint8_t tw_[cmax(cmax(GT * 16, G * GT * 8), G * D * 4)];
     float pbase[G];
     float m[G], l[G];
     __align__(16) uint8_t head[GRP][CB];          // COO counts of a group's records
-    int start[GRP][P];                            // offset of each slot's COO bytes in its page
+    int start[G == 1 ? 1 : GRP][P];               // offset of each slot's COO bytes in its page
     __align__(16) uint8_t sparse[SPL + 80];       // page p's COO bytes at p*SSLOT; + slack for
                                                   // whole-dword reads past a bucket
 
-    // correction table [COO class][token][nibble bit 3]
+    // correction table [COO class][token][nibble bit 3] (several heads)
     __device__ float2 (&tab())[4][GT][2] { return *reinterpret_cast<float2 (*)[4][GT][2]>(tab_); }
     // query in fixed point (before the key pass)
     __device__ int (&qi())[G][D] { return *reinterpret_cast<int (*)[G][D]>(tab_); }
-    // query in fp32, the heads of a channel side by side (key pass)
+    // query in fp32, the heads of a channel side by side (key pass, several heads)
     __device__ float (&q())[D][G] { return *reinterpret_cast<float (*)[D][G]>(qo_); }
-    // value corrections of one group, fixed point (value pass)
-    __device__ int (&oci())[G][D] { return *reinterpret_cast<int (*)[G][D]>(qo_); }
+    // query in fp16 (key pass, one head)
+    __device__ __half (&q16())[D] { return *reinterpret_cast<__half (*)[D]>(qo_); }
+    // value corrections of one group, fixed point (value pass): [head][channel], or
+    // [channel][2] with one head
+    __device__ int& oci(int hd, int ch) {
+        return G == 1 ? reinterpret_cast<int*>(qo_)[2 * ch] : reinterpret_cast<int*>(qo_)[hd * D + ch];
+    }
     // base, Delta, Gp of the group's tokens (key pass)
     __device__ float4 (&tokc())[GT] { return *reinterpret_cast<float4 (*)[GT]>(tw_); }
     // value-pass weights of token pairs: 4 features, 4 limbs (value pass)
@@ -280,16 +292,38 @@ __device__ __forceinline__ Meta meta_words(const Grp& gr, int lane) {
     return Meta{m[0], m[1], m[2]};
 }
 
-// Start of each slot's COO bytes in its page, from group buffer b's counts.  Returns the
-// COO bytes used by the lane's page (lane >> 4) and whether every page fits its staging
-// slot.
+// The COO entries of the lane's token (lane = 16 * page + slot), in stream order: cnt
+// entries from byte st of its page's stream, the first c0 of them in chunk 0.  Carried
+// between groups packed in one register: st (bits 0-11), c0 (12-19), cnt (20-31).
+struct Run {
+    int st, c0, cnt;
+};
+__device__ __forceinline__ uint32_t pack_run(const Run& r) {
+    return (uint32_t)r.st | ((uint32_t)r.c0 << 12) | ((uint32_t)r.cnt << 20);
+}
+__device__ __forceinline__ Run unpack_run(uint32_t x) {
+    return Run{(int)(x & 0xfffu), (int)((x >> 12) & 0xffu), (int)(x >> 20)};
+}
+
+// Start of each slot's COO bytes in its page, from the group's counts in the head
+// buffer.  Returns the COO bytes used by the lane's page (lane >> 4) and whether every
+// page fits its staging slot; with one head, also the lane's own run.
 template <int G>
-__device__ __forceinline__ int group_layout(Smem<G>& S, const Grp& gr, int lane, bool& fits) {
+__device__ __forceinline__ int group_layout(Smem<G>& S, const Grp& gr, int lane, bool& fits, Run& run) {
     const int pg = lane >> 4, t = lane & 15;
     const int nv = pick4(pg, gr.nval[0], gr.nval[1], gr.nval[2], gr.nval[3]);
-    const int tot = (t < nv) ? (int)S.head[pg][2 * t] + (int)S.head[pg][2 * t + 1] : 0;
+    const int c0 = (t < nv) ? (int)S.head[pg][2 * t] : 0;
+    const int c1 = (t < nv) ? (int)S.head[pg][2 * t + 1] : 0;
+    const int tot = c0 + c1;
     const int incl = row_scan16(tot);
-    S.start[pg][t] = incl - tot;
+    if constexpr (G == 1) {
+        // a 64-value chunk has at most 64 entries; larger counts are not a valid record
+        run.st = incl - tot;
+        run.c0 = min(c0, 64);
+        run.cnt = max(0, min(run.c0 + min(c1, 64), SPCAP - run.st));
+    } else {
+        S.start[pg][t] = incl - tot;
+    }
     const int u0 = __builtin_amdgcn_readlane(incl, 15), u1 = __builtin_amdgcn_readlane(incl, 31);
     const int u2 = __builtin_amdgcn_readlane(incl, 47), u3 = __builtin_amdgcn_readlane(incl, 63);
     fits = max(max(u0, u1), max(u2, u3)) <= SSLOT;
@@ -343,9 +377,11 @@ __device__ __forceinline__ void token_table(Smem<G>& S, int tg, const Tok& T, fl
     const float x[4] = {T.b_il - T.base, T.b_ol - T.base, T.b_ih - T.base, T.b_oh - T.base};
     const float y[4] = {T.kd_i, T.kd_o, T.kd_i, T.kd_o};
 #pragma unroll
-    for (int cls = 0; cls < 4; ++cls)
-        *reinterpret_cast<float4*>(&S.tab()[cls][tg][0]) =
-            make_float4(w * x[cls], w * y[cls], w * (x[cls] - T.gp), w * y[cls]);
+    for (int cls = 0; cls < 4; ++cls) {
+        float4* row = G == 1 ? reinterpret_cast<float4*>(&S.tab_[tg * 64 + ((cls ^ ((tg >> 1) & 3)) << 4)])
+                             : reinterpret_cast<float4*>(&S.tab()[cls][tg][0]);
+        *row = make_float4(w * x[cls], w * y[cls], w * (x[cls] - T.gp), w * y[cls]);
+    }
 }
 
 // Per-lane bucket of COO entries: lane = (page of the pair, 64-value chunk, token).
@@ -558,7 +594,7 @@ __device__ __forceinline__ void value_corrections(Smem<G>& S, const AttnArgs& a,
             pt[nb][hd] = (G > 1 && k[nb].vt) ? sc[hd * cap + tok0 + k[nb].tg] : 1.0f;
     }
     const uint32_t nsh = (lane & 7) * 4;
-    const uint32_t occ = off_of(S, &S.oci()[0][((lane >> 4) & 1) * 64]);
+    const uint32_t occ = off_of(S, &S.oci(0, ((lane >> 4) & 1) * 64));
     const int maxc = wave_max_i(mc);
     // Every slot is computed and added; slots past the bucket add zero (no branches).
     // The loads of a block's slots come first, then its LDS additions, so that the
@@ -649,6 +685,196 @@ __device__ __forceinline__ void value_corrections(Smem<G>& S, const AttnArgs& a,
     }
 }
 
+// ---- one query head per KV head: one token per lane -----------------------------------
+//
+// Lane 16*page + slot walks every COO entry of its token, both chunks, as one run of the
+// staged stream.  The entries of a dword are decoded together, one byte per entry:
+// position bytes (128 + i - c0, whose top bit marks chunk 1), query and dense offsets,
+// nibble shifts and table slots.  Each entry then costs one OR per LDS address.  The
+// loop runs over the lane's whole dwords of entries (lanes leave it as their runs end),
+// and the last 1-3 entries are taken one by one.
+
+__device__ __forceinline__ uint32_t byte_at(uint32_t x, int i) { return (x >> (8 * i)) & 0xffu; }
+
+// base | byte i of x, and byte i of x << s, each one VALU operation with a sub-dword
+// operand select (i is a constant after unrolling).
+#define OAKEN_SDWA_OR(I)                                                                              \
+    asm("v_or_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_" #I " src1_sel:DWORD" \
+        : "=v"(r) : "v"(x), "v"(base))
+__device__ __forceinline__ uint32_t or_byte(uint32_t x, uint32_t base, int i) {
+    uint32_t r;
+    switch (i) {
+        case 0: OAKEN_SDWA_OR(0); break;
+        case 1: OAKEN_SDWA_OR(1); break;
+        case 2: OAKEN_SDWA_OR(2); break;
+        default: OAKEN_SDWA_OR(3); break;
+    }
+    return r;
+}
+#undef OAKEN_SDWA_OR
+#define OAKEN_SDWA_SHL(I)                                                                                  \
+    asm("v_lshlrev_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_" #I \
+        : "=v"(r) : "v"(sh), "v"(x))
+__device__ __forceinline__ uint32_t shl_byte(uint32_t x, uint32_t sh, int i) {
+    uint32_t r;
+    switch (i) {
+        case 0: OAKEN_SDWA_SHL(0); break;
+        case 1: OAKEN_SDWA_SHL(1); break;
+        case 2: OAKEN_SDWA_SHL(2); break;
+        default: OAKEN_SDWA_SHL(3); break;
+    }
+    return r;
+}
+#undef OAKEN_SDWA_SHL
+
+// Scores: each entry adds q_j * (true value - middle reading) to its token's score.
+template <bool PG>
+__device__ __forceinline__ void key_corrections_g1(Smem<1>& S, const AttnArgs& a, float* sc, float scale,
+                                                   const Run& r, bool staged, const Grp& gr, int tok0, int lane) {
+    const int pg = lane >> 4, t = lane & 15;
+    const uint32_t tbo = (uint32_t)lane * 64u;                    // the token's table row
+    const uint32_t swz = (uint32_t)((lane >> 1) & 3) * 0x10101010u;
+    const uint32_t qb = off_of(S, &S.q16()[0]);                   // 256-aligned
+    const uint32_t drow = off_of(S, &S.dense[pg][t * 64]);        // 64-aligned
+    float corr = 0.0f;
+    // one entry: query offset byte qo (channel * 2), dense offset byte dof (dword of the
+    // channel within the token row), nibble shift ns, table slot byte ct
+    auto entry = [&](uint32_t qo, uint32_t dof, uint32_t ns, uint32_t ct) {
+        const uint32_t dw = lds_at<uint32_t>(S, drow | dof);
+        const float q = __half2float(lds_at<__half>(S, qb | qo));
+        const uint32_t n = __builtin_amdgcn_ubfe(dw, ns, 4);
+        const float2 kv = lds_at<float2>(S, (tbo | ct) | (n & 8u));
+        corr = fmaf(q, fmaf((float)n, kv.y, kv.x), corr);
+    };
+    if (staged) {
+        const int pos = pg * SSLOT + r.st;
+        const uint32_t* w = reinterpret_cast<const uint32_t*>(&S.sparse[pos & ~3]);
+        const uint32_t sh = pos & 3;
+        uint32_t cur = w[0], nxt = w[1];
+        const uint32_t pc0 = 0x03020100u + (uint32_t)(128 - r.c0) * 0x01010101u;
+        auto decode = [&](int kk, uint32_t& qo4, uint32_t& do4, uint32_t& ns4, uint32_t& ct4) {
+            const uint32_t ent = __builtin_amdgcn_alignbyte(nxt, cur, sh);
+            const uint32_t chk = (pc0 + (uint32_t)kk * 0x01010101u) & 0x80808080u;
+            qo4 = ((ent << 1) & 0x7e7e7e7eu) | chk;       // channel * 2
+            do4 = (qo4 >> 2) & 0x3c3c3c3cu;               // (channel / 8) * 4
+            ns4 = ent;                                    // nibble shift: (byte << 2) mod 32
+            ct4 = ((ent >> 2) & 0x30303030u) ^ swz;
+        };
+        const int full = r.cnt & ~3;
+        for (int kk = 0; kk < full; kk += 4) {
+            uint32_t qo4, do4, ns4, ct4;
+            decode(kk, qo4, do4, ns4, ct4);
+            cur = nxt;
+            nxt = w[(kk >> 2) + 2];
+            // phases kept apart so that a dword's reads issue together
+            uint32_t dw[4];
+            float q[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                dw[i] = lds_at<uint32_t>(S, or_byte(do4, drow, i));
+                q[i] = __half2float(lds_at<__half>(S, qb | byte_at(qo4, i)));
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            uint32_t n[4];
+            float2 kv[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                n[i] = __builtin_amdgcn_ubfe(dw[i], shl_byte(ns4, 2u, i), 4);
+                kv[i] = lds_at<float2>(S, or_byte(ct4, tbo, i) | (n[i] & 8u));
+            }
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) corr = fmaf(q[i], fmaf((float)n[i], kv[i].y, kv[i].x), corr);
+        }
+        if (full < r.cnt) {
+            uint32_t qo4, do4, ns4, ct4;
+            decode(full, qo4, do4, ns4, ct4);
+            entry(byte_at(qo4, 0), byte_at(do4, 0), byte_at(ns4, 0) << 2, byte_at(ct4, 0));
+            if (full + 1 < r.cnt) entry(byte_at(qo4, 1), byte_at(do4, 1), byte_at(ns4, 1) << 2, byte_at(ct4, 1));
+            if (full + 2 < r.cnt) entry(byte_at(qo4, 2), byte_at(do4, 2), byte_at(ns4, 2) << 2, byte_at(ct4, 2));
+        }
+    } else {
+        for (int kk = 0; kk < r.cnt; ++kk) {
+            const uint32_t b = coo_byte<PG>(a, gr, pg, r.st + kk);
+            const uint32_t ch = (b & 63u) | (kk >= r.c0 ? 64u : 0u);
+            entry(ch * 2u, (ch >> 3) * 4u, (ch & 7u) * 4u, ((b >> 2) & 0x30u) ^ (swz & 0xffu));
+        }
+    }
+    const int nv = pick4(pg, gr.nval[0], gr.nval[1], gr.nval[2], gr.nval[3]);
+    if (t < nv) sc[tok0 + lane] += scale * corr;
+}
+
+// Values: each entry adds p_t * (true value - middle reading) to its channel, through the
+// table that already carries p_t and the group's fixed-point scale.
+template <bool PG>
+__device__ __forceinline__ void value_corrections_g1(Smem<1>& S, const AttnArgs& a, const Run& r, bool staged,
+                                                     const Grp& gr, int lane) {
+    const int pg = lane >> 4, t = lane & 15;
+    const uint32_t tbo = (uint32_t)lane * 64u;
+    const uint32_t swz = (uint32_t)((lane >> 1) & 3) * 0x10101010u;
+    const uint32_t dcol = off_of(S, &S.dense[pg][(t >> 3) * 4]);  // + 8 * channel
+    const uint32_t nsh = (uint32_t)(t & 7) * 4u;
+    const uint32_t occ = off_of(S, &S.oci(0, 0));                 // + 8 * channel; 1024-aligned
+    // one entry: channel offset x = 8 * channel, table slot byte ct
+    auto entry = [&](uint32_t x, uint32_t ct) {
+        const uint32_t dw = lds_at<uint32_t>(S, dcol | x);
+        const uint32_t n = __builtin_amdgcn_ubfe(dw, nsh, 4);
+        const float2 kv = lds_at<float2>(S, (tbo | ct) | (n & 8u));
+        atomicAdd(&const_cast<int&>(lds_at<int>(S, occ + x)), (int)fmaf((float)n, kv.y, kv.x));
+    };
+    if (staged) {
+        const int pos = pg * SSLOT + r.st;
+        const uint32_t* w = reinterpret_cast<const uint32_t*>(&S.sparse[pos & ~3]);
+        const uint32_t sh = pos & 3;
+        uint32_t cur = w[0], nxt = w[1];
+        const uint32_t pc0 = 0x03020100u + (uint32_t)(128 - r.c0) * 0x01010101u;
+        auto decode = [&](int kk, uint32_t& ch4, uint32_t& ct4) {
+            const uint32_t ent = __builtin_amdgcn_alignbyte(nxt, cur, sh);
+            const uint32_t chk = (pc0 + (uint32_t)kk * 0x01010101u) & 0x80808080u;
+            ch4 = (ent & 0x3f3f3f3fu) | (chk >> 1);               // channel per byte
+            ct4 = ((ent >> 2) & 0x30303030u) ^ swz;
+        };
+        const int full = r.cnt & ~3;
+        for (int kk = 0; kk < full; kk += 4) {
+            uint32_t ch4, ct4;
+            decode(kk, ch4, ct4);
+            cur = nxt;
+            nxt = w[(kk >> 2) + 2];
+            uint32_t x[4], dw[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                x[i] = shl_byte(ch4, 3u, i);
+                dw[i] = lds_at<uint32_t>(S, dcol | x[i]);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            uint32_t n[4];
+            float2 kv[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                n[i] = __builtin_amdgcn_ubfe(dw[i], nsh, 4);
+                kv[i] = lds_at<float2>(S, or_byte(ct4, tbo, i) | (n[i] & 8u));
+            }
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                atomicAdd(&const_cast<int&>(lds_at<int>(S, occ + x[i])), (int)fmaf((float)n[i], kv[i].y, kv[i].x));
+        }
+        if (full < r.cnt) {
+            uint32_t ch4, ct4;
+            decode(full, ch4, ct4);
+            entry(byte_at(ch4, 0) << 3, byte_at(ct4, 0));
+            if (full + 1 < r.cnt) entry(byte_at(ch4, 1) << 3, byte_at(ct4, 1));
+            if (full + 2 < r.cnt) entry(byte_at(ch4, 2) << 3, byte_at(ct4, 2));
+        }
+    } else {
+        for (int kk = 0; kk < r.cnt; ++kk) {
+            const uint32_t b = coo_byte<PG>(a, gr, pg, r.st + kk);
+            const uint32_t ch = (b & 63u) | (kk >= r.c0 ? 64u : 0u);
+            entry(ch * 8u, ((b >> 2) & 0x30u) ^ (swz & 0xffu));
+        }
+    }
+}
+
 template <int G, bool PG>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 : 1))) void attn_mfma_kernel(AttnArgs a) {
     constexpr int NRS = (G + 1) / 2;        // key-pass MFMA row sets (8 rows per head)
@@ -693,8 +919,13 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
     for (int hd = 0; hd < G; ++hd) {
         const uint16_t* qp = a.q + ((int64_t)s * a.Hq + h * G + hd) * D;
         const float x0 = h2f(qp[lane]), x1 = h2f(qp[lane + 64]);
-        S.q()[lane][hd] = x0;
-        S.q()[lane + 64][hd] = x1;
+        if constexpr (G == 1) {
+            S.q16()[lane] = __ushort_as_half(qp[lane]);
+            S.q16()[lane + 64] = __ushort_as_half(qp[lane + 64]);
+        } else {
+            S.q()[lane][hd] = x0;
+            S.q()[lane + 64][hd] = x1;
+        }
         const float mx = wave_max_nonneg(fmaxf(fabsf(x0), fabsf(x1)));
         const float sum = wave_sum(x0 + x1);
         const int sh = fix_shift(mx);
@@ -749,8 +980,11 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
     // (a staged page fits its slot, so its second chunk row is needed only within it)
     const bool stg1_in = 256 + (lane & 15) * 16 < SSLOT;
     bool fits_c, fits_n;
+    uint32_t run_c, run_n;   // (one head) the lane's COO run in the current and the next group
     {
-        const int used = group_layout(S, gc, lane, fits_c);
+        Run r;
+        const int used = group_layout(S, gc, lane, fits_c, r);
+        run_c = pack_run(r);
         wave_sync();
 #pragma unroll
         for (int pg = 0; pg < GRP; ++pg) dreg[pg] = ld16(gc.base[pg] + koff);
@@ -823,17 +1057,22 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         }
         // the walk's buckets leave the head buffer before the next group's heads replace it
         Bucket kb[GRP / 2];
+        if constexpr (G > 1) {
 #pragma unroll
-        for (int nb = 0; nb < GRP / 2; ++nb) kb[nb] = bucket_of(S, gc, 2 * nb, lane);
+            for (int nb = 0; nb < GRP / 2; ++nb) kb[nb] = bucket_of(S, gc, 2 * nb, lane);
+        }
         wave_sync();
         // next group: heads -> layout -> issue its sparse bytes and the heads after it
         Grp gnn = gn;
         int2 tab_nn = tab_n;
         fits_n = true;
+        run_n = 0;
         if (gn.npg > 0) {
             if (lane < 2 * GRP) *reinterpret_cast<uint4*>(&S.head[0][16 * lane]) = hreg;
             wave_sync();
-            const int used = group_layout(S, gn, lane, fits_n);
+            Run r;
+            const int used = group_layout(S, gn, lane, fits_n, r);
+            run_n = pack_run(r);
             wave_sync();
             sparse_chunks<PG>(a, gn, tab_n, used, lane, sreg0, sreg1);
             mreg = meta_words(gn, lane);
@@ -843,7 +1082,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         }
         wave_sync();
         // sparse part
-        if (staged)
+        if constexpr (G == 1)
+            key_corrections_g1<PG>(S, a, sc, a.scale, unpack_run(run_c), staged, gc, tok0, lane);
+        else if (staged)
             key_corrections<G, true, GRP / 2, PG>(S, a, sc, cap, a.scale, kb, gc, tok0, lane);
         else
             key_corrections<G, false, GRP / 2, PG>(S, a, sc, cap, a.scale, kb, gc, tok0, lane);
@@ -852,6 +1093,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         gn = gnn;
         tab_n = tab_nn;
         fits_c = fits_n;
+        run_c = run_n;
     }
 
     // the first value group's heads go out before the softmax
@@ -877,8 +1119,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
             S.m[hd] = mx;
             S.l[hd] = sum;
         }
-        S.oci()[hd][lane] = 0;
-        S.oci()[hd][lane + 64] = 0;
+        S.oci(hd, lane) = 0;
+        S.oci(hd, lane + 64) = 0;
     }
     if (lane < 2 * GRP) *reinterpret_cast<uint4*>(&S.head[0][16 * lane]) = hreg;
     wave_sync();
@@ -893,7 +1135,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
 #pragma unroll
     for (int hd = 0; hd < G; ++hd) pb[hd] = ocr[hd][0] = ocr[hd][1] = 0.0f;
     {
-        const int used = group_layout(S, gc, lane, fits_c);
+        Run r;
+        const int used = group_layout(S, gc, lane, fits_c, r);
+        run_c = pack_run(r);
         wave_sync();
 #pragma unroll
         for (int pg = 0; pg < GRP; ++pg) dreg[pg] = ld16(gc.base[pg] + voff);
@@ -961,17 +1205,22 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         }
         // the walk's buckets leave the head buffer before the next group's heads replace it
         Bucket kb[GRP / 2];
+        if constexpr (G > 1) {
 #pragma unroll
-        for (int nb = 0; nb < GRP / 2; ++nb) kb[nb] = bucket_of(S, gc, 2 * nb, lane);
+            for (int nb = 0; nb < GRP / 2; ++nb) kb[nb] = bucket_of(S, gc, 2 * nb, lane);
+        }
         wave_sync();
         // next group: heads -> layout -> issue its sparse bytes and the heads after it
         Grp gnn = gn;
         int2 tab_nn = tab_n;
         fits_n = true;
+        run_n = 0;
         if (gn.npg > 0) {
             if (lane < 2 * GRP) *reinterpret_cast<uint4*>(&S.head[0][16 * lane]) = hreg;
             wave_sync();
-            const int used = group_layout(S, gn, lane, fits_n);
+            Run r;
+            const int used = group_layout(S, gn, lane, fits_n, r);
+            run_n = pack_run(r);
             wave_sync();
             sparse_chunks<PG>(a, gn, tab_n, used, lane, sreg0, sreg1);
             mreg = meta_words(gn, lane);
@@ -1020,7 +1269,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
 #pragma unroll
             for (int nt = 0; nt < 8; ++nt) oacc[nt] += ldexpf(limbs(gacc[nt]), -e);
         }
-        if (staged)
+        if constexpr (G == 1)
+            value_corrections_g1<PG>(S, a, unpack_run(run_c), staged, gc, lane);
+        else if (staged)
             value_corrections<G, true, GRP / 2, PG>(S, a, sc, cap, kb, gc, tok0, lane);
         else
             value_corrections<G, false, GRP / 2, PG>(S, a, sc, cap, kb, gc, tok0, lane);
@@ -1028,15 +1279,16 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         // fold the group's integer sums into the fp32 outputs
 #pragma unroll
         for (int hd = 0; hd < G; ++hd) {
-            ocr[hd][0] += ldexpf((float)S.oci()[hd][lane], -fsh);
-            ocr[hd][1] += ldexpf((float)S.oci()[hd][lane + 64], -fsh);
-            S.oci()[hd][lane] = 0;
-            S.oci()[hd][lane + 64] = 0;
+            ocr[hd][0] += ldexpf((float)S.oci(hd, lane), -fsh);
+            ocr[hd][1] += ldexpf((float)S.oci(hd, lane + 64), -fsh);
+            S.oci(hd, lane) = 0;
+            S.oci(hd, lane + 64) = 0;
         }
         gc = gn;
         gn = gnn;
         tab_n = tab_nn;
         fits_c = fits_n;
+        run_c = run_n;
     }
 
 #pragma unroll
