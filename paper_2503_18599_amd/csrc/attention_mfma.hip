@@ -43,7 +43,12 @@ constexpr int CB = 32;                     // COO count bytes at the start of a 
 constexpr int cmax(int x, int y) { return x > y ? x : y; }
 constexpr int GRP = 4;                     // pages per group (two correction pairs)
 constexpr int GT = GRP * P;                // tokens per group
-constexpr int PSTR = 1024;                 // LDS stride of a page's dense bytes
+// LDS stride of a page's dense bytes.  With one query head the value pages are staged in
+// two token halves 576 bytes apart (a channel's dword of eight tokens at 4 * channel), so
+// that the halves and neighbouring pages fall on opposite bank halves.
+template <int G>
+constexpr int pstr() { return G == 1 ? 1088 : 1024; }
+constexpr int VHALF = 576;
 constexpr int SPCAP = P * D;               // sparse capacity of one record
 constexpr int SSLOT = 448;                 // staged COO bytes per page (larger pages: read from HBM)
 constexpr int SPL = GRP * SSLOT;           // group sparse bytes staged in LDS
@@ -197,13 +202,14 @@ __device__ __forceinline__ uint4 ld16(const uint8_t* p) {
 // table is token-major: row tg (64 bytes) holds the four classes at 16-byte slots rotated
 // by bits 1-2 of tg (so that lanes reading one class spread over the banks), each slot
 // the two nibble halves.  The key walk reads the query in fp16 (one byte of offset per
-// entry), and the value walk adds into corrections at an 8-byte stride (the channel's
-// dense offset doubles as its correction offset).
+// entry); in the value walk 4 * channel locates both the channel's dense dword and its
+// correction.
 template <int G>
 struct Smem {
     __align__(16) uint8_t tab_[4 * GT * 2 * 8];   // correction table; qi
-    __align__(16) uint8_t dense[GRP][PSTR];       // K: token rows of 64 bytes; V: channel rows of 8
-    __align__(16) uint8_t qo_[G == 1 ? D * 8 : G * D * 4];   // q (keys); oci (values)
+    __align__(16) uint8_t dense[GRP][pstr<G>()];  // K: token rows of 64 bytes; V: channel rows of 8
+                                                  // (one head: two halves of channel dwords)
+    __align__(16) uint8_t qo_[G * D * 4];         // q (keys); oci (values)
     __align__(16) uint8_t tw_[cmax(cmax(GT * 16, G * GT * 8), G * D * 4)];
     float pbase[G];
     float m[G], l[G];
@@ -220,11 +226,8 @@ struct Smem {
     __device__ float (&q())[D][G] { return *reinterpret_cast<float (*)[D][G]>(qo_); }
     // query in fp16 (key pass, one head)
     __device__ __half (&q16())[D] { return *reinterpret_cast<__half (*)[D]>(qo_); }
-    // value corrections of one group, fixed point (value pass): [head][channel], or
-    // [channel][2] with one head
-    __device__ int& oci(int hd, int ch) {
-        return G == 1 ? reinterpret_cast<int*>(qo_)[2 * ch] : reinterpret_cast<int*>(qo_)[hd * D + ch];
-    }
+    // value corrections of one group, fixed point (value pass)
+    __device__ int& oci(int hd, int ch) { return reinterpret_cast<int*>(qo_)[hd * D + ch]; }
     // base, Delta, Gp of the group's tokens (key pass)
     __device__ float4 (&tokc())[GT] { return *reinterpret_cast<float4 (*)[GT]>(tw_); }
     // value-pass weights of token pairs: 4 features, 4 limbs (value pass)
@@ -424,9 +427,9 @@ __device__ __forceinline__ float entry_delta(Smem<G>& S, uint32_t tbo, uint32_t 
     return fmaf((float)n, kv.y, kv.x);
 }
 
-static_assert(offsetof(Smem<1>, dense) == 4096 && offsetof(Smem<1>, qo_) == 8192 &&
-              offsetof(Smem<4>, qo_) == 8192 && sizeof(Smem<1>::tab_) >= sizeof(int) * 4 * D,
-              "LDS layout the correction addressing relies on");
+static_assert(offsetof(Smem<1>, dense) == 4096 && offsetof(Smem<1>, qo_) % 256 == 0 &&
+              offsetof(Smem<2>, qo_) == 8192 && offsetof(Smem<4>, qo_) == 8192 &&
+              sizeof(Smem<1>::tab_) >= sizeof(int) * 4 * D, "LDS layout the correction addressing relies on");
 
 template <int G>
 __device__ __forceinline__ uint32_t off_of(const Smem<G>& S, const void* p) {
@@ -812,12 +815,12 @@ __device__ __forceinline__ void value_corrections_g1(Smem<1>& S, const AttnArgs&
     const int pg = lane >> 4, t = lane & 15;
     const uint32_t tbo = (uint32_t)lane * 64u;
     const uint32_t swz = (uint32_t)((lane >> 1) & 3) * 0x10101010u;
-    const uint32_t dcol = off_of(S, &S.dense[pg][(t >> 3) * 4]);  // + 8 * channel
+    const uint32_t dcol = off_of(S, &S.dense[pg][(t >> 3) * VHALF]);  // + 4 * channel
     const uint32_t nsh = (uint32_t)(t & 7) * 4u;
-    const uint32_t occ = off_of(S, &S.oci(0, 0));                 // + 8 * channel; 1024-aligned
-    // one entry: channel offset x = 8 * channel, table slot byte ct
+    const uint32_t occ = off_of(S, &S.oci(0, 0));                     // + 4 * channel
+    // one entry: channel offset x = 4 * channel, table slot byte ct
     auto entry = [&](uint32_t x, uint32_t ct) {
-        const uint32_t dw = lds_at<uint32_t>(S, dcol | x);
+        const uint32_t dw = lds_at<uint32_t>(S, dcol + x);
         const uint32_t n = __builtin_amdgcn_ubfe(dw, nsh, 4);
         const float2 kv = lds_at<float2>(S, (tbo | ct) | (n & 8u));
         atomicAdd(&const_cast<int&>(lds_at<int>(S, occ + x)), (int)fmaf((float)n, kv.y, kv.x));
@@ -843,8 +846,8 @@ __device__ __forceinline__ void value_corrections_g1(Smem<1>& S, const AttnArgs&
             uint32_t x[4], dw[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                x[i] = shl_byte(ch4, 3u, i);
-                dw[i] = lds_at<uint32_t>(S, dcol | x[i]);
+                x[i] = shl_byte(ch4, 2u, i);
+                dw[i] = lds_at<uint32_t>(S, dcol + x[i]);
             }
             __builtin_amdgcn_sched_barrier(0);
             uint32_t n[4];
@@ -862,15 +865,15 @@ __device__ __forceinline__ void value_corrections_g1(Smem<1>& S, const AttnArgs&
         if (full < r.cnt) {
             uint32_t ch4, ct4;
             decode(full, ch4, ct4);
-            entry(byte_at(ch4, 0) << 3, byte_at(ct4, 0));
-            if (full + 1 < r.cnt) entry(byte_at(ch4, 1) << 3, byte_at(ct4, 1));
-            if (full + 2 < r.cnt) entry(byte_at(ch4, 2) << 3, byte_at(ct4, 2));
+            entry(byte_at(ch4, 0) << 2, byte_at(ct4, 0));
+            if (full + 1 < r.cnt) entry(byte_at(ch4, 1) << 2, byte_at(ct4, 1));
+            if (full + 2 < r.cnt) entry(byte_at(ch4, 2) << 2, byte_at(ct4, 2));
         }
     } else {
         for (int kk = 0; kk < r.cnt; ++kk) {
             const uint32_t b = coo_byte<PG>(a, gr, pg, r.st + kk);
             const uint32_t ch = (b & 63u) | (kk >= r.c0 ? 64u : 0u);
-            entry(ch * 8u, ((b >> 2) & 0x30u) ^ (swz & 0xffu));
+            entry(ch * 4u, ((b >> 2) & 0x30u) ^ (swz & 0xffu));
         }
     }
 }
@@ -1150,7 +1153,15 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         const int tok0 = (g0 - p_begin) * P;
         const bool staged = fits_c;
 #pragma unroll
-        for (int pg = 0; pg < GRP; ++pg) *reinterpret_cast<uint4*>(&S.dense[pg][lane * 16]) = dreg[pg];
+        for (int pg = 0; pg < GRP; ++pg) {
+            if constexpr (G == 1) {
+                // channels 2*lane and 2*lane+1: tokens 0-7 to the first half, 8-15 to the second
+                *reinterpret_cast<uint2*>(&S.dense[pg][lane * 8]) = make_uint2(dreg[pg].x, dreg[pg].z);
+                *reinterpret_cast<uint2*>(&S.dense[pg][VHALF + lane * 8]) = make_uint2(dreg[pg].y, dreg[pg].w);
+            } else {
+                *reinterpret_cast<uint4*>(&S.dense[pg][lane * 16]) = dreg[pg];
+            }
+        }
         // the next group's dense bytes go out as soon as these are staged
 #pragma unroll
         for (int pg = 0; pg < GRP; ++pg) dreg[pg] = ld16(gn.base[pg] + voff);
@@ -1253,11 +1264,11 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
                     av[2] = col(w0.z, w1.z, w2.z, w3.z);
                     av[3] = col(w0.w, w1.w, w2.w, w3.w);
                 }
-                const uint8_t* dsrc = &S.dense[pp + (g4 >> 1)][(g4 & 1) * 4];
+                const uint8_t* dsrc = &S.dense[pp + (g4 >> 1)][(g4 & 1) * (G == 1 ? VHALF : 4)];
 #pragma unroll
                 for (int nt = 0; nt < 8; ++nt) {
                     const int j = nt * 16 + (lane & 15);
-                    const uint32_t dw = *reinterpret_cast<const uint32_t*>(dsrc + j * 8);
+                    const uint32_t dw = *reinterpret_cast<const uint32_t*>(dsrc + j * (G == 1 ? 4 : 8));
                     gacc[nt] = mfma(av, features(dw), gacc[nt]);
                 }
             }
