@@ -62,6 +62,16 @@ def _load():
     lib.oaken_ref_calibrate.restype = i32
     lib.oaken_ref_max_threads.argtypes = []
     lib.oaken_ref_max_threads.restype = i32
+    lib.oaken_ref_variant_info.argtypes = [i32, P]
+    lib.oaken_ref_variant_info.restype = i32
+    lib.oaken_ref_variant_quantize_vector.argtypes = [i32, P, i32, P, P, P, P, P, P]
+    lib.oaken_ref_variant_quantize_vector.restype = i32
+    lib.oaken_ref_variant_dequantize_vector.argtypes = [i32, P, P, P, P, i32, P, P]
+    lib.oaken_ref_variant_dequantize_vector.restype = i32
+    lib.oaken_ref_variant_quantize.argtypes = [i32, P, i32, i32, i32, P, P, P, P, P, P]
+    lib.oaken_ref_variant_quantize.restype = i32
+    lib.oaken_ref_variant_dequantize.argtypes = [i32, P, P, P, P, i32, i32, i32, P, P]
+    lib.oaken_ref_variant_dequantize.restype = i32
     _lib = lib
     return lib
 
@@ -180,4 +190,92 @@ def calibrate(k_calib, v_calib, outer_ratio=0.04, inner_ratio=0.06):
                                      float(inner_ratio), _ptr(out))
     if rc != 0:
         raise ValueError("oracle calibrate: invalid ratios or shapes")
+    return out
+
+
+# --------------------------------------------------------------------------- #
+# Group-count variants (Sec. 6.2, number-of-groups study).
+VARIANTS = {"g3": 0, "g2": 1, "g4": 2, "g5": 3, "g4-o4": 4, "g5-o4": 5}
+
+
+def variant_info(variant: int) -> dict:
+    """Outer levels, inner levels, outlier magnitude bits, COO bits and bytes, groups."""
+    out = np.zeros(6, np.int32)
+    if _load().oaken_ref_variant_info(int(variant), _ptr(out)) != 0:
+        raise ValueError("unknown variant")
+    return dict(n_out=int(out[0]), n_in=int(out[1]), out_bits=int(out[2]), coo_bits=int(out[3]),
+                coo_bytes=int(out[4]), groups=int(out[5]))
+
+
+def variant_thresholds(variant: int, thr_a, thr_b=None) -> np.ndarray:
+    """The eight boundaries [..][8] = lo_ob, lo_oa, lo_ia, lo_ib, hi_ib, hi_ia, hi_oa, hi_ob from
+    calibrations at the variant's full shares (thr_a) and at its innermost/outermost level
+    shares (thr_b), each [..][4] = lo_o, lo_i, hi_i, hi_o.  Unused boundaries repeat a used one."""
+    info = variant_info(variant)
+    a = np.asarray(thr_a, np.float32)
+    b = a if thr_b is None else np.asarray(thr_b, np.float32)
+    lo_oa, lo_ia, hi_ia, hi_oa = a[..., 0], a[..., 1], a[..., 2], a[..., 3]
+    lo_ob, hi_ob = (b[..., 0], b[..., 3]) if info["n_out"] == 2 else (lo_oa, hi_oa)
+    lo_ib, hi_ib = (b[..., 1], b[..., 2]) if info["n_in"] == 2 else (lo_ia, hi_ia)
+    return np.ascontiguousarray(np.stack([lo_ob, lo_oa, lo_ia, lo_ib, hi_ib, hi_ia, hi_oa, hi_ob], -1))
+
+
+def variant_quantize_vector(variant: int, x, thr8) -> dict:
+    x = _bits16(x).reshape(-1)
+    d = x.size
+    info = variant_info(variant)
+    thr8 = np.ascontiguousarray(np.asarray(thr8, np.float32).reshape(8))
+    nib = np.zeros(d // 2, np.uint8)
+    coo = np.zeros(d * info["coo_bytes"], np.uint8)
+    counts = np.zeros(d // 64, np.uint8)
+    meta = np.zeros(2 * info["groups"], np.uint16)
+    n = ctypes.c_int(0)
+    if _load().oaken_ref_variant_quantize_vector(int(variant), _ptr(x), d, _ptr(thr8), _ptr(nib), _ptr(coo),
+                                                 _ptr(counts), _ptr(meta), ctypes.byref(n)) != 0:
+        raise ValueError("oracle variant quantize: invalid arguments")
+    return dict(nib=nib, coo=coo[: n.value * info["coo_bytes"]].copy(), counts=counts, meta=meta, n_coo=n.value)
+
+
+def variant_dequantize_vector(variant: int, enc: dict, thr8) -> np.ndarray:
+    info = variant_info(variant)
+    nib = np.ascontiguousarray(enc["nib"], dtype=np.uint8)
+    d = nib.size * 2
+    coo = np.zeros(d * info["coo_bytes"], np.uint8)
+    coo[: enc["coo"].size] = enc["coo"]
+    counts = np.ascontiguousarray(enc["counts"], dtype=np.uint8)
+    meta = np.ascontiguousarray(enc["meta"], dtype=np.uint16)
+    thr8 = np.ascontiguousarray(np.asarray(thr8, np.float32).reshape(8))
+    out = np.zeros(d, np.float64)
+    if _load().oaken_ref_variant_dequantize_vector(int(variant), _ptr(nib), _ptr(coo), _ptr(counts), _ptr(meta), d,
+                                                   _ptr(thr8), _ptr(out)) != 0:
+        raise ValueError("oracle variant dequantize: invalid encoding")
+    return out
+
+
+def variant_quantize(variant: int, x, thr8) -> dict:
+    """Batch encode fp16 [n][H][d] with per-head boundaries thr8 [H][8]."""
+    x = _bits16(x)
+    n, H, d = x.shape
+    info = variant_info(variant)
+    thr8 = np.ascontiguousarray(np.asarray(thr8, np.float32).reshape(H, 8))
+    out = dict(nib=np.zeros((n, H, d // 2), np.uint8), coo=np.zeros((n, H, d * info["coo_bytes"]), np.uint8),
+               counts=np.zeros((n, H, d // 64), np.uint8), meta=np.zeros((n, H, 2 * info["groups"]), np.uint16),
+               n_coo=np.zeros((n, H), np.int32))
+    if _load().oaken_ref_variant_quantize(int(variant), _ptr(x), n, H, d, _ptr(thr8), _ptr(out["nib"]),
+                                          _ptr(out["coo"]), _ptr(out["counts"]), _ptr(out["meta"]),
+                                          _ptr(out["n_coo"])) != 0:
+        raise ValueError("oracle variant quantize: invalid arguments")
+    return out
+
+
+def variant_dequantize(variant: int, enc: dict, thr8) -> np.ndarray:
+    """fp64 [n][H][d] from a batch encoding."""
+    n, H, half = enc["nib"].shape
+    d = 2 * half
+    thr8 = np.ascontiguousarray(np.asarray(thr8, np.float32).reshape(H, 8))
+    out = np.zeros((n, H, d), np.float64)
+    a = {k: np.ascontiguousarray(enc[k]) for k in ("nib", "coo", "counts", "meta")}
+    if _load().oaken_ref_variant_dequantize(int(variant), _ptr(a["nib"]), _ptr(a["coo"]), _ptr(a["counts"]),
+                                            _ptr(a["meta"]), n, H, d, _ptr(thr8), _ptr(out)) != 0:
+        raise ValueError("oracle variant dequantize: invalid encoding")
     return out

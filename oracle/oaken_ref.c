@@ -445,6 +445,239 @@ int oaken_ref_calibrate(const uint16_t* k_calib, const uint16_t* v_calib, int R,
     return 0;
 }
 
+/* ------------------------------------------------------------------------ */
+/* Group-count variants (Sec. 6.2, the number-of-groups study).  The paper    */
+/* compares its three groups with two groups (a COO entry of 6 index bits,   */
+/* the sign and one pad bit), four or five groups (two group bits: 9-bit COO */
+/* entries, padded) and 4-bit outliers (the sign moves into the nibble so    */
+/* that the COO entry keeps 8 bits).  The group layout of the four- and      */
+/* five-group variants is not given; the reading used here splits the outer */
+/* share (and, for five groups, the inner share) into two equal levels, the  */
+/* total outlier share staying at 10 %.                                      */
+/*                                                                           */
+/* thr8 = lo_ob, lo_oa, lo_ia, lo_ib, hi_ib, hi_ia, hi_oa, hi_ob: outer      */
+/* boundaries a (inner) and b (outermost), inner boundaries a (the middle's  */
+/* edge) and b (innermost).  Groups, numbered from the inside out: the       */
+/* innermost (not shifted), inner a (shifted by ib), middle (shifted by ia,  */
+/* or not shifted without inner groups), outer a (shifted by oa), outer b    */
+/* (shifted by ob).  A value on a boundary belongs to the inner side, as in  */
+/* Eq. 1.  Middle magnitudes have 3 bits; outliers 4 bits, or 3 bits with     */
+/* 4-bit outliers.  Codes are offset binary with the side on top, as in the  */
+/* three-group quantizer.                                                    */
+/*                                                                           */
+/* Per vector: nibbles (d/2 bytes, element j in byte j/2, even j low), COO   */
+/* entries in chunk then index order (1 or 2 bytes each, little endian),     */
+/* per-64-chunk counts, and meta = (Min, Delta) fp16 per group.             */
+/* COO entry = side << (6 + gb) | outlier group rank << 6 | index, gb = 1    */
+/* for up to two outlier groups and 2 otherwise; without the side bit for    */
+/* 4-bit outliers.                                                           */
+/* ------------------------------------------------------------------------ */
+
+enum { REF_V3 = 0, REF_V2 = 1, REF_V4 = 2, REF_V5 = 3, REF_V4_O4 = 4, REF_V5_O4 = 5 };
+
+/* out: n_out, n_in, outlier magnitude bits, COO bits, COO bytes, groups. */
+int oaken_ref_variant_info(int variant, int out[6])
+{
+    static const int tab[6][3] = {{1, 1, 4}, {1, 0, 4}, {2, 1, 4}, {2, 2, 4}, {2, 1, 3}, {2, 2, 3}};
+    if (variant < 0 || variant > 5) return -1;
+    const int n_out = tab[variant][0], n_in = tab[variant][1], ob = tab[variant][2];
+    const int n_outlier_groups = n_out + n_in;
+    const int gb = n_outlier_groups <= 2 ? 1 : 2;
+    const int coo_bits = 6 + gb + (ob == 4 ? 1 : 0);
+    out[0] = n_out;
+    out[1] = n_in;
+    out[2] = ob;
+    out[3] = coo_bits;
+    out[4] = coo_bits <= 8 ? 1 : 2;
+    out[5] = n_in + 1 + n_out;
+    return 0;
+}
+
+int oaken_ref_variant_quantize_vector(int variant, const uint16_t* x, int d, const float thr8[8],
+                                      uint8_t* nib, uint8_t* coo, uint8_t* counts, uint16_t* meta,
+                                      int* n_coo)
+{
+    int info[6];
+    if (oaken_ref_variant_info(variant, info) || d < 64 || d % 64) return -1;
+    const int n_out = info[0], n_in = info[1], ob = info[2], coo_bits = info[3], cb = info[4], ng = info[5];
+    const int gb = coo_bits - 6 - (ob == 4 ? 1 : 0);
+    const int mid = n_in;
+    const float lo_ob = thr8[0], lo_oa = thr8[1], lo_ia = thr8[2], lo_ib = thr8[3];
+    const float hi_ib = thr8[4], hi_ia = thr8[5], hi_oa = thr8[6], hi_ob = thr8[7];
+    float* a = (float*)malloc(sizeof(float) * d);
+    uint8_t* side = (uint8_t*)malloc(d);
+    uint8_t* grp = (uint8_t*)malloc(d);
+    uint8_t* code = (uint8_t*)malloc(d);
+
+    for (int j = 0; j < d; ++j) {
+        const float xf = oaken_ref_half_to_float(x[j]);
+        float t;
+        int g, shifted = 1;
+        if (n_out == 2 && (xf < lo_ob || xf > hi_ob)) {
+            g = mid + 2; side[j] = xf > hi_ob; t = side[j] ? hi_ob : lo_ob;
+        } else if (xf < lo_oa || xf > hi_oa) {
+            g = mid + 1; side[j] = xf > hi_oa; t = side[j] ? hi_oa : lo_oa;
+        } else if (n_in == 0) {
+            g = mid; shifted = 0; t = 0.0f;
+        } else if (xf < lo_ia || xf > hi_ia) {
+            g = mid; side[j] = xf > hi_ia; t = side[j] ? hi_ia : lo_ia;
+        } else if (n_in == 2 && (xf < lo_ib || xf > hi_ib)) {
+            g = 1; side[j] = xf > hi_ib; t = side[j] ? hi_ib : lo_ib;
+        } else {
+            g = 0; shifted = 0; t = 0.0f;
+        }
+        if (!shifted) {
+            side[j] = xf >= 0.0f;
+            a[j] = fabsf(xf);
+        } else {
+            a[j] = fabsf(xf - t);
+        }
+        grp[j] = (uint8_t)g;
+    }
+
+    for (int g = 0; g < ng; ++g) {
+        float mn = INFINITY, mx = -INFINITY;
+        int any = 0;
+        for (int j = 0; j < d; ++j)
+            if (grp[j] == g) {
+                any = 1;
+                if (a[j] < mn) mn = a[j];
+                if (a[j] > mx) mx = a[j];
+            }
+        if (!any) { mn = 0.0f; mx = 0.0f; }
+        const int bits = (g == mid) ? 3 : ob;
+        const int levels = (1 << bits) - 1;
+        const float range = mx - mn;
+        const float sigma = (range == 0.0f) ? 0.0f : (float)levels / range;   /* Eq. 2 */
+        for (int j = 0; j < d; ++j) {
+            if (grp[j] != g) continue;
+            const float r = rintf((a[j] - mn) * sigma);                        /* Eq. 3 */
+            int c = (int)r;
+            if (c < 0) c = 0;
+            if (c > levels) c = levels;
+            code[j] = (uint8_t)(side[j] ? (levels + 1) + c : levels - c);
+        }
+        meta[2 * g] = oaken_ref_float_to_half(mn);
+        meta[2 * g + 1] = oaken_ref_float_to_half(range / (float)levels);
+    }
+
+    memset(nib, 0, (size_t)d / 2);
+    for (int j = 0; j < d; ++j)
+        nib[j / 2] |= (uint8_t)((code[j] & 15) << (4 * (j & 1)));
+
+    int n = 0;
+    for (int c = 0; c < d / 64; ++c) {
+        int cnt = 0;
+        for (int j = c * 64; j < c * 64 + 64; ++j) {
+            if (grp[j] == mid) continue;
+            /* rank among the outlier groups, from the inside out */
+            const int rank = grp[j] < mid ? grp[j] : grp[j] - 1;
+            uint32_t e = ((uint32_t)rank << 6) | (uint32_t)(j & 63);
+            if (ob == 4) e |= (uint32_t)(code[j] >> 4) << (6 + gb);
+            coo[(size_t)n * cb] = (uint8_t)(e & 0xff);
+            if (cb == 2) coo[(size_t)n * cb + 1] = (uint8_t)(e >> 8);
+            ++n;
+            ++cnt;
+        }
+        counts[c] = (uint8_t)cnt;
+    }
+    *n_coo = n;
+    free(a);
+    free(side);
+    free(grp);
+    free(code);
+    return 0;
+}
+
+/* Dequantization of one variant-encoded vector, fp64 (the plain definition:
+ * the magnitude is Min + c * Delta, the value is the side's threshold plus or
+ * minus it, or +-magnitude for unshifted groups). */
+int oaken_ref_variant_dequantize_vector(int variant, const uint8_t* nib, const uint8_t* coo,
+                                        const uint8_t* counts, const uint16_t* meta, int d,
+                                        const float thr8[8], double* out)
+{
+    int info[6];
+    if (oaken_ref_variant_info(variant, info) || d < 64 || d % 64) return -1;
+    const int n_out = info[0], n_in = info[1], ob = info[2], coo_bits = info[3], cb = info[4], ng = info[5];
+    const int gb = coo_bits - 6 - (ob == 4 ? 1 : 0);
+    const int mid = n_in;
+    int* u = (int*)malloc(sizeof(int) * d);
+    uint8_t* grp = (uint8_t*)malloc(d);
+    for (int j = 0; j < d; ++j) {
+        u[j] = (nib[j / 2] >> (4 * (j & 1))) & 15;
+        grp[j] = (uint8_t)mid;
+    }
+    int e = 0;
+    for (int c = 0; c < d / 64; ++c)
+        for (int k = 0; k < counts[c]; ++k, ++e) {
+            uint32_t v = coo[(size_t)e * cb];
+            if (cb == 2) v |= (uint32_t)coo[(size_t)e * cb + 1] << 8;
+            const int j = c * 64 + (int)(v & 63);
+            const int rank = (int)((v >> 6) & ((1u << gb) - 1));
+            grp[j] = (uint8_t)(rank < mid ? rank : rank + 1);
+            if (ob == 4) u[j] |= (int)((v >> (6 + gb)) & 1) << 4;
+        }
+    const double th[8] = {thr8[0], thr8[1], thr8[2], thr8[3], thr8[4], thr8[5], thr8[6], thr8[7]};
+    for (int j = 0; j < d; ++j) {
+        const int g = grp[j];
+        if (g >= ng) { free(u); free(grp); return -1; }
+        const int bits = (g == mid) ? 3 : ob;
+        const int half = 1 << bits;
+        const int hi = u[j] >> bits;
+        const int c = hi ? u[j] - half : half - 1 - u[j];
+        const double mag = (double)oaken_ref_half_to_float(meta[2 * g]) +
+                           (double)c * (double)oaken_ref_half_to_float(meta[2 * g + 1]);
+        double lo_t, hi_t;
+        if (g == mid + 2)                { lo_t = th[0]; hi_t = th[7]; }
+        else if (g == mid + 1)           { lo_t = th[1]; hi_t = th[6]; }
+        else if (g == mid && n_in > 0)   { lo_t = th[2]; hi_t = th[5]; }
+        else if (g == 1 && n_in == 2)    { lo_t = th[3]; hi_t = th[4]; }
+        else                             { lo_t = 0.0; hi_t = 0.0; }
+        out[j] = hi ? hi_t + mag : lo_t - mag;
+    }
+    (void)n_out;
+    free(u);
+    free(grp);
+    return 0;
+}
+
+/* Batch over [n][H] vectors; thr8 per head ([H][8]), outputs laid out per vector:
+ * nib [n][H][d/2], coo [n][H][d * coo_bytes], counts [n][H][d/64], meta [n][H][2 * groups],
+ * n_coo [n][H]. */
+int oaken_ref_variant_quantize(int variant, const uint16_t* x, int n, int H, int d, const float* thr8,
+                               uint8_t* nib, uint8_t* coo, uint8_t* counts, uint16_t* meta, int32_t* n_coo)
+{
+    int info[6];
+    if (oaken_ref_variant_info(variant, info) || d < 64 || d % 64) return -1;
+    const int cb = info[4], ng = info[5];
+    int bad = 0;
+#pragma omp parallel for schedule(static) reduction(| : bad)
+    for (int64_t v = 0; v < (int64_t)n * H; ++v) {
+        const int h = (int)(v % H);
+        int nc = 0;
+        bad |= oaken_ref_variant_quantize_vector(variant, x + v * d, d, thr8 + 8 * h, nib + v * (d / 2),
+                                                 coo + v * d * cb, counts + v * (d / 64), meta + v * 2 * ng, &nc);
+        n_coo[v] = nc;
+    }
+    return bad ? -1 : 0;
+}
+
+int oaken_ref_variant_dequantize(int variant, const uint8_t* nib, const uint8_t* coo, const uint8_t* counts,
+                                 const uint16_t* meta, int n, int H, int d, const float* thr8, double* out)
+{
+    int info[6];
+    if (oaken_ref_variant_info(variant, info) || d < 64 || d % 64) return -1;
+    const int cb = info[4], ng = info[5];
+    int bad = 0;
+#pragma omp parallel for schedule(static) reduction(| : bad)
+    for (int64_t v = 0; v < (int64_t)n * H; ++v) {
+        const int h = (int)(v % H);
+        bad |= oaken_ref_variant_dequantize_vector(variant, nib + v * (d / 2), coo + v * d * cb, counts + v * (d / 64),
+                                                   meta + v * 2 * ng, d, thr8 + 8 * h, out + v * d);
+    }
+    return bad ? -1 : 0;
+}
+
 int oaken_ref_max_threads(void)
 {
 #ifdef _OPENMP

@@ -58,3 +58,60 @@ def order_stat_ok(values: np.ndarray, t: float, k: int, side: str) -> bool:
     if side == "low":
         return (v < t).sum() <= k < (v <= t).sum()
     return (v > t).sum() <= k < (v >= t).sum()
+
+
+# ---- group-count variants ----------------------------------------------------
+def variant_membership(x: np.ndarray, thr8, n_out: int, n_in: int) -> np.ndarray:
+    """Group of each value for the nested-interval variants, numbered from the inside
+    out (0 = innermost, n_in = middle, n_in + n_out = outermost), from the interval
+    definitions directly; asserts that the sets partition x.  Boundaries belong to the
+    inner side, as in Eq. 1."""
+    lo_ob, lo_oa, lo_ia, lo_ib, hi_ib, hi_ia, hi_oa, hi_ob = (float(t) for t in thr8)
+    x = np.asarray(x, dtype=np.float64)
+    inside = lambda lo, hi: (lo <= x) & (x <= hi)
+    sets = []
+    if n_in == 2:
+        sets.append(inside(lo_ib, hi_ib))                            # innermost
+        sets.append(inside(lo_ia, hi_ia) & ~inside(lo_ib, hi_ib))    # inner a
+    elif n_in == 1:
+        sets.append(inside(lo_ia, hi_ia))
+    mid = inside(lo_oa, hi_oa) & (~inside(lo_ia, hi_ia) if n_in else True)
+    sets.append(mid)
+    if n_out == 2:
+        sets.append(inside(lo_ob, hi_ob) & ~inside(lo_oa, hi_oa))    # outer a
+        sets.append(~inside(lo_ob, hi_ob))                           # outer b
+    else:
+        sets.append(~inside(lo_oa, hi_oa))
+    hits = sum(s.astype(int) for s in sets)
+    assert np.all(hits == 1), "the variant's sets must partition the values"
+    g = np.zeros(x.shape, int)
+    for k, s in enumerate(sets):
+        g[s] = k
+    return g
+
+
+def variant_shift(x: np.ndarray, grp: np.ndarray, thr8, n_out: int, n_in: int):
+    """(|x - T|, side) with T the boundary on the value's side between its group and the
+    next group inwards; the innermost group (and the middle without inner groups) is not
+    shifted and its side is x >= 0."""
+    lo_ob, lo_oa, lo_ia, lo_ib, hi_ib, hi_ia, hi_oa, hi_ob = (float(t) for t in thr8)
+    x = np.asarray(x, dtype=np.float64)
+    mid = n_in
+    lo = np.zeros(x.shape)
+    hi = np.zeros(x.shape)
+    shifted = np.ones(x.shape, bool)
+    for g in range(n_in + 1 + n_out):
+        sel = grp == g
+        if g == mid + 2:
+            lo[sel], hi[sel] = lo_ob, hi_ob
+        elif g == mid + 1:
+            lo[sel], hi[sel] = lo_oa, hi_oa
+        elif g == mid and n_in > 0:
+            lo[sel], hi[sel] = lo_ia, hi_ia
+        elif g == 1 and n_in == 2:
+            lo[sel], hi[sel] = lo_ib, hi_ib
+        else:
+            shifted[sel] = False
+    side = np.where(shifted, x > hi, x >= 0).astype(int)
+    t = np.where(shifted, np.where(side == 1, hi, lo), 0.0)
+    return np.abs(x - t), side
