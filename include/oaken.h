@@ -253,6 +253,51 @@ const char* oaken_status_string(int status);
 /* Detail of the last non-OK return on the calling thread ("" if none). */
 const char* oaken_last_error(void);
 
+/* ------------------------------------------------------------------------
+ * Group-count variants of the quantizer (Sec. 6.2, the number-of-groups study),
+ * for measuring accuracy against effective bits.  They write flat per-vector
+ * buffers, not page records; decode attention reads only the three-group records.
+ *
+ * variant: 0 three groups (the default encoding), 1 two groups (outer and middle;
+ * COO entry = sign, a zero pad bit, 6-bit index), 2 four groups (two outer levels,
+ * one inner), 3 five groups (two outer, two inner) -- 2 and 3 with 9-bit COO entries
+ * stored as little-endian uint16 --, 4 and 5 the four- and five-group layouts with
+ * 4-bit outliers (3 magnitude bits; the sign is the nibble's top bit and the COO
+ * entry keeps 8 bits).  A COO entry is (sign << (6 + r)) | (outlier group rank << 6) |
+ * index within the 64-value chunk, r = 1 for up to two outlier groups and 2 otherwise,
+ * without the sign for 4-bit outliers; ranks count the outlier groups from the
+ * inside out.
+ *
+ * Boundaries thr8 [n_kv_heads][8] = lo_ob, lo_oa, lo_ia, lo_ib, hi_ib, hi_ia, hi_oa,
+ * hi_ob (outer levels a and b, b outermost; inner levels a and b, b innermost); a
+ * variant ignores the levels it does not have.  Groups from the inside out: the
+ * innermost (not shifted), inner a (shifted by the b boundary on its side), middle
+ * (shifted by the a inner boundary; not shifted without inner groups), outer a
+ * (shifted by oa), outer b (shifted by ob).  Middle magnitudes use 3 bits, outliers
+ * 4 (or 3); codes are offset binary with the side on top, as in the three-group
+ * quantizer.
+ *
+ * Per vector (x is fp16 [n][n_kv_heads][head_dim], head_dim 64 or 128): nib [d/2]
+ * (element j in byte j/2, even j in the low nibble), coo [d * coo_bytes] (entries in
+ * chunk then index order), counts [d/64], meta [2 * groups] fp16 (Min, Delta) per
+ * group from the inside out, n_coo (int32).  All device pointers; asynchronous on
+ * stream.
+ * ------------------------------------------------------------------------ */
+
+/* out[6] = outer levels, inner levels, outlier magnitude bits, COO bits, COO bytes,
+ * groups.  Host only. */
+int oaken_variant_info(int32_t variant, int32_t* out);
+
+int oaken_variant_quantize(int32_t variant, const void* x, int32_t n, int32_t n_kv_heads, int32_t head_dim,
+                           const float* thr8, void* nib, void* coo, void* counts, void* meta, int32_t* n_coo,
+                           void* stream);
+
+/* out: fp32 [n][n_kv_heads][head_dim], the boundary on the value's side plus or minus
+ * Min + code * Delta of its group. */
+int oaken_variant_dequantize(int32_t variant, const void* nib, const void* coo, const void* counts,
+                             const void* meta, int32_t n, int32_t n_kv_heads, int32_t head_dim,
+                             const float* thr8, float* out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

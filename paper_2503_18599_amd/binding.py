@@ -85,6 +85,12 @@ def lib():
     L.oaken_decode_attention_window.argtypes = [ctypes.POINTER(_CacheStruct), P, i32, P, i32, P, i32, i32,
                                                 i32, f32, P, P, sz, P]
     L.oaken_decode_attention_window.restype = ctypes.c_int
+    L.oaken_variant_info.argtypes = [i32, P]
+    L.oaken_variant_info.restype = ctypes.c_int
+    L.oaken_variant_quantize.argtypes = [i32, P, i32, i32, i32, P, P, P, P, P, P, P]
+    L.oaken_variant_quantize.restype = ctypes.c_int
+    L.oaken_variant_dequantize.argtypes = [i32, P, P, P, P, i32, i32, i32, P, P, P]
+    L.oaken_variant_dequantize.restype = ctypes.c_int
     L.oaken_status_string.argtypes = [ctypes.c_int]
     L.oaken_status_string.restype = ctypes.c_char_p
     L.oaken_last_error.argtypes = []
@@ -276,4 +282,57 @@ def prefill_attention(cache: Cache, q: torch.Tensor, block_table: torch.Tensor, 
         block_table.shape[1], _dev(start_pos, torch.int32, "start_pos"), _dev(cu_tokens, torch.int32, "cu_tokens"),
         n_seqs, n_tokens, int(max_seq_len), int(window), float(scale), _dev(out, torch.float32, "out"),
         workspace.data_ptr(), ws_bytes, _stream()))
+    return out
+
+
+# --------------------------------------------------------------------------- #
+# Group-count variants (Sec. 6.2, number-of-groups study)
+VARIANTS = {"g3": 0, "g2": 1, "g4": 2, "g5": 3, "g4-o4": 4, "g5-o4": 5}
+
+
+def variant_info(variant: int) -> dict:
+    out = (ctypes.c_int32 * 6)()
+    _check(lib().oaken_variant_info(int(variant), out))
+    return dict(n_out=out[0], n_in=out[1], out_bits=out[2], coo_bits=out[3], coo_bytes=out[4], groups=out[5])
+
+
+def variant_boundaries(variant: int, thr_full: torch.Tensor, thr_level: torch.Tensor | None = None) -> torch.Tensor:
+    """[..][8] = lo_ob, lo_oa, lo_ia, lo_ib, hi_ib, hi_ia, hi_oa, hi_ob from thresholds [..][4]
+    (lo_o, lo_i, hi_i, hi_o) calibrated at the variant's full outer/inner shares and, for the
+    extra levels, at the outermost and innermost level shares."""
+    info = variant_info(variant)
+    a = thr_full
+    b = thr_level if thr_level is not None else thr_full
+    ob = (b[..., 0], b[..., 3]) if info["n_out"] == 2 else (a[..., 0], a[..., 3])
+    ib = (b[..., 1], b[..., 2]) if info["n_in"] == 2 else (a[..., 1], a[..., 2])
+    return torch.stack([ob[0], a[..., 0], a[..., 1], ib[0], ib[1], a[..., 2], a[..., 3], ob[1]], -1).contiguous()
+
+
+def variant_quantize(variant: int, x: torch.Tensor, thr8: torch.Tensor) -> dict:
+    """Encode fp16 [n][H][d] (d 64 or 128) with boundaries [H][8]; returns the buffers."""
+    n, H, d = x.shape
+    info = variant_info(variant)
+    dev = x.device
+    enc = dict(nib=torch.empty(n, H, d // 2, dtype=torch.uint8, device=dev),
+               coo=torch.zeros(n, H, d * info["coo_bytes"], dtype=torch.uint8, device=dev),
+               counts=torch.empty(n, H, d // 64, dtype=torch.uint8, device=dev),
+               meta=torch.empty(n, H, 2 * info["groups"], dtype=torch.int16, device=dev),
+               n_coo=torch.empty(n, H, dtype=torch.int32, device=dev))
+    if tuple(thr8.shape) != (H, 8):
+        raise ValueError("boundaries must be [n_kv_heads][8]")
+    _check(lib().oaken_variant_quantize(
+        int(variant), _dev(x, torch.float16, "x"), n, H, d, _dev(thr8, torch.float32, "thr8"),
+        enc["nib"].data_ptr(), enc["coo"].data_ptr(), enc["counts"].data_ptr(), enc["meta"].data_ptr(),
+        enc["n_coo"].data_ptr(), _stream()))
+    return enc
+
+
+def variant_dequantize(variant: int, enc: dict, thr8: torch.Tensor) -> torch.Tensor:
+    n, H, half = enc["nib"].shape
+    d = 2 * half
+    out = torch.empty(n, H, d, dtype=torch.float32, device=enc["nib"].device)
+    _check(lib().oaken_variant_dequantize(
+        int(variant), _dev(enc["nib"], torch.uint8, "nib"), _dev(enc["coo"], torch.uint8, "coo"),
+        _dev(enc["counts"], torch.uint8, "counts"), _dev(enc["meta"], torch.int16, "meta"), n, H, d,
+        _dev(thr8, torch.float32, "thr8"), out.data_ptr(), _stream()))
     return out

@@ -352,6 +352,67 @@ int oaken_prefill_attention(const oaken_cache* cache, const void* q, int32_t n_q
                           max_seq_len, sliding_window, softmax_scale, out, part ? workspace : nullptr, part, stream);
 }
 
+int oaken_variant_info(int32_t variant, int32_t* out) {
+    if (!out) return fail(OAKEN_ERR_INVALID_ARG, "variant info output NULL");
+    const oaken::VariantInfo v = oaken::variant_info(variant);
+    if (v.groups == 0) return fail(OAKEN_ERR_INVALID_ARG, "unknown variant %d", (int)variant);
+    const int32_t vals[6] = {v.n_out, v.n_in, v.out_bits, v.coo_bits, v.coo_bytes, v.groups};
+    for (int i = 0; i < 6; ++i) out[i] = vals[i];
+    return OAKEN_OK;
+}
+
+namespace {
+int variant_args(int32_t variant, int32_t n, int32_t n_kv_heads, int32_t head_dim, const float* thr8,
+                 oaken::VariantArgs& a) {
+    a = oaken::VariantArgs{};
+    a.info = oaken::variant_info(variant);
+    if (a.info.groups == 0) return fail(OAKEN_ERR_INVALID_ARG, "unknown variant %d", (int)variant);
+    if (n < 0 || n_kv_heads <= 0) return fail(OAKEN_ERR_INVALID_ARG, "sizes must be positive");
+    if (head_dim != 64 && head_dim != 128)
+        return fail(OAKEN_ERR_UNSUPPORTED, "variant encodings support head_dim 64 and 128, not %d", (int)head_dim);
+    if (!thr8) return fail(OAKEN_ERR_INVALID_ARG, "boundaries NULL");
+    a.thr8 = thr8;
+    a.n = n;
+    a.H = n_kv_heads;
+    return OAKEN_OK;
+}
+}  // namespace
+
+int oaken_variant_quantize(int32_t variant, const void* x, int32_t n, int32_t n_kv_heads, int32_t head_dim,
+                           const float* thr8, void* nib, void* coo, void* counts, void* meta, int32_t* n_coo,
+                           void* stream) {
+    oaken::VariantArgs a;
+    const int st = variant_args(variant, n, n_kv_heads, head_dim, thr8, a);
+    if (st != OAKEN_OK) return st;
+    if (n == 0) return OAKEN_OK;
+    if (!x || !nib || !coo || !counts || !meta || !n_coo) return fail(OAKEN_ERR_INVALID_ARG, "buffer NULL");
+    a.x = static_cast<const uint16_t*>(x);
+    a.nib = static_cast<uint8_t*>(nib);
+    a.coo = static_cast<uint8_t*>(coo);
+    a.counts = static_cast<uint8_t*>(counts);
+    a.meta = static_cast<uint16_t*>(meta);
+    a.n_coo = n_coo;
+    return hip_status(oaken::launch_variant_quantize(a, head_dim, static_cast<hipStream_t>(stream)),
+                      "variant quantize launch");
+}
+
+int oaken_variant_dequantize(int32_t variant, const void* nib, const void* coo, const void* counts,
+                             const void* meta, int32_t n, int32_t n_kv_heads, int32_t head_dim,
+                             const float* thr8, float* out, void* stream) {
+    oaken::VariantArgs a;
+    const int st = variant_args(variant, n, n_kv_heads, head_dim, thr8, a);
+    if (st != OAKEN_OK) return st;
+    if (n == 0) return OAKEN_OK;
+    if (!nib || !coo || !counts || !meta || !out) return fail(OAKEN_ERR_INVALID_ARG, "buffer NULL");
+    a.nib = const_cast<uint8_t*>(static_cast<const uint8_t*>(nib));
+    a.coo = const_cast<uint8_t*>(static_cast<const uint8_t*>(coo));
+    a.counts = const_cast<uint8_t*>(static_cast<const uint8_t*>(counts));
+    a.meta = const_cast<uint16_t*>(static_cast<const uint16_t*>(meta));
+    a.out = out;
+    return hip_status(oaken::launch_variant_dequantize(a, head_dim, static_cast<hipStream_t>(stream)),
+                      "variant dequantize launch");
+}
+
 const char* oaken_status_string(int status) {
     switch (status) {
         case OAKEN_OK: return "ok";

@@ -103,6 +103,26 @@ hipError_t launch_attention(const AttnArgs& a, int d, hipStream_t st);
 hipError_t launch_token_map(const int32_t* cu_tokens, const int32_t* start_pos, int n_seqs, int n_tokens,
                             int32_t* tok_seq, int32_t* tok_pos, hipStream_t st);
 
+// Group-count variants of the quantizer (variants.hip).
+struct VariantInfo {
+    int32_t n_out, n_in, out_bits, rank_bits, coo_bits, coo_bytes, groups;   // groups == 0: unknown
+};
+VariantInfo variant_info(int variant);
+struct VariantArgs {
+    VariantInfo info;
+    const uint16_t* x;            // fp16 bits [n][H][d]
+    const float* thr8;            // [H][8]
+    uint8_t* nib;                 // [n][H][d/2]
+    uint8_t* coo;                 // [n][H][d * coo_bytes]
+    uint8_t* counts;              // [n][H][d/64]
+    uint16_t* meta;               // [n][H][2 * groups] fp16 bits
+    int32_t* n_coo;               // [n][H]
+    float* out;                   // [n][H][d] (dequantization)
+    int32_t n, H;
+};
+hipError_t launch_variant_quantize(const VariantArgs& a, int d, hipStream_t st);
+hipError_t launch_variant_dequantize(const VariantArgs& a, int d, hipStream_t st);
+
 // Matrix-core decode attention (head_dim 128; 1, 2 or 4 query heads per KV head).
 bool mfma_attention_supported(int d, int G);
 int mfma_score_cap();   // tokens per query head in one workgroup's page range
