@@ -45,6 +45,8 @@ def parse():
                     help="sequences in the layer step (0: the whole workload batch)")
     ap.add_argument("--ratio-sweep", action="store_true",
                     help="group-ratio trade-off: effective bits vs attention error for several (outer, inner) ratios")
+    ap.add_argument("--variants", action="store_true",
+                    help="number-of-groups study: effective bits and error of each encoding variant")
     ap.add_argument("--prefill-chunk", type=int, default=0,
                     help="time chunked-prefill attention for the last N cached tokens of every sequence")
     ap.add_argument("--cpu-sample-seqs", type=int, default=128)
@@ -193,6 +195,87 @@ def ratio_sweep(args):
                       "sweep": rows}), flush=True)
 
 
+def variant_sweep(args):
+    """Number-of-groups study (Sec. 6.2) on synthetic data: for each encoding variant,
+    calibrate its boundaries, encode and decode the keys and values, and report the
+    effective bits per element (from the stored bytes), the relative error of K and V,
+    the relative L2 error of fp32 attention over the decoded K/V against attention over
+    the unquantized values, and the encoder's throughput."""
+    import numpy as np
+    import torch
+
+    from paper_2503_18599_amd import binding as B
+    from paper_2503_18599_amd import synth
+
+    dev = "cuda"
+    w = synth.scaled(synth.WORKLOADS[args.workload], n_seqs=32, ctx=1024)
+    H, Hq, d, n = w.n_kv_heads, w.n_q_heads, w.head_dim, w.n_seqs
+    G = Hq // H
+    lens = synth.seq_lengths(w)
+    k = [synth.kv_values_seq(w, "k", s, int(lens[s]), dev) for s in range(n)]
+    v = [synth.kv_values_seq(w, "v", s, int(lens[s]), dev) for s in range(n)]
+    kk, vv = torch.cat(k).contiguous(), torch.cat(v).contiguous()
+    q = synth.queries(w, 0, dev)
+    scale = float(np.float32(1.0 / math.sqrt(d)))
+    cu = [0] + np.cumsum(lens.numpy()).tolist()
+
+    def attention(kx, vx):
+        out = []
+        for s in range(n):
+            ks, vs = kx[cu[s]:cu[s + 1]], vx[cu[s]:cu[s + 1]]
+            kt = ks.float().repeat_interleave(G, 1).permute(1, 2, 0).contiguous()   # [Hq][d][L]
+            vt = vs.float().repeat_interleave(G, 1).permute(1, 0, 2).contiguous()   # [Hq][L][d]
+            sc = torch.bmm(q[s].float()[:, None, :], kt)[:, 0, :] * scale
+            out.append(torch.bmm(torch.softmax(sc, -1)[:, None, :], vt)[:, 0, :])
+        return torch.stack(out)
+
+    ref = attention(kk, vv)
+    kc = synth.calibration_set(w, "k", dev)
+    vc = synth.calibration_set(w, "v", dev)
+    shares = {"g3": ((0.04, 0.06), None), "g2": ((0.10, 0.0), None), "g4": ((0.04, 0.06), (0.02, 0.06)),
+              "g5": ((0.04, 0.06), (0.02, 0.03)), "g4-o4": ((0.04, 0.06), (0.02, 0.06)),
+              "g5-o4": ((0.04, 0.06), (0.02, 0.03))}
+    rows = []
+    for name, vid in B.VARIANTS.items():
+        info = B.variant_info(vid)
+        full, lvl = shares[name]
+        ta = B.calibrate_thresholds(kc, vc, *full)
+        tb = B.calibrate_thresholds(kc, vc, *lvl) if lvl else None
+        dec, n_coo = [], 0
+        for which, x in ((0, kk), (1, vv)):
+            thr8 = B.variant_boundaries(vid, ta[:, which], None if tb is None else tb[:, which])
+            enc = B.variant_quantize(vid, x, thr8)
+            n_coo += int(enc["n_coo"].sum())
+            dec.append(B.variant_dequantize(vid, enc, thr8))
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        thr8 = B.variant_boundaries(vid, ta[:, 0], None if tb is None else tb[:, 0])
+        for _ in range(3):
+            B.variant_quantize(vid, kk, thr8)
+        e0.record()
+        for _ in range(10):
+            B.variant_quantize(vid, kk, thr8)
+        e1.record()
+        torch.cuda.synchronize()
+        t = e0.elapsed_time(e1) / 10 / 1e3
+        n_vec = kk.shape[0] * H * 2
+        n_el = n_vec * d
+        nbytes = n_vec * (d // 2 + 4 * info["groups"] + d // 64) + n_coo * info["coo_bytes"]
+        out = attention(dec[0], dec[1])
+        err = float(((out - ref).norm() / ref.norm()).item())
+        kerr = float(((dec[0] - kk.float()).norm() / kk.float().norm()).item())
+        verr = float(((dec[1] - vv.float()).norm() / vv.float().norm()).item())
+        rows.append({"variant": name, "groups": info["groups"], "coo_bits": info["coo_bits"],
+                     "outlier_bits": info["out_bits"] + 1, "outlier_fraction": round(n_coo / n_el, 4),
+                     "effective_bits": round(8.0 * nbytes / n_el, 3), "k_rel_err": round(kerr, 5),
+                     "v_rel_err": round(verr, 5), "attention_rel_err": round(err, 5),
+                     "encode_gbs": round(kk.numel() * 2 / t / 1e9, 1)})
+        log(f"{name}: {rows[-1]}")
+    print(json.dumps({"metric": "group-count variants (effective bits vs K/V and attention relative L2 error)",
+                      "config": {"workload": f"{w.name}: {n} sequences x {w.ctx} tokens, {Hq}/{H} heads, d {d}"},
+                      "data": "synthetic", "reference": "fp32 attention over the unquantized fp16 K/V",
+                      "variants": rows}), flush=True)
+
+
 def prefill_bench(args, w, cache, bt, lens, dev):
     """Chunked-prefill attention: the last C cached tokens of every sequence attend causally
     over their prefixes (each query token reads its own prefix; the query heads of a KV
@@ -244,6 +327,8 @@ def prefill_bench(args, w, cache, bt, lens, dev):
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.variants:
+        return variant_sweep(args)
     if args.ratio_sweep:
         return ratio_sweep(args)
     if args.gpus != 1 or world != 1:
