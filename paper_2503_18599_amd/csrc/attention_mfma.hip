@@ -43,11 +43,10 @@ constexpr int CB = 32;                     // COO count bytes at the start of a 
 constexpr int cmax(int x, int y) { return x > y ? x : y; }
 constexpr int GRP = 4;                     // pages per group (two correction pairs)
 constexpr int GT = GRP * P;                // tokens per group
-// LDS stride of a page's dense bytes.  With one query head the value pages are staged in
-// two token halves 576 bytes apart (a channel's dword of eight tokens at 4 * channel), so
-// that the halves and neighbouring pages fall on opposite bank halves.
-template <int G>
-constexpr int pstr() { return G == 1 ? 1088 : 1024; }
+// LDS stride of a page's dense bytes.  Value pages are staged in two token halves 576
+// bytes apart (a channel's dword of eight tokens at 4 * channel), so that the halves and
+// neighbouring pages fall on opposite bank halves.
+constexpr int PSTR = 1088;
 constexpr int VHALF = 576;
 constexpr int SPCAP = P * D;               // sparse capacity of one record
 constexpr int SSLOT = 448;                 // staged COO bytes per page (larger pages: read from HBM)
@@ -198,34 +197,28 @@ __device__ __forceinline__ uint4 ld16(const uint8_t* p) {
 // pass); tokc (key pass) shares with wv (value pass) and, after the value pass, with the
 // value corrections on their way to the output lanes.
 //
-// With one query head per KV head the correction walks take one token per lane, and the
-// table is token-major: row tg (64 bytes) holds the four classes at 16-byte slots rotated
-// by bits 1-2 of tg (so that lanes reading one class spread over the banks), each slot
-// the two nibble halves.  The key walk reads the query in fp16 (one byte of offset per
-// entry); in the value walk 4 * channel locates both the channel's dense dword and its
-// correction.
+// The correction walks take one token per lane, and the table is token-major: row tg (64
+// bytes) holds the four classes at 16-byte slots rotated by bits 1-2 of tg (so that lanes
+// reading one class spread over the banks), each slot the two nibble halves.  The key walk
+// reads the query heads of a channel in fp16; in the value walk 4 * channel locates both
+// the channel's dense dword and its correction.
 template <int G>
 struct Smem {
     __align__(16) uint8_t tab_[4 * GT * 2 * 8];   // correction table; qi
-    __align__(16) uint8_t dense[GRP][pstr<G>()];  // K: token rows of 64 bytes; V: channel rows of 8
-                                                  // (one head: two halves of channel dwords)
+    __align__(16) uint8_t dense[GRP][PSTR];       // K: token rows of 64 bytes; V: two halves of
+                                                  // channel dwords
     __align__(16) uint8_t qo_[G * D * 4];         // q (keys); oci (values)
     __align__(16) uint8_t tw_[cmax(cmax(GT * 16, G * GT * 8), G * D * 4)];
     float pbase[G];
     float m[G], l[G];
     __align__(16) uint8_t head[GRP][CB];          // COO counts of a group's records
-    int start[G == 1 ? 1 : GRP][P];               // offset of each slot's COO bytes in its page
     __align__(16) uint8_t sparse[SPL + 80];       // page p's COO bytes at p*SSLOT; + slack for
-                                                  // whole-dword reads past a bucket
+                                                  // whole-dword reads past a run
 
-    // correction table [COO class][token][nibble bit 3] (several heads)
-    __device__ float2 (&tab())[4][GT][2] { return *reinterpret_cast<float2 (*)[4][GT][2]>(tab_); }
     // query in fixed point (before the key pass)
     __device__ int (&qi())[G][D] { return *reinterpret_cast<int (*)[G][D]>(tab_); }
-    // query in fp32, the heads of a channel side by side (key pass, several heads)
-    __device__ float (&q())[D][G] { return *reinterpret_cast<float (*)[D][G]>(qo_); }
-    // query in fp16 (key pass, one head)
-    __device__ __half (&q16())[D] { return *reinterpret_cast<__half (*)[D]>(qo_); }
+    // query in fp16, the heads of a channel side by side (key pass)
+    __device__ __half (&q16())[D][G] { return *reinterpret_cast<__half (*)[D][G]>(qo_); }
     // value corrections of one group, fixed point (value pass)
     __device__ int& oci(int hd, int ch) { return reinterpret_cast<int*>(qo_)[hd * D + ch]; }
     // base, Delta, Gp of the group's tokens (key pass)
@@ -309,8 +302,8 @@ __device__ __forceinline__ Run unpack_run(uint32_t x) {
 }
 
 // Start of each slot's COO bytes in its page, from the group's counts in the head
-// buffer.  Returns the COO bytes used by the lane's page (lane >> 4) and whether every
-// page fits its staging slot; with one head, also the lane's own run.
+// buffer.  Returns the COO bytes used by the lane's page (lane >> 4), whether every page
+// fits its staging slot, and the lane's own run.
 template <int G>
 __device__ __forceinline__ int group_layout(Smem<G>& S, const Grp& gr, int lane, bool& fits, Run& run) {
     const int pg = lane >> 4, t = lane & 15;
@@ -319,14 +312,10 @@ __device__ __forceinline__ int group_layout(Smem<G>& S, const Grp& gr, int lane,
     const int c1 = (t < nv) ? (int)S.head[pg][2 * t + 1] : 0;
     const int tot = c0 + c1;
     const int incl = row_scan16(tot);
-    if constexpr (G == 1) {
-        // a 64-value chunk has at most 64 entries; larger counts are not a valid record
-        run.st = incl - tot;
-        run.c0 = min(c0, 64);
-        run.cnt = max(0, min(run.c0 + min(c1, 64), SPCAP - run.st));
-    } else {
-        S.start[pg][t] = incl - tot;
-    }
+    // a 64-value chunk has at most 64 entries; larger counts are not a valid record
+    run.st = incl - tot;
+    run.c0 = min(c0, 64);
+    run.cnt = max(0, min(run.c0 + min(c1, 64), SPCAP - run.st));
     const int u0 = __builtin_amdgcn_readlane(incl, 15), u1 = __builtin_amdgcn_readlane(incl, 31);
     const int u2 = __builtin_amdgcn_readlane(incl, 47), u3 = __builtin_amdgcn_readlane(incl, 63);
     fits = max(max(u0, u1), max(u2, u3)) <= SSLOT;
@@ -373,322 +362,35 @@ __device__ __forceinline__ uint32_t coo_byte(const AttnArgs& a, const Grp& gr, i
 
 // Writes the token's correction table: for COO class cls = COO >> 6 (bit 0 outer,
 // bit 1 upper side) and nibble n with high bit h, the true value minus the nibble's
-// middle reading is x + n*y with (x, y) = tab[cls][tg][h]: x = B_cls - base - h*Gp,
-// y = Delta_group - Delta_middle.  Everything is scaled by w.
+// middle reading is x + n*y with (x, y) the float2 at row tg, class slot cls ^ (bits 1-2
+// of tg), half h: x = B_cls - base - h*Gp, y = Delta_group - Delta_middle.  Everything is
+// scaled by w.
 template <int G>
 __device__ __forceinline__ void token_table(Smem<G>& S, int tg, const Tok& T, float w) {
     const float x[4] = {T.b_il - T.base, T.b_ol - T.base, T.b_ih - T.base, T.b_oh - T.base};
     const float y[4] = {T.kd_i, T.kd_o, T.kd_i, T.kd_o};
 #pragma unroll
     for (int cls = 0; cls < 4; ++cls) {
-        float4* row = G == 1 ? reinterpret_cast<float4*>(&S.tab_[tg * 64 + ((cls ^ ((tg >> 1) & 3)) << 4)])
-                             : reinterpret_cast<float4*>(&S.tab()[cls][tg][0]);
+        float4* row = reinterpret_cast<float4*>(&S.tab_[tg * 64 + ((cls ^ ((tg >> 1) & 3)) << 4)]);
         *row = make_float4(w * x[cls], w * y[cls], w * (x[cls] - T.gp), w * y[cls]);
     }
 }
-
-// Per-lane bucket of COO entries: lane = (page of the pair, 64-value chunk, token).
-struct Bucket {
-    int pg, c, t, tg, cnt, st;
-    bool vt;
-};
-
-template <int G>
-__device__ __forceinline__ Bucket bucket_of(Smem<G>& S, const Grp& gr, int pp, int lane) {
-    Bucket k;
-    k.c = (lane >> 4) & 1;
-    k.t = lane & 15;
-    k.pg = pp + (lane >> 5);
-    k.tg = k.pg * P + k.t;
-    const int nv = pick4(k.pg, gr.nval[0], gr.nval[1], gr.nval[2], gr.nval[3]);
-    k.vt = k.t < nv;
-    const int c0 = k.vt ? (int)S.head[k.pg][2 * k.t] : 0;
-    const int c1 = k.vt ? (int)S.head[k.pg][2 * k.t + 1] : 0;
-    k.st = k.vt ? S.start[k.pg][k.t] + (k.c ? c0 : 0) : 0;
-    // a 64-value chunk has at most 64 entries; larger counts are not a valid record
-    k.cnt = max(0, min(min(k.c ? c1 : c0, 64), SPCAP - k.st));
-    return k;
-}
-
-// x >> s for s >= 0, x << -s otherwise (s is a compile-time constant after unrolling).
-__device__ __forceinline__ uint32_t shr(uint32_t x, int s) { return s >= 0 ? x >> s : x << -s; }
 
 template <typename T, int G>
 __device__ __forceinline__ const T& lds_at(const Smem<G>& S, uint32_t off) {
     return *reinterpret_cast<const T*>(reinterpret_cast<const char*>(&S) + off);
 }
 
-// Correction of the COO entry held in bits o..o+7 of ent, whose nibble is n; tbo is
-// the LDS offset of the token's table row tab[0][tg][0].
-template <int G>
-__device__ __forceinline__ float entry_delta(Smem<G>& S, uint32_t tbo, uint32_t ent, int o, uint32_t n) {
-    const uint32_t ta = (tbo | (shr(ent, o - 4) & 0xc00u)) | (n & 8u);
-    const float2 kv = *reinterpret_cast<const float2*>(reinterpret_cast<const char*>(&S) + ta);
-    return fmaf((float)n, kv.y, kv.x);
-}
-
 static_assert(offsetof(Smem<1>, dense) == 4096 && offsetof(Smem<1>, qo_) % 256 == 0 &&
-              offsetof(Smem<2>, qo_) == 8192 && offsetof(Smem<4>, qo_) == 8192 &&
-              sizeof(Smem<1>::tab_) >= sizeof(int) * 4 * D, "LDS layout the correction addressing relies on");
+              offsetof(Smem<2>, qo_) % 256 == 0 && offsetof(Smem<4>, qo_) % 256 == 0 &&
+              sizeof(Smem<4>::tab_) >= sizeof(int) * 4 * D, "LDS layout the correction addressing relies on");
 
 template <int G>
 __device__ __forceinline__ uint32_t off_of(const Smem<G>& S, const void* p) {
     return (uint32_t)(reinterpret_cast<const char*>(p) - reinterpret_cast<const char*>(&S));
 }
 
-// Walks each lane's buckets and adds every entry's q-weighted correction (true value
-// minus middle reading) to its token's score.  A lane owns NB buckets, one in each of
-// the page pairs 0, 2, ..., walked side by side so that their LDS loads overlap.
-// Staged entries are read four at a time from one aligned dword pair, one block ahead of
-// their use; the corrections of a block are independent, and entries past a bucket
-// contribute zero.
-template <int G, bool STAGED, int NB, bool PG>
-__device__ __forceinline__ void key_corrections(Smem<G>& S, const AttnArgs& a, float* sc, int cap, float scale,
-                                                const Bucket (&kb)[NB], const Grp& gr, int tok0, int lane) {
-    Bucket k[NB];
-    uint32_t tbo[NB], drow[NB];
-    float corr[NB][G];
-    int mc = 0;
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-        k[nb] = kb[nb];
-        tbo[nb] = off_of(S, &S.tab()[0][k[nb].tg][0]);
-        drow[nb] = off_of(S, &S.dense[k[nb].pg][k[nb].t * 64 + k[nb].c * 32]);
-        mc = max(mc, k[nb].cnt);
-#pragma unroll
-        for (int hd = 0; hd < G; ++hd) corr[nb][hd] = 0.0f;
-    }
-    const uint32_t qc = off_of(S, &S.q()[((lane >> 4) & 1) * 64][0]);
-    constexpr int LG = G == 1 ? 0 : G == 2 ? 1 : 2;   // log2 G: one channel's heads span 4G bytes
-    const int maxc = wave_max_i(mc);
-    // The entry in bits o..o+7 of ent: index j (6 bits), class (2 bits).  Every slot is
-    // computed; slots past the bucket get a zero weight (no branches).
-    auto slot = [&](int nb, uint32_t ent, int o, bool valid) {
-        const uint32_t dw = lds_at<uint32_t>(S, drow[nb] | (shr(ent, o + 1) & 0x1cu));
-        const uint32_t n = __builtin_amdgcn_ubfe(dw, ((ent >> o) & 0xffu) << 2, 4);
-        const float delta = entry_delta(S, tbo[nb], ent, o, n);
-        const uint32_t qo = qc | (shr(ent, o - 2 - LG) & (0xfcu << LG));
-#pragma unroll
-        for (int hd = 0; hd < G; ++hd) {
-            const float q = lds_at<float>(S, qo + hd * 4);
-            corr[nb][hd] = fmaf(valid ? q : 0.0f, delta, corr[nb][hd]);
-        }
-    };
-    if (STAGED) {
-        const uint32_t* w[NB];
-        uint32_t sh[NB], cur[NB], nxt[NB], ent[NB];
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-            const int pos = k[nb].pg * SSLOT + k[nb].st;
-            w[nb] = reinterpret_cast<const uint32_t*>(&S.sparse[pos & ~3]);
-            sh[nb] = pos & 3;
-            cur[nb] = w[nb][0];
-            nxt[nb] = w[nb][1];
-        }
-        const int full = maxc & ~3;
-        for (int kk = 0; kk < full; kk += 4) {
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb) {
-                ent[nb] = __builtin_amdgcn_alignbyte(nxt[nb], cur[nb], sh[nb]);
-                cur[nb] = nxt[nb];
-                nxt[nb] = w[nb][(kk >> 2) + 2];
-            }
-            // three phases, kept apart so that a block's reads issue together: the nibble
-            // dwords and queries, then the table rows, then the accumulation
-            uint32_t dw[NB][4];
-            float qv[NB][4][G];
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int o = 8 * i;
-                    dw[nb][i] = lds_at<uint32_t>(S, drow[nb] | (shr(ent[nb], o + 1) & 0x1cu));
-                    const uint32_t qo = qc | (shr(ent[nb], o - 2 - LG) & (0xfcu << LG));
-                    if constexpr (G == 4) {
-                        const float4 v4 = lds_at<float4>(S, qo);
-                        qv[nb][i][0] = v4.x;
-                        qv[nb][i][G > 1 ? 1 : 0] = v4.y;
-                        qv[nb][i][G > 2 ? 2 : 0] = v4.z;
-                        qv[nb][i][G > 3 ? 3 : 0] = v4.w;
-                    } else {
-#pragma unroll
-                        for (int hd = 0; hd < G; ++hd) qv[nb][i][hd] = lds_at<float>(S, qo + hd * 4);
-                    }
-                }
-            __builtin_amdgcn_sched_barrier(0);
-            float2 kv[NB][4];
-            uint32_t nn[NB][4];
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int o = 8 * i;
-                    nn[nb][i] = __builtin_amdgcn_ubfe(dw[nb][i], ((ent[nb] >> o) & 0xffu) << 2, 4);
-                    const uint32_t ta = (tbo[nb] | (shr(ent[nb], o - 4) & 0xc00u)) | (nn[nb][i] & 8u);
-                    kv[nb][i] = lds_at<float2>(S, ta);
-                }
-            __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const float delta = fmaf((float)nn[nb][i], kv[nb][i].y, kv[nb][i].x);
-                    const bool valid = kk + i < k[nb].cnt;
-#pragma unroll
-                    for (int hd = 0; hd < G; ++hd)
-                        corr[nb][hd] = fmaf(valid ? qv[nb][i][hd] : 0.0f, delta, corr[nb][hd]);
-                }
-        }
-        // the last 1-3 slots (the wave's longest bucket decides how many)
-        const int rem = maxc - full;
-        if (rem > 0) {
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb) {
-                ent[nb] = __builtin_amdgcn_alignbyte(nxt[nb], cur[nb], sh[nb]);
-                slot(nb, ent[nb], 0, full < k[nb].cnt);
-            }
-            if (rem > 1)
-#pragma unroll
-                for (int nb = 0; nb < NB; ++nb) slot(nb, ent[nb], 8, full + 1 < k[nb].cnt);
-            if (rem > 2)
-#pragma unroll
-                for (int nb = 0; nb < NB; ++nb) slot(nb, ent[nb], 16, full + 2 < k[nb].cnt);
-        }
-    } else {
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-            // (a bucket of an absent page is empty)
-            if constexpr (PG) {
-                for (int kk = 0; kk < maxc; ++kk)
-                    if (kk < k[nb].cnt) slot(nb, coo_byte<PG>(a, gr, k[nb].pg, k[nb].st + kk), 0, true);
-            } else {
-                const uint8_t* spp = pick4(k[nb].pg, gr.base[0], gr.base[1], gr.base[2], gr.base[3]) + LY.sparse + k[nb].st;
-                for (int kk = 0; kk < maxc; ++kk)
-                    if (kk < k[nb].cnt) slot(nb, spp[kk], 0, true);
-            }
-        }
-    }
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-        for (int hd = 0; hd < G; ++hd) {
-            const float o = corr[nb][hd] + __shfl_xor(corr[nb][hd], 16, 64);
-            if (k[nb].c == 0 && k[nb].vt) sc[hd * cap + tok0 + k[nb].tg] += scale * o;
-        }
-}
-
-// Same walk for values: each entry adds p_t * (true value - middle reading) to its
-// channel.  With one head the probability is already folded into the table and Gp.
-template <int G, bool STAGED, int NB, bool PG>
-__device__ __forceinline__ void value_corrections(Smem<G>& S, const AttnArgs& a, const float* sc, int cap,
-                                                  const Bucket (&kb)[NB], const Grp& gr, int tok0, int lane) {
-    Bucket k[NB];
-    uint32_t tbo[NB], dcol[NB];
-    float pt[NB][G];
-    int mc = 0;
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-        k[nb] = kb[nb];
-        tbo[nb] = off_of(S, &S.tab()[0][k[nb].tg][0]);
-        dcol[nb] = off_of(S, &S.dense[k[nb].pg][(k[nb].t >> 3) * 4 + k[nb].c * 512]);
-        mc = max(mc, k[nb].cnt);
-#pragma unroll
-        for (int hd = 0; hd < G; ++hd)
-            pt[nb][hd] = (G > 1 && k[nb].vt) ? sc[hd * cap + tok0 + k[nb].tg] : 1.0f;
-    }
-    const uint32_t nsh = (lane & 7) * 4;
-    const uint32_t occ = off_of(S, &S.oci(0, ((lane >> 4) & 1) * 64));
-    const int maxc = wave_max_i(mc);
-    // Every slot is computed and added; slots past the bucket add zero (no branches).
-    // The loads of a block's slots come first, then its LDS additions, so that the
-    // additions do not serialise the loads behind them.
-    struct Upd {
-        uint32_t addr;
-        int v[G];
-    };
-    auto slot = [&](int nb, uint32_t ent, int o, bool valid) {
-        const uint32_t dw = lds_at<uint32_t>(S, dcol[nb] | (shr(ent, o - 3) & 0x1f8u));
-        const uint32_t n = __builtin_amdgcn_ubfe(dw, nsh, 4);
-        const float delta = entry_delta(S, tbo[nb], ent, o, n);
-        Upd u;
-        u.addr = occ | (shr(ent, o - 2) & 0xfcu);
-#pragma unroll
-        for (int hd = 0; hd < G; ++hd) {
-            const int v = (int)(G == 1 ? delta : pt[nb][hd] * delta);
-            u.v[hd] = valid ? v : 0;
-        }
-        return u;
-    };
-    auto apply = [&](const Upd& u) {
-#pragma unroll
-        for (int hd = 0; hd < G; ++hd) atomicAdd(&const_cast<int&>(lds_at<int>(S, u.addr + hd * D * 4)), u.v[hd]);
-    };
-    if (STAGED) {
-        const uint32_t* w[NB];
-        uint32_t sh[NB], cur[NB], nxt[NB], ent[NB];
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-            const int pos = k[nb].pg * SSLOT + k[nb].st;
-            w[nb] = reinterpret_cast<const uint32_t*>(&S.sparse[pos & ~3]);
-            sh[nb] = pos & 3;
-            cur[nb] = w[nb][0];
-            nxt[nb] = w[nb][1];
-        }
-        const int full = maxc & ~3;
-        for (int kk = 0; kk < full; kk += 4) {
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb) {
-                ent[nb] = __builtin_amdgcn_alignbyte(nxt[nb], cur[nb], sh[nb]);
-                cur[nb] = nxt[nb];
-                nxt[nb] = w[nb][(kk >> 2) + 2];
-            }
-            Upd u[NB][4];
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) u[nb][i] = slot(nb, ent[nb], 8 * i, kk + i < k[nb].cnt);
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) apply(u[nb][i]);
-        }
-        // the last 1-3 slots (the wave's longest bucket decides how many)
-        const int rem = maxc - full;
-        if (rem > 0) {
-            Upd u[NB][3];
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb) {
-                ent[nb] = __builtin_amdgcn_alignbyte(nxt[nb], cur[nb], sh[nb]);
-                u[nb][0] = slot(nb, ent[nb], 0, full < k[nb].cnt);
-                u[nb][1] = u[nb][0];
-                u[nb][2] = u[nb][0];
-                if (rem > 1) u[nb][1] = slot(nb, ent[nb], 8, full + 1 < k[nb].cnt);
-                if (rem > 2) u[nb][2] = slot(nb, ent[nb], 16, full + 2 < k[nb].cnt);
-            }
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb) {
-                apply(u[nb][0]);
-                if (rem > 1) apply(u[nb][1]);
-                if (rem > 2) apply(u[nb][2]);
-            }
-        }
-    } else {
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-            // (a bucket of an absent page is empty)
-            if constexpr (PG) {
-                for (int kk = 0; kk < maxc; ++kk)
-                    if (kk < k[nb].cnt) apply(slot(nb, coo_byte<PG>(a, gr, k[nb].pg, k[nb].st + kk), 0, true));
-            } else {
-                const uint8_t* spp = pick4(k[nb].pg, gr.base[0], gr.base[1], gr.base[2], gr.base[3]) + LY.sparse + k[nb].st;
-                for (int kk = 0; kk < maxc; ++kk)
-                    if (kk < k[nb].cnt) apply(slot(nb, spp[kk], 0, true));
-            }
-        }
-    }
-}
-
-// ---- one query head per KV head: one token per lane -----------------------------------
+// ---- correction walks: one token per lane --------------------------------------------
 //
 // Lane 16*page + slot walks every COO entry of its token, both chunks, as one run of the
 // staged stream.  The entries of a dword are decoded together, one byte per entry:
@@ -730,24 +432,49 @@ __device__ __forceinline__ uint32_t shl_byte(uint32_t x, uint32_t sh, int i) {
 }
 #undef OAKEN_SDWA_SHL
 
-// Scores: each entry adds q_j * (true value - middle reading) to its token's score.
-template <bool PG>
-__device__ __forceinline__ void key_corrections_g1(Smem<1>& S, const AttnArgs& a, float* sc, float scale,
-                                                   const Run& r, bool staged, const Grp& gr, int tok0, int lane) {
+// Query-head count as a shift (G = 1, 2, 4).
+template <int G>
+constexpr int log2g() { return G == 1 ? 0 : G == 2 ? 1 : 2; }
+
+// One fp16 query head of a channel's heads (loaded together) into a float.
+template <int G>
+__device__ __forceinline__ float q_head(const uint2& qv, int hd) {
+    const uint32_t w = hd < 2 ? qv.x : qv.y;
+    return __half2float(__ushort_as_half((uint16_t)((hd & 1) ? (w >> 16) : (w & 0xffffu))));
+}
+
+// The G fp16 query heads of the channel at byte offset qa (G * 2 bytes).
+template <int G>
+__device__ __forceinline__ uint2 q_heads(const Smem<G>& S, uint32_t qa) {
+    if constexpr (G == 4) return lds_at<uint2>(S, qa);
+    else if constexpr (G == 2) return make_uint2(lds_at<uint32_t>(S, qa), 0u);
+    else return make_uint2((uint32_t)lds_at<uint16_t>(S, qa), 0u);
+}
+
+// Scores: each entry adds q_j * (true value - middle reading) to its token's score, for
+// each of the G query heads.
+template <int G, bool PG>
+__device__ __forceinline__ void key_corrections(Smem<G>& S, const AttnArgs& a, float* sc, int cap, float scale,
+                                                const Run& r, bool staged, const Grp& gr, int tok0, int lane) {
+    constexpr int QS = 1 + log2g<G>();                            // log2 of the query bytes per channel
     const int pg = lane >> 4, t = lane & 15;
     const uint32_t tbo = (uint32_t)lane * 64u;                    // the token's table row
     const uint32_t swz = (uint32_t)((lane >> 1) & 3) * 0x10101010u;
-    const uint32_t qb = off_of(S, &S.q16()[0]);                   // 256-aligned
+    const uint32_t qb = off_of(S, &S.q16()[0][0]);                // 256-aligned
     const uint32_t drow = off_of(S, &S.dense[pg][t * 64]);        // 64-aligned
-    float corr = 0.0f;
-    // one entry: query offset byte qo (channel * 2), dense offset byte dof (dword of the
+    float corr[G];
+#pragma unroll
+    for (int hd = 0; hd < G; ++hd) corr[hd] = 0.0f;
+    // one entry: query offset qo (channel << QS), dense offset byte dof (dword of the
     // channel within the token row), nibble shift ns, table slot byte ct
     auto entry = [&](uint32_t qo, uint32_t dof, uint32_t ns, uint32_t ct) {
         const uint32_t dw = lds_at<uint32_t>(S, drow | dof);
-        const float q = __half2float(lds_at<__half>(S, qb | qo));
+        const uint2 qv = q_heads<G>(S, qb + qo);
         const uint32_t n = __builtin_amdgcn_ubfe(dw, ns, 4);
         const float2 kv = lds_at<float2>(S, (tbo | ct) | (n & 8u));
-        corr = fmaf(q, fmaf((float)n, kv.y, kv.x), corr);
+        const float delta = fmaf((float)n, kv.y, kv.x);
+#pragma unroll
+        for (int hd = 0; hd < G; ++hd) corr[hd] = fmaf(q_head<G>(qv, hd), delta, corr[hd]);
     };
     if (staged) {
         const int pos = pg * SSLOT + r.st;
@@ -755,75 +482,92 @@ __device__ __forceinline__ void key_corrections_g1(Smem<1>& S, const AttnArgs& a
         const uint32_t sh = pos & 3;
         uint32_t cur = w[0], nxt = w[1];
         const uint32_t pc0 = 0x03020100u + (uint32_t)(128 - r.c0) * 0x01010101u;
-        auto decode = [&](int kk, uint32_t& qo4, uint32_t& do4, uint32_t& ns4, uint32_t& ct4) {
-            const uint32_t ent = __builtin_amdgcn_alignbyte(nxt, cur, sh);
+        // per dword: channels (7 bits, chunk on top), dense offsets, raw entries (nibble
+        // shifts), table slots
+        auto decode = [&](int kk, uint32_t& ch4, uint32_t& do4, uint32_t& ent, uint32_t& ct4) {
+            ent = __builtin_amdgcn_alignbyte(nxt, cur, sh);
             const uint32_t chk = (pc0 + (uint32_t)kk * 0x01010101u) & 0x80808080u;
-            qo4 = ((ent << 1) & 0x7e7e7e7eu) | chk;       // channel * 2
-            do4 = (qo4 >> 2) & 0x3c3c3c3cu;               // (channel / 8) * 4
-            ns4 = ent;                                    // nibble shift: (byte << 2) mod 32
+            ch4 = (ent & 0x3f3f3f3fu) | (chk >> 1);                 // channel
+            do4 = (ch4 >> 1) & 0x3c3c3c3cu;                         // (channel / 8) * 4
             ct4 = ((ent >> 2) & 0x30303030u) ^ swz;
         };
         const int full = r.cnt & ~3;
         for (int kk = 0; kk < full; kk += 4) {
-            uint32_t qo4, do4, ns4, ct4;
-            decode(kk, qo4, do4, ns4, ct4);
+            uint32_t ch4, do4, ent, ct4;
+            decode(kk, ch4, do4, ent, ct4);
             cur = nxt;
             nxt = w[(kk >> 2) + 2];
             // phases kept apart so that a dword's reads issue together
             uint32_t dw[4];
-            float q[4];
+            uint2 qv[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 dw[i] = lds_at<uint32_t>(S, or_byte(do4, drow, i));
-                q[i] = __half2float(lds_at<__half>(S, qb | byte_at(qo4, i)));
+                qv[i] = q_heads<G>(S, qb + shl_byte(ch4, (uint32_t)QS, i));
             }
             __builtin_amdgcn_sched_barrier(0);
             uint32_t n[4];
             float2 kv[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                n[i] = __builtin_amdgcn_ubfe(dw[i], shl_byte(ns4, 2u, i), 4);
+                n[i] = __builtin_amdgcn_ubfe(dw[i], shl_byte(ent, 2u, i), 4);
                 kv[i] = lds_at<float2>(S, or_byte(ct4, tbo, i) | (n[i] & 8u));
             }
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-            for (int i = 0; i < 4; ++i) corr = fmaf(q[i], fmaf((float)n[i], kv[i].y, kv[i].x), corr);
+            for (int i = 0; i < 4; ++i) {
+                const float delta = fmaf((float)n[i], kv[i].y, kv[i].x);
+#pragma unroll
+                for (int hd = 0; hd < G; ++hd) corr[hd] = fmaf(q_head<G>(qv[i], hd), delta, corr[hd]);
+            }
         }
         if (full < r.cnt) {
-            uint32_t qo4, do4, ns4, ct4;
-            decode(full, qo4, do4, ns4, ct4);
-            entry(byte_at(qo4, 0), byte_at(do4, 0), byte_at(ns4, 0) << 2, byte_at(ct4, 0));
-            if (full + 1 < r.cnt) entry(byte_at(qo4, 1), byte_at(do4, 1), byte_at(ns4, 1) << 2, byte_at(ct4, 1));
-            if (full + 2 < r.cnt) entry(byte_at(qo4, 2), byte_at(do4, 2), byte_at(ns4, 2) << 2, byte_at(ct4, 2));
+            uint32_t ch4, do4, ent, ct4;
+            decode(full, ch4, do4, ent, ct4);
+            entry(byte_at(ch4, 0) << QS, byte_at(do4, 0), byte_at(ent, 0) << 2, byte_at(ct4, 0));
+            if (full + 1 < r.cnt) entry(byte_at(ch4, 1) << QS, byte_at(do4, 1), byte_at(ent, 1) << 2, byte_at(ct4, 1));
+            if (full + 2 < r.cnt) entry(byte_at(ch4, 2) << QS, byte_at(do4, 2), byte_at(ent, 2) << 2, byte_at(ct4, 2));
         }
     } else {
         for (int kk = 0; kk < r.cnt; ++kk) {
             const uint32_t b = coo_byte<PG>(a, gr, pg, r.st + kk);
             const uint32_t ch = (b & 63u) | (kk >= r.c0 ? 64u : 0u);
-            entry(ch * 2u, (ch >> 3) * 4u, (ch & 7u) * 4u, ((b >> 2) & 0x30u) ^ (swz & 0xffu));
+            entry(ch << QS, (ch >> 3) * 4u, (ch & 7u) * 4u, ((b >> 2) & 0x30u) ^ (swz & 0xffu));
         }
     }
     const int nv = pick4(pg, gr.nval[0], gr.nval[1], gr.nval[2], gr.nval[3]);
-    if (t < nv) sc[tok0 + lane] += scale * corr;
+    if (t < nv) {
+#pragma unroll
+        for (int hd = 0; hd < G; ++hd) sc[hd * cap + tok0 + lane] += scale * corr[hd];
+    }
 }
 
-// Values: each entry adds p_t * (true value - middle reading) to its channel, through the
-// table that already carries p_t and the group's fixed-point scale.
-template <bool PG>
-__device__ __forceinline__ void value_corrections_g1(Smem<1>& S, const AttnArgs& a, const Run& r, bool staged,
-                                                     const Grp& gr, int lane) {
+// Values: each entry adds p_t * (true value - middle reading) to its channel, once per
+// query head, in the group's fixed point.  With one head the table already carries p_t.
+template <int G, bool PG>
+__device__ __forceinline__ void value_corrections(Smem<G>& S, const AttnArgs& a, const float* sc, int cap,
+                                                  const Run& r, bool staged, const Grp& gr, int tok0, int lane) {
     const int pg = lane >> 4, t = lane & 15;
     const uint32_t tbo = (uint32_t)lane * 64u;
     const uint32_t swz = (uint32_t)((lane >> 1) & 3) * 0x10101010u;
     const uint32_t dcol = off_of(S, &S.dense[pg][(t >> 3) * VHALF]);  // + 4 * channel
     const uint32_t nsh = (uint32_t)(t & 7) * 4u;
-    const uint32_t occ = off_of(S, &S.oci(0, 0));                     // + 4 * channel
+    const uint32_t occ = off_of(S, &S.oci(0, 0));                     // + 4 * channel (+ 4 D * head)
+    float pt[G];
+    const int nv = pick4(pg, gr.nval[0], gr.nval[1], gr.nval[2], gr.nval[3]);
+#pragma unroll
+    for (int hd = 0; hd < G; ++hd) pt[hd] = (G > 1 && t < nv) ? sc[hd * cap + tok0 + lane] : 1.0f;
+    auto add = [&](uint32_t x, float delta) {
+#pragma unroll
+        for (int hd = 0; hd < G; ++hd)
+            atomicAdd(&const_cast<int&>(lds_at<int>(S, occ + x + hd * D * 4)), (int)(G == 1 ? delta : pt[hd] * delta));
+    };
     // one entry: channel offset x = 4 * channel, table slot byte ct
     auto entry = [&](uint32_t x, uint32_t ct) {
         const uint32_t dw = lds_at<uint32_t>(S, dcol + x);
         const uint32_t n = __builtin_amdgcn_ubfe(dw, nsh, 4);
         const float2 kv = lds_at<float2>(S, (tbo | ct) | (n & 8u));
-        atomicAdd(&const_cast<int&>(lds_at<int>(S, occ + x)), (int)fmaf((float)n, kv.y, kv.x));
+        add(x, fmaf((float)n, kv.y, kv.x));
     };
     if (staged) {
         const int pos = pg * SSLOT + r.st;
@@ -859,8 +603,7 @@ __device__ __forceinline__ void value_corrections_g1(Smem<1>& S, const AttnArgs&
             }
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-                atomicAdd(&const_cast<int&>(lds_at<int>(S, occ + x[i])), (int)fmaf((float)n[i], kv[i].y, kv[i].x));
+            for (int i = 0; i < 4; ++i) add(x[i], fmaf((float)n[i], kv[i].y, kv[i].x));
         }
         if (full < r.cnt) {
             uint32_t ch4, ct4;
@@ -922,13 +665,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
     for (int hd = 0; hd < G; ++hd) {
         const uint16_t* qp = a.q + ((int64_t)s * a.Hq + h * G + hd) * D;
         const float x0 = h2f(qp[lane]), x1 = h2f(qp[lane + 64]);
-        if constexpr (G == 1) {
-            S.q16()[lane] = __ushort_as_half(qp[lane]);
-            S.q16()[lane + 64] = __ushort_as_half(qp[lane + 64]);
-        } else {
-            S.q()[lane][hd] = x0;
-            S.q()[lane + 64][hd] = x1;
-        }
+        S.q16()[lane][hd] = __ushort_as_half(qp[lane]);
+        S.q16()[lane + 64][hd] = __ushort_as_half(qp[lane + 64]);
         const float mx = wave_max_nonneg(fmaxf(fabsf(x0), fabsf(x1)));
         const float sum = wave_sum(x0 + x1);
         const int sh = fix_shift(mx);
@@ -1058,12 +796,6 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
             *reinterpret_cast<uint4*>(&S.sparse[stg]) = sreg0;
             if (stg1_in) *reinterpret_cast<uint4*>(&S.sparse[stg + 256]) = sreg1;
         }
-        // the walk's buckets leave the head buffer before the next group's heads replace it
-        Bucket kb[GRP / 2];
-        if constexpr (G > 1) {
-#pragma unroll
-            for (int nb = 0; nb < GRP / 2; ++nb) kb[nb] = bucket_of(S, gc, 2 * nb, lane);
-        }
         wave_sync();
         // next group: heads -> layout -> issue its sparse bytes and the heads after it
         Grp gnn = gn;
@@ -1085,12 +817,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         }
         wave_sync();
         // sparse part
-        if constexpr (G == 1)
-            key_corrections_g1<PG>(S, a, sc, a.scale, unpack_run(run_c), staged, gc, tok0, lane);
-        else if (staged)
-            key_corrections<G, true, GRP / 2, PG>(S, a, sc, cap, a.scale, kb, gc, tok0, lane);
-        else
-            key_corrections<G, false, GRP / 2, PG>(S, a, sc, cap, a.scale, kb, gc, tok0, lane);
+        key_corrections<G, PG>(S, a, sc, cap, a.scale, unpack_run(run_c), staged, gc, tok0, lane);
         wave_sync();
         gc = gn;
         gn = gnn;
@@ -1154,13 +881,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         const bool staged = fits_c;
 #pragma unroll
         for (int pg = 0; pg < GRP; ++pg) {
-            if constexpr (G == 1) {
-                // channels 2*lane and 2*lane+1: tokens 0-7 to the first half, 8-15 to the second
-                *reinterpret_cast<uint2*>(&S.dense[pg][lane * 8]) = make_uint2(dreg[pg].x, dreg[pg].z);
-                *reinterpret_cast<uint2*>(&S.dense[pg][VHALF + lane * 8]) = make_uint2(dreg[pg].y, dreg[pg].w);
-            } else {
-                *reinterpret_cast<uint4*>(&S.dense[pg][lane * 16]) = dreg[pg];
-            }
+            // channels 2*lane and 2*lane+1: tokens 0-7 to the first half, 8-15 to the second
+            *reinterpret_cast<uint2*>(&S.dense[pg][lane * 8]) = make_uint2(dreg[pg].x, dreg[pg].z);
+            *reinterpret_cast<uint2*>(&S.dense[pg][VHALF + lane * 8]) = make_uint2(dreg[pg].y, dreg[pg].w);
         }
         // the next group's dense bytes go out as soon as these are staged
 #pragma unroll
@@ -1214,12 +937,6 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
             const float ws = ldexpf(w, fsh);
             token_table(S, lane, T, ws);
         }
-        // the walk's buckets leave the head buffer before the next group's heads replace it
-        Bucket kb[GRP / 2];
-        if constexpr (G > 1) {
-#pragma unroll
-            for (int nb = 0; nb < GRP / 2; ++nb) kb[nb] = bucket_of(S, gc, 2 * nb, lane);
-        }
         wave_sync();
         // next group: heads -> layout -> issue its sparse bytes and the heads after it
         Grp gnn = gn;
@@ -1264,11 +981,11 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
                     av[2] = col(w0.z, w1.z, w2.z, w3.z);
                     av[3] = col(w0.w, w1.w, w2.w, w3.w);
                 }
-                const uint8_t* dsrc = &S.dense[pp + (g4 >> 1)][(g4 & 1) * (G == 1 ? VHALF : 4)];
+                const uint8_t* dsrc = &S.dense[pp + (g4 >> 1)][(g4 & 1) * VHALF];
 #pragma unroll
                 for (int nt = 0; nt < 8; ++nt) {
                     const int j = nt * 16 + (lane & 15);
-                    const uint32_t dw = *reinterpret_cast<const uint32_t*>(dsrc + j * (G == 1 ? 4 : 8));
+                    const uint32_t dw = *reinterpret_cast<const uint32_t*>(dsrc + j * 4);
                     gacc[nt] = mfma(av, features(dw), gacc[nt]);
                 }
             }
@@ -1280,12 +997,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
 #pragma unroll
             for (int nt = 0; nt < 8; ++nt) oacc[nt] += ldexpf(limbs(gacc[nt]), -e);
         }
-        if constexpr (G == 1)
-            value_corrections_g1<PG>(S, a, unpack_run(run_c), staged, gc, lane);
-        else if (staged)
-            value_corrections<G, true, GRP / 2, PG>(S, a, sc, cap, kb, gc, tok0, lane);
-        else
-            value_corrections<G, false, GRP / 2, PG>(S, a, sc, cap, kb, gc, tok0, lane);
+        value_corrections<G, PG>(S, a, sc, cap, unpack_run(run_c), staged, gc, tok0, lane);
         wave_sync();
         // fold the group's integer sums into the fp32 outputs
 #pragma unroll
