@@ -95,7 +95,8 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
     __shared__ float s_acc[TQ][kMaxG][D];
     __shared__ float s_tmp[kThreads / 64];
 
-    const int split = blockIdx.x, h = blockIdx.y, s = blockIdx.z;
+    const AttnTile tile = attn_tile(a);
+    const int split = tile.split, h = tile.h, s = tile.s;
     const int G = a.Hq / a.H;
     const int tid = threadIdx.x;
     // row s: a sequence (decode), or a query token of a prefill chunk
@@ -269,7 +270,8 @@ hipError_t launch_attention(const AttnArgs& a, int d, hipStream_t st) {
     const int G = a.Hq / a.H;
     if (G > kMaxG) return hipErrorInvalidValue;
     const size_t shm = (size_t)G * a.pages_per_split * kPage * sizeof(float);
-    dim3 grid(a.n_splits, a.H, a.n_seqs);
+    const uint32_t grid = attn_grid(a);
+    if (grid == 0) return hipErrorInvalidValue;
     if (mfma_attention_supported(d, G)) {
         hipError_t e = launch_attention_mfma(a, st);
         if (e != hipSuccess || a.n_splits == 1) return e;
@@ -277,9 +279,9 @@ hipError_t launch_attention(const AttnArgs& a, int d, hipStream_t st) {
         return hipGetLastError();
     }
     if (d == 64) {
-        hipLaunchKernelGGL(attn_split_kernel<64>, grid, dim3(kThreads), shm, st, a);
+        hipLaunchKernelGGL(attn_split_kernel<64>, dim3(grid), dim3(kThreads), shm, st, a);
     } else if (d == 128) {
-        hipLaunchKernelGGL(attn_split_kernel<128>, grid, dim3(kThreads), shm, st, a);
+        hipLaunchKernelGGL(attn_split_kernel<128>, dim3(grid), dim3(kThreads), shm, st, a);
     } else {
         return hipErrorInvalidValue;
     }

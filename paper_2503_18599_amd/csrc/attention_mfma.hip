@@ -628,7 +628,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
     extern __shared__ float sc[];           // [G][cap]: scores, then probabilities
 
     const int lane = threadIdx.x;
-    const int split = blockIdx.x, h = blockIdx.y, s = blockIdx.z;
+    const AttnTile tile = attn_tile(a);
+    const int split = tile.split, h = tile.h, s = tile.s;
     // row s: a sequence (decode), or a query token of a prefill chunk, which sees its
     // sequence's keys up to its own position
     const int srow = a.tok_seq ? a.tok_seq[s] : s;
@@ -641,6 +642,16 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
     const int p_end = min(n_pages, p_begin + a.pages_per_split);
     const int cap = a.pages_per_split * P;
     const int n_tok = max(0, min(L, p_end * P) - p_begin * P);
+    // a range past the end of a shorter sequence of the batch: an empty partial (l = 0,
+    // which the combine skips) and nothing else
+    if (n_tok <= 0 && a.n_splits > 1) {
+        if (lane < G) {
+            float* pp = a.partial + (((int64_t)s * a.Hq + h * G + lane) * a.n_splits + split) * (D + 2);
+            pp[D] = -INFINITY;
+            pp[D + 1] = 0.0f;
+        }
+        return;
+    }
     const int32_t* btab = a.block_table + (int64_t)srow * a.max_blocks;
     constexpr bool paged = PG;   // on-demand sparse pages
     // block ids of the range, one page per lane (a range spans at most 64 pages)
@@ -1053,13 +1064,14 @@ static hipError_t launch_mfma(const AttnArgs& a, hipStream_t st) {
     const int G = a.Hq / a.H;
     if (a.pages_per_split > 64) return hipErrorInvalidValue;
     const size_t shm = (size_t)G * a.pages_per_split * P * sizeof(float);
-    dim3 grid(a.n_splits, a.H, a.n_seqs);
+    const uint32_t grid = attn_grid(a);
+    if (grid == 0) return hipErrorInvalidValue;
     if (G == 1)
-        hipLaunchKernelGGL((attn_mfma_kernel<1, PG>), grid, dim3(64), shm, st, a);
+        hipLaunchKernelGGL((attn_mfma_kernel<1, PG>), dim3(grid), dim3(64), shm, st, a);
     else if (G == 2)
-        hipLaunchKernelGGL((attn_mfma_kernel<2, PG>), grid, dim3(64), shm, st, a);
+        hipLaunchKernelGGL((attn_mfma_kernel<2, PG>), dim3(grid), dim3(64), shm, st, a);
     else if (G == 4)
-        hipLaunchKernelGGL((attn_mfma_kernel<4, PG>), grid, dim3(64), shm, st, a);
+        hipLaunchKernelGGL((attn_mfma_kernel<4, PG>), dim3(grid), dim3(64), shm, st, a);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();

@@ -79,6 +79,25 @@ struct AttnArgs {
     const int32_t* tok_pos;
 };
 
+// Attention workgroups form a 1-D grid with the KV head varying fastest, then the row,
+// then the page range.  Workgroups are handed to the eight XCDs round-robin by linear id,
+// so every XCD receives the same heads of every row and range: an equal share of the
+// work even when sequence lengths vary (with the range fastest, XCD k would get ranges k
+// and k + 8 of every sequence, and the late ranges exist only for long sequences).  Early
+// ranges go out first, so the short or empty last ranges fill the tail.
+struct AttnTile {
+    int split, h, s;
+};
+__device__ __forceinline__ AttnTile attn_tile(const AttnArgs& a) {
+    const uint32_t id = blockIdx.x, hs = id / (uint32_t)a.H;   // the grid fits 31 bits
+    return AttnTile{(int)(hs / (uint32_t)a.n_seqs), (int)(id % (uint32_t)a.H), (int)(hs % (uint32_t)a.n_seqs)};
+}
+// Workgroups of an attention launch; 0 when the grid would not fit one dimension.
+inline uint32_t attn_grid(const AttnArgs& a) {
+    const int64_t n = (int64_t)a.n_splits * a.H * a.n_seqs;
+    return (n > 0 && n <= 0x7fffffff) ? (uint32_t)n : 0u;
+}
+
 // Split-K plan used by both the workspace query and the launch.
 struct SplitPlan {
     int32_t pages_per_split, n_splits;
