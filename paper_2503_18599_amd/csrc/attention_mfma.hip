@@ -481,13 +481,15 @@ __device__ __forceinline__ void key_corrections(Smem<G>& S, const AttnArgs& a, f
         const uint32_t* w = reinterpret_cast<const uint32_t*>(&S.sparse[pos & ~3]);
         const uint32_t sh = pos & 3;
         uint32_t cur = w[0], nxt = w[1];
-        const uint32_t pc0 = 0x03020100u + (uint32_t)(128 - r.c0) * 0x01010101u;
+        // position bytes 64 + i - c0 of entries i..i+3: bit 6 marks chunk 1 (a chunk holds at
+        // most 64 entries, so the used bytes stay below 128)
+        const uint32_t pc0 = 0x03020100u + (uint32_t)(64 - r.c0) * 0x01010101u;
         // per dword: channels (7 bits, chunk on top), dense offsets, raw entries (nibble
         // shifts), table slots
         auto decode = [&](int kk, uint32_t& ch4, uint32_t& do4, uint32_t& ent, uint32_t& ct4) {
             ent = __builtin_amdgcn_alignbyte(nxt, cur, sh);
-            const uint32_t chk = (pc0 + (uint32_t)kk * 0x01010101u) & 0x80808080u;
-            ch4 = (ent & 0x3f3f3f3fu) | (chk >> 1);                 // channel
+            const uint32_t pcb = pc0 + (uint32_t)kk * 0x01010101u;
+            ch4 = (ent & 0x3f3f3f3fu) | (pcb & 0xc0c0c0c0u);        // channel
             do4 = (ch4 >> 1) & 0x3c3c3c3cu;                         // (channel / 8) * 4
             ct4 = ((ent >> 2) & 0x30303030u) ^ swz;
         };
@@ -495,7 +497,8 @@ __device__ __forceinline__ void key_corrections(Smem<G>& S, const AttnArgs& a, f
         for (int kk = 0; kk < full; kk += 4) {
             uint32_t ch4, do4, ent, ct4;
             decode(kk, ch4, do4, ent, ct4);
-            cur = nxt;
+            // the next block's pair of dwords, read whole (no register shuffle between blocks)
+            cur = w[(kk >> 2) + 1];
             nxt = w[(kk >> 2) + 2];
             // phases kept apart so that a dword's reads issue together
             uint32_t dw[4];
@@ -574,18 +577,21 @@ __device__ __forceinline__ void value_corrections(Smem<G>& S, const AttnArgs& a,
         const uint32_t* w = reinterpret_cast<const uint32_t*>(&S.sparse[pos & ~3]);
         const uint32_t sh = pos & 3;
         uint32_t cur = w[0], nxt = w[1];
-        const uint32_t pc0 = 0x03020100u + (uint32_t)(128 - r.c0) * 0x01010101u;
+        // position bytes 64 + i - c0 of entries i..i+3: bit 6 marks chunk 1 (a chunk holds at
+        // most 64 entries, so the used bytes stay below 128)
+        const uint32_t pc0 = 0x03020100u + (uint32_t)(64 - r.c0) * 0x01010101u;
         auto decode = [&](int kk, uint32_t& ch4, uint32_t& ct4) {
             const uint32_t ent = __builtin_amdgcn_alignbyte(nxt, cur, sh);
-            const uint32_t chk = (pc0 + (uint32_t)kk * 0x01010101u) & 0x80808080u;
-            ch4 = (ent & 0x3f3f3f3fu) | (chk >> 1);               // channel per byte
+            const uint32_t pcb = pc0 + (uint32_t)kk * 0x01010101u;
+            ch4 = (ent & 0x3f3f3f3fu) | (pcb & 0xc0c0c0c0u);      // channel per byte
             ct4 = ((ent >> 2) & 0x30303030u) ^ swz;
         };
         const int full = r.cnt & ~3;
         for (int kk = 0; kk < full; kk += 4) {
             uint32_t ch4, ct4;
             decode(kk, ch4, ct4);
-            cur = nxt;
+            // the next block's pair of dwords, read whole (no register shuffle between blocks)
+            cur = w[(kk >> 2) + 1];
             nxt = w[(kk >> 2) + 2];
             uint32_t x[4], dw[4];
 #pragma unroll
@@ -692,35 +698,56 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
 
     // Key-pass A operand: row = 8*(head%2) + 4*type + limb, type 0 -> sum q u, 1 -> sum q h.
     // Byte (4f + b) of k-group g4 in MFMA m pairs with feature f of dense byte 16*g4+4*m+b.
+    // Each lane first encodes the eight limb words of dense byte `lane` (channels 2 lane and
+    // 2 lane + 1) for each head of the row set into LDS (the dense staging area, unused until
+    // the key loop); a lane then gathers limb r of four bytes with three byte permutes.
     v4i afk[NRS][4];
     {
-        const int row = lane & 15, g4 = lane >> 4, type = (row >> 2) & 1, r = row & 3;
+        // (a copy of the lane id the compiler cannot see through, so that no address formed
+        // here is kept alive for reuse in the loops)
+        int ln;
+        asm volatile("v_mov_b32 %0, %1" : "=v"(ln) : "v"(lane));
+        const int row = ln & 15, g4 = ln >> 4, type = (row >> 2) & 1, r = row & 3;
+        uint32_t* E = reinterpret_cast<uint32_t*>(&S.dense[0][0]);   // [2 heads][2 types][4 features][64 bytes]
+        const uint32_t sel = (uint32_t)r | ((uint32_t)(r + 4) << 8);
 #pragma unroll
         for (int rs = 0; rs < NRS; ++rs) {
-            const int hd = rs * 2 + (row >> 3);
+#pragma unroll
+            for (int hl = 0; hl < 2; ++hl) {
+                if (rs * 2 + hl < G) {
+                    const int2 qq = *reinterpret_cast<const int2*>(&S.qi()[rs * 2 + hl][2 * ln]);
+                    const int qe = qq.x, qo = qq.y;
+                    uint32_t* e = E + hl * 512 + ln;
+                    // the weights of (raw byte, low nibble, bits 7|3, bit 3) for sum q u ...
+                    e[0 * 64] = enc(8 * qo);
+                    e[1 * 64] = enc(128 * qe - 8 * qo);
+                    e[2 * 64] = enc(-16 * qo);
+                    e[3 * 64] = enc(16 * qo);
+                    // ... and for sum q h
+                    e[4 * 64] = 0u;
+                    e[5 * 64] = 0u;
+                    e[6 * 64] = enc(-qo);
+                    e[7 * 64] = enc(16 * qe + qo);
+                }
+            }
+            wave_sync();
+            const bool live = rs * 2 + (row >> 3) < G;
 #pragma unroll
             for (int m = 0; m < 4; ++m) {
-                uint32_t f0 = 0, f1 = 0, f2 = 0, f3 = 0;
-                if (hd < G) {
 #pragma unroll
-                    for (int bb = 0; bb < 4; ++bb) {
-                        const int pr = g4 * 16 + m * 4 + bb;
-                        const int qe = S.qi()[hd][2 * pr], qo = S.qi()[hd][2 * pr + 1];
-                        const int w0 = type ? 0 : 8 * qo;
-                        const int w1 = type ? 0 : 128 * qe - 8 * qo;
-                        const int w2 = type ? -qo : -16 * qo;
-                        const int w3 = type ? 16 * qe + qo : 16 * qo;
-                        f0 |= byte_of(enc(w0), r) << (8 * bb);
-                        f1 |= byte_of(enc(w1), r) << (8 * bb);
-                        f2 |= byte_of(enc(w2), r) << (8 * bb);
-                        f3 |= byte_of(enc(w3), r) << (8 * bb);
+                for (int f = 0; f < 4; ++f) {
+                    uint32_t x = 0;
+                    if (live) {
+                        const uint4 w = *reinterpret_cast<const uint4*>(
+                            &E[(row >> 3) * 512 + (type * 4 + f) * 64 + g4 * 16 + m * 4]);
+                        const uint32_t t01 = __builtin_amdgcn_perm(w.y, w.x, sel);
+                        const uint32_t t23 = __builtin_amdgcn_perm(w.w, w.z, sel);
+                        x = __builtin_amdgcn_perm(t23, t01, 0x05040100u);
                     }
+                    afk[rs][m][f] = (int)x;
                 }
-                afk[rs][m][0] = (int)f0;
-                afk[rs][m][1] = (int)f1;
-                afk[rs][m][2] = (int)f2;
-                afk[rs][m][3] = (int)f3;
             }
+            if (rs + 1 < NRS) wave_sync();   // (the next row set's words replace these)
         }
     }
 
@@ -867,10 +894,14 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
     wave_sync();
 
     // ---- pass 2: values ------------------------------------------------------------
-    const int hq = lane >> 4;               // output lane owns (head hq, dim 16*nt + (lane&15))
-    float oacc[8];
+    // Output lane (head hq, dim 16*nt + (lane&15)) for several heads.  With one head the
+    // sums of tiles nt = 4*hf + hq (hf = 0, 1) are gathered into row group hq first, so that
+    // every lane converts two tiles.
+    const int hq = lane >> 4;
+    constexpr int NO = G == 1 ? 2 : 8;
+    float oacc[NO];
 #pragma unroll
-    for (int nt = 0; nt < 8; ++nt) oacc[nt] = 0.0f;
+    for (int nt = 0; nt < NO; ++nt) oacc[nt] = 0.0f;
     float pb[G];
     float ocr[G][2];   // value corrections of channels lane and lane + 64
 #pragma unroll
@@ -905,27 +936,32 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         }
         // fixed-point coefficients p*Delta, p*Gp of the group's tokens (lane = token), one
         // shift per head; correction tables (scaled by p when one head reads them)
-        int vsh[G];
+        int vsh;   // one fixed-point shift for every head of the group
         int fsh;
         {
             const int pg = lane >> 4, t = lane & 15;
             const int nv = pick4(pg, gc.nval[0], gc.nval[1], gc.nval[2], gc.nval[3]);
             const bool vt = t < nv;
             const Tok T = token_consts(mreg, tv);
-            float p0 = 0.0f;
+            float p0 = 0.0f, cx[G], gx[G], mx = 0.0f;
 #pragma unroll
             for (int hd = 0; hd < G; ++hd) {
                 const float p = vt ? sc[hd * cap + tok0 + lane] : 0.0f;
                 if (hd == 0) p0 = p;
-                const float cx = vt ? p * T.dm : 0.0f;
-                const float gx = vt ? p * T.gp : 0.0f;
+                cx[hd] = vt ? p * T.dm : 0.0f;
+                gx[hd] = vt ? p * T.gp : 0.0f;
                 if (vt) pb[hd] = fmaf(p, T.base, pb[hd]);
-                const int sh = fix_shift(wave_max_nonneg(fmaxf(fabsf(cx), fabsf(gx))));
-                vsh[hd] = sh;
+                mx = fmaxf(mx, fmaxf(fabsf(cx[hd]), fabsf(gx[hd])));
+            }
+            // (a head whose weights are far below the group's largest keeps fewer bits, but
+            // its group then adds little next to its own range total, which is at least 1)
+            vsh = fix_shift(wave_max_nonneg(mx));
+#pragma unroll
+            for (int hd = 0; hd < G; ++hd) {
                 // Weights of token pair lane/2 (even lane: its own C, G and the odd
                 // partner's): 128 (C_e u_e + C_o u_o + G_e h_e + G_o h_o) over the features
                 // (raw byte, low nibble, bits 7|3, bit 3) of the nibble byte, as 4 limbs each.
-                const int ce = (int)rintf(ldexpf(cx, sh)), ge = (int)rintf(ldexpf(gx, sh));
+                const int ce = (int)rintf(ldexpf(cx[hd], vsh)), ge = (int)rintf(ldexpf(gx[hd], vsh));
                 const int co = __builtin_amdgcn_update_dpp(0, ce, 0x101, 0xf, 0xf, false);   // row_shl:1
                 const int go = __builtin_amdgcn_update_dpp(0, ge, 0x101, 0xf, 0xf, false);
                 if ((lane & 1) == 0)
@@ -1003,8 +1039,23 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         }
         // the dense sums leave the accumulators before the correction walk, which then has
         // their registers
-        if (hq < G) {
-            const int e = pick4(hq, vsh[0], vsh[G > 1 ? 1 : 0], vsh[G > 2 ? 2 : 0], vsh[G > 3 ? 3 : 0]) + 7;
+        if constexpr (G == 1) {
+            // rows 4-15 are zero (no second head): two 16-lane row swaps and one 32-lane swap
+            // move the limbs of tiles 4hf+1..4hf+3 into row groups 1-3 of tile 4hf's registers
+            const int e = vsh + 7;
+#pragma unroll
+            for (int hf = 0; hf < 2; ++hf) {
+                v4i m;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int a01 = __builtin_amdgcn_permlane16_swap(gacc[4 * hf][r], gacc[4 * hf + 1][r], false, false)[0];
+                    const int a23 = __builtin_amdgcn_permlane16_swap(gacc[4 * hf + 2][r], gacc[4 * hf + 3][r], false, false)[0];
+                    m[r] = (int)__builtin_amdgcn_permlane32_swap(a01, a23, false, false)[0];
+                }
+                oacc[hf] += ldexpf(limbs(m), -e);
+            }
+        } else if (hq < G) {
+            const int e = vsh + 7;
 #pragma unroll
             for (int nt = 0; nt < 8; ++nt) oacc[nt] += ldexpf(limbs(gacc[nt]), -e);
         }
@@ -1033,20 +1084,21 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         S.oc()[hd][lane + 64] = ocr[hd][1];
     }
     wave_sync();
-    if (hq < G) {
-        const int64_t row = (int64_t)s * a.Hq + h * G + hq;
-        const float l = S.l[hq];
+    if (hq < G || G == 1) {
+        const int hd = G == 1 ? 0 : hq;
+        const int64_t row = (int64_t)s * a.Hq + h * G + hd;
+        const float l = S.l[hd];
 #pragma unroll
-        for (int nt = 0; nt < 8; ++nt) {
-            const int j = nt * 16 + (lane & 15);
-            const float o = S.pbase[hq] + oacc[nt] + S.oc()[hq][j];
+        for (int nt = 0; nt < NO; ++nt) {
+            const int j = (G == 1 ? 4 * nt + hq : nt) * 16 + (lane & 15);
+            const float o = S.pbase[hd] + oacc[nt] + S.oc()[hd][j];
             if (a.n_splits == 1) {
                 a.out[row * D + j] = (l > 0.0f) ? o / l : 0.0f;
             } else {
                 float* pp = a.partial + (row * a.n_splits + split) * (D + 2);
                 pp[j] = o;
                 if (j == 0) {
-                    pp[D] = S.m[hq];
+                    pp[D] = S.m[hd];
                     pp[D + 1] = l;
                 }
             }
