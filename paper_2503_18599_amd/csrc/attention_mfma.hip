@@ -43,11 +43,15 @@ constexpr int CB = 32;                     // COO count bytes at the start of a 
 constexpr int cmax(int x, int y) { return x > y ? x : y; }
 constexpr int GRP = 4;                     // pages per group (two correction pairs)
 constexpr int GT = GRP * P;                // tokens per group
-// LDS stride of a page's dense bytes.  Value pages are staged in two token halves 576
-// bytes apart (a channel's dword of eight tokens at 4 * channel), so that the halves and
-// neighbouring pages fall on opposite bank halves.
+// LDS stride of a key page's dense bytes (token rows of 64 bytes).
 constexpr int PSTR = 1088;
-constexpr int VHALF = 576;
+// Value pages are staged as stored (channel c's dwords of tokens 0-7 and 8-15 at 8c and
+// 8c + 4), page q + 2 right after page q, pair q at q * VREG: the two dwords a value MFMA
+// lane takes (pages q and q + 2) are then 1024 bytes apart, one two-address read, and
+// staging writes the loaded registers unchanged.
+constexpr int VREG = 2 * 1024 + 128;
+static_assert(2 * VREG <= GRP * PSTR, "value staging fits the dense buffer");
+__host__ __device__ constexpr int vpos(int pg) { return (pg & 1) * VREG + (pg >> 1) * 1024; }
 constexpr int SPCAP = P * D;               // sparse capacity of one record
 constexpr int SSLOT = 448;                 // staged COO bytes per page (larger pages: read from HBM)
 constexpr int SPL = GRP * SSLOT;           // group sparse bytes staged in LDS
@@ -71,6 +75,13 @@ __device__ __forceinline__ v4i features(uint32_t d) {
     b[2] = (int)(d & 0x88888888u);
     b[3] = (int)(d & 0x08080808u);
     return b;
+}
+
+// Feature f of four dwords of nibble bytes (f = 0 the bytes themselves).
+__device__ __forceinline__ v4i feature_of(const uint4& d, int f) {
+    const uint32_t msk = f == 1 ? 0x0f0f0f0fu : f == 2 ? 0x88888888u : 0x08080808u;
+    if (f == 0) return v4i{(int)d.x, (int)d.y, (int)d.z, (int)d.w};
+    return v4i{(int)(d.x & msk), (int)(d.y & msk), (int)(d.z & msk), (int)(d.w & msk)};
 }
 
 __device__ __forceinline__ v4i mfma(v4i a, v4i b, v4i c) {
@@ -205,8 +216,8 @@ __device__ __forceinline__ uint4 ld16(const uint8_t* p) {
 template <int G>
 struct Smem {
     __align__(16) uint8_t tab_[4 * GT * 2 * 8];   // correction table; qi
-    __align__(16) uint8_t dense[GRP][PSTR];       // K: token rows of 64 bytes; V: two halves of
-                                                  // channel dwords
+    __align__(16) uint8_t dense[GRP][PSTR];       // K: token rows of 64 bytes; V: page pairs
+                                                  // (vflat)
     __align__(16) uint8_t qo_[G * D * 4];         // q (keys); oci (values)
     __align__(16) uint8_t tw_[cmax(cmax(GT * 16, G * GT * 8), G * D * 4)];
     float pbase[G];
@@ -215,6 +226,9 @@ struct Smem {
     __align__(16) uint8_t sparse[SPL + 80];       // page p's COO bytes at p*SSLOT; + slack for
                                                   // whole-dword reads past a run
 
+    // the dense buffer as bytes (value staging)
+    __device__ uint8_t* vflat() { return &dense[0][0]; }
+    __device__ const uint8_t* vflat() const { return &dense[0][0]; }
     // query in fixed point (before the key pass)
     __device__ int (&qi())[G][D] { return *reinterpret_cast<int (*)[G][D]>(tab_); }
     // query in fp16, the heads of a channel side by side (key pass)
@@ -236,22 +250,36 @@ struct Grp {
     int npg;
 };
 
-// `blk_lane` holds, in lane i, the block id of page p_begin + i of the range (or -1).
-__device__ __forceinline__ Grp make_group(const AttnArgs& a, int blk_lane, int p_begin, int g0,
-                                          int p_end, int L, int h, int which) {
+// The range's pages, one per lane (lane i: page p_begin + i; a range spans at most 32
+// pages, and every lane index read below stays under 64): the byte offset of the page's
+// key record from the pool (0, a valid stand-in record, when the page is absent or outside
+// the range) and its valid slots (0 then).  Formed once per range, so a group's pages cost
+// three lane reads each instead of a block-id check and a 64-bit product.
+struct PageLanes {
+    uint32_t off_lo, off_hi;
+    int nval;
+};
+
+__device__ __forceinline__ PageLanes page_lanes(const AttnArgs& a, const int32_t* btab, int p_begin, int p_end,
+                                                int L, int h, int lane) {
+    const int pi = p_begin + lane;
+    const int blk = (pi < p_end) ? btab[pi] : -1;
+    const bool ok = blk >= 0 && blk < a.num_blocks;
+    const uint64_t off = ok ? (uint64_t)(((int64_t)blk * a.H + h) * 2) * (uint64_t)a.stride : 0u;
+    return PageLanes{(uint32_t)off, (uint32_t)(off >> 32), ok ? max(0, min(P, L - pi * P)) : 0};
+}
+
+// Group of pages g0 .. g0 + 3 of the range; `rec` is the pool plus `which` record strides.
+__device__ __forceinline__ Grp make_group(const PageLanes& pl, const uint8_t* rec, int p_begin, int g0, int p_end) {
     Grp gr;
     gr.npg = max(0, min(GRP, p_end - g0));
 #pragma unroll
     for (int pg = 0; pg < GRP; ++pg) {
-        gr.base[pg] = a.pool;
-        gr.nval[pg] = 0;
-        if (pg < gr.npg) {
-            const int blk = __builtin_amdgcn_readlane(blk_lane, g0 + pg - p_begin);
-            if (blk >= 0 && blk < a.num_blocks) {
-                gr.base[pg] = a.pool + (((int64_t)blk * a.H + h) * 2 + which) * a.stride;
-                gr.nval[pg] = max(0, min(P, L - (g0 + pg) * P));
-            }
-        }
+        const int li = g0 + pg - p_begin;
+        const uint64_t off = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)pl.off_hi, li) << 32) |
+                             (uint32_t)__builtin_amdgcn_readlane((int)pl.off_lo, li);
+        gr.base[pg] = rec + off;
+        gr.nval[pg] = __builtin_amdgcn_readlane(pl.nval, li);
     }
     return gr;
 }
@@ -553,7 +581,8 @@ __device__ __forceinline__ void value_corrections(Smem<G>& S, const AttnArgs& a,
     const int pg = lane >> 4, t = lane & 15;
     const uint32_t tbo = (uint32_t)lane * 64u;
     const uint32_t swz = (uint32_t)((lane >> 1) & 3) * 0x10101010u;
-    const uint32_t dcol = off_of(S, &S.dense[pg][(t >> 3) * VHALF]);  // + 4 * channel
+    // the token's dwords: + 8 * channel
+    const uint32_t dcol = off_of(S, S.vflat() + vpos(pg) + (t >> 3) * 4);
     const uint32_t nsh = (uint32_t)(t & 7) * 4u;
     const uint32_t occ = off_of(S, &S.oci(0, 0));                     // + 4 * channel (+ 4 D * head)
     float pt[G];
@@ -567,7 +596,7 @@ __device__ __forceinline__ void value_corrections(Smem<G>& S, const AttnArgs& a,
     };
     // one entry: channel offset x = 4 * channel, table slot byte ct
     auto entry = [&](uint32_t x, uint32_t ct) {
-        const uint32_t dw = lds_at<uint32_t>(S, dcol + x);
+        const uint32_t dw = lds_at<uint32_t>(S, dcol + 2 * x);
         const uint32_t n = __builtin_amdgcn_ubfe(dw, nsh, 4);
         const float2 kv = lds_at<float2>(S, (tbo | ct) | (n & 8u));
         add(x, fmaf((float)n, kv.y, kv.x));
@@ -597,7 +626,7 @@ __device__ __forceinline__ void value_corrections(Smem<G>& S, const AttnArgs& a,
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 x[i] = shl_byte(ch4, 2u, i);
-                dw[i] = lds_at<uint32_t>(S, dcol + x[i]);
+                dw[i] = lds_at<uint32_t>(S, dcol + 2 * x[i]);
             }
             __builtin_amdgcn_sched_barrier(0);
             uint32_t n[4];
@@ -660,8 +689,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
     }
     const int32_t* btab = a.block_table + (int64_t)srow * a.max_blocks;
     constexpr bool paged = PG;   // on-demand sparse pages
-    // block ids of the range, one page per lane (a range spans at most 64 pages)
-    const int blk_lane = (p_begin + lane < p_end) ? btab[p_begin + lane] : -1;
+    const PageLanes pl = page_lanes(a, btab, p_begin, p_end, L, h, lane);
+    const uint8_t* const krec = a.pool;
+    const uint8_t* const vrec = a.pool + a.stride;
 
     float tk[4], tv[4];
 #pragma unroll
@@ -671,7 +701,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
     }
 
     // the first key group's counts and metadata are needed before anything else
-    Grp gc = make_group(a, blk_lane, p_begin, p_begin, p_end, L, h, 0);
+    Grp gc = make_group(pl, krec, p_begin, p_begin, p_end);
     uint4 hreg = count_chunk(gc, lane);
     int2 tab_c = paged ? page_tab(gc, lane) : int2{0, 0};   // (on-demand sparse pages)
     Meta mreg = meta_words(gc, lane);
@@ -697,7 +727,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
     wave_sync();
 
     // Key-pass A operand: row = 8*(head%2) + 4*type + limb, type 0 -> sum q u, 1 -> sum q h.
-    // Byte (4f + b) of k-group g4 in MFMA m pairs with feature f of dense byte 16*g4+4*m+b.
+    // MFMA f takes feature f of the lane's 16 dense bytes: its byte (4m + b) of k-group g4
+    // pairs with feature f of dense byte 16*g4 + 4*m + b.  The raw-byte operand is then the
+    // loaded register itself and the others one AND per dword.
     // Each lane first encodes the eight limb words of dense byte `lane` (channels 2 lane and
     // 2 lane + 1) for each head of the row set into LDS (the dense staging area, unused until
     // the key loop); a lane then gathers limb r of four bytes with three byte permutes.
@@ -744,7 +776,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
                         const uint32_t t23 = __builtin_amdgcn_perm(w.w, w.z, sel);
                         x = __builtin_amdgcn_perm(t23, t01, 0x05040100u);
                     }
-                    afk[rs][m][f] = (int)x;
+                    afk[rs][f][m] = (int)x;
                 }
             }
             if (rs + 1 < NRS) wave_sync();   // (the next row set's words replace these)
@@ -769,7 +801,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         for (int pg = 0; pg < GRP; ++pg) dreg[pg] = ld16(gc.base[pg] + koff);
         sparse_chunks<PG>(a, gc, tab_c, used, lane, sreg0, sreg1);
     }
-    Grp gn = make_group(a, blk_lane, p_begin, p_begin + GRP, p_end, L, h, 0);
+    Grp gn = make_group(pl, krec, p_begin, p_begin + GRP, p_end);
     hreg = count_chunk(gn, lane);
     int2 tab_n = paged ? page_tab(gn, lane) : int2{0, 0};
     for (int g0 = p_begin; g0 < p_end; g0 += GRP) {
@@ -784,13 +816,12 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
 #pragma unroll
                 for (int rs = 0; rs < NRS; ++rs) acc[pg][rs] = v4i{0, 0, 0, 0};
 #pragma unroll
-            for (int m = 0; m < 4; ++m) {
+            for (int f = 0; f < 4; ++f) {
 #pragma unroll
                 for (int pg = 0; pg < GRP; ++pg) {
-                    const uint4 dv = dreg[pg];
-                    const v4i B = features(m == 0 ? dv.x : m == 1 ? dv.y : m == 2 ? dv.z : dv.w);
+                    const v4i B = feature_of(dreg[pg], f);
 #pragma unroll
-                    for (int rs = 0; rs < NRS; ++rs) acc[pg][rs] = mfma(afk[rs][m], B, acc[pg][rs]);
+                    for (int rs = 0; rs < NRS; ++rs) acc[pg][rs] = mfma(afk[rs][f], B, acc[pg][rs]);
                 }
             }
 #pragma unroll
@@ -835,12 +866,13 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
             if (stg1_in) *reinterpret_cast<uint4*>(&S.sparse[stg + 256]) = sreg1;
         }
         wave_sync();
-        // next group: heads -> layout -> issue its sparse bytes and the heads after it
-        Grp gnn = gn;
+        // next group: heads -> layout -> issue its sparse bytes and the heads after it.
+        // Also past the range's last group (stand-in records without valid slots): every
+        // path through the loop then has the same loads in flight, so the compiler's wait
+        // counts stay exact instead of draining the whole prefetch at the loop's edges.
+        Grp gnn;
         int2 tab_nn = tab_n;
-        fits_n = true;
-        run_n = 0;
-        if (gn.npg > 0) {
+        {
             if (lane < 2 * GRP) *reinterpret_cast<uint4*>(&S.head[0][16 * lane]) = hreg;
             wave_sync();
             Run r;
@@ -849,7 +881,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
             wave_sync();
             sparse_chunks<PG>(a, gn, tab_n, used, lane, sreg0, sreg1);
             mreg = meta_words(gn, lane);
-            gnn = make_group(a, blk_lane, p_begin, g0 + 2 * GRP, p_end, L, h, 0);
+            gnn = make_group(pl, krec, p_begin, g0 + 2 * GRP, p_end);
             hreg = count_chunk(gnn, lane);
             if constexpr (PG) tab_nn = page_tab(gnn, lane);
         }
@@ -865,7 +897,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
     }
 
     // the first value group's heads go out before the softmax
-    gc = make_group(a, blk_lane, p_begin, p_begin, p_end, L, h, 1);
+    gc = make_group(pl, vrec, p_begin, p_begin, p_end);
     hreg = count_chunk(gc, lane);
     if constexpr (PG) tab_c = page_tab(gc, lane);
     mreg = meta_words(gc, lane);
@@ -915,18 +947,14 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         for (int pg = 0; pg < GRP; ++pg) dreg[pg] = ld16(gc.base[pg] + voff);
         sparse_chunks<PG>(a, gc, tab_c, used, lane, sreg0, sreg1);
     }
-    gn = make_group(a, blk_lane, p_begin, p_begin + GRP, p_end, L, h, 1);
+    gn = make_group(pl, vrec, p_begin, p_begin + GRP, p_end);
     hreg = count_chunk(gn, lane);
     if constexpr (PG) tab_n = page_tab(gn, lane);
     for (int g0 = p_begin; g0 < p_end; g0 += GRP) {
         const int tok0 = (g0 - p_begin) * P;
         const bool staged = fits_c;
 #pragma unroll
-        for (int pg = 0; pg < GRP; ++pg) {
-            // channels 2*lane and 2*lane+1: tokens 0-7 to the first half, 8-15 to the second
-            *reinterpret_cast<uint2*>(&S.dense[pg][lane * 8]) = make_uint2(dreg[pg].x, dreg[pg].z);
-            *reinterpret_cast<uint2*>(&S.dense[pg][VHALF + lane * 8]) = make_uint2(dreg[pg].y, dreg[pg].w);
-        }
+        for (int pg = 0; pg < GRP; ++pg) *reinterpret_cast<uint4*>(S.vflat() + vpos(pg) + lane * 16) = dreg[pg];
         // the next group's dense bytes go out as soon as these are staged
 #pragma unroll
         for (int pg = 0; pg < GRP; ++pg) dreg[pg] = ld16(gn.base[pg] + voff);
@@ -985,12 +1013,13 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
             token_table(S, lane, T, ws);
         }
         wave_sync();
-        // next group: heads -> layout -> issue its sparse bytes and the heads after it
-        Grp gnn = gn;
+        // next group: heads -> layout -> issue its sparse bytes and the heads after it.
+        // Also past the range's last group (stand-in records without valid slots): every
+        // path through the loop then has the same loads in flight, so the compiler's wait
+        // counts stay exact instead of draining the whole prefetch at the loop's edges.
+        Grp gnn;
         int2 tab_nn = tab_n;
-        fits_n = true;
-        run_n = 0;
-        if (gn.npg > 0) {
+        {
             if (lane < 2 * GRP) *reinterpret_cast<uint4*>(&S.head[0][16 * lane]) = hreg;
             wave_sync();
             Run r;
@@ -999,7 +1028,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
             wave_sync();
             sparse_chunks<PG>(a, gn, tab_n, used, lane, sreg0, sreg1);
             mreg = meta_words(gn, lane);
-            gnn = make_group(a, blk_lane, p_begin, g0 + 2 * GRP, p_end, L, h, 1);
+            gnn = make_group(pl, vrec, p_begin, g0 + 2 * GRP, p_end);
             hreg = count_chunk(gnn, lane);
             if constexpr (PG) tab_nn = page_tab(gnn, lane);
         }
@@ -1007,34 +1036,44 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         v4i gacc[8];
 #pragma unroll
         for (int nt = 0; nt < 8; ++nt) gacc[nt] = v4i{0, 0, 0, 0};
-#pragma unroll
-        for (int pp = 0; pp < GRP; pp += 2) {
+        {
             // A operand of lane (row = 4*head + limb r, k-group g4): for each feature f the
-            // limb-r bytes of token pairs 4*g4 + 0..3 of this page pair (a byte transpose)
-            {
-                const int row = lane & 15, hdr = row >> 2, g4 = lane >> 4, r = row & 3;
-                v4i av = v4i{0, 0, 0, 0};
-                if (hdr < G) {
-                    const uint4* wp = &S.wv()[hdr][(pp >> 1) * 16 + g4 * 4];
-                    const uint4 w0 = wp[0], w1 = wp[1], w2 = wp[2], w3 = wp[3];
-                    const uint32_t sel = (uint32_t)r | ((uint32_t)(r + 4) << 8);
-                    auto col = [&](uint32_t a0, uint32_t a1, uint32_t a2, uint32_t a3) {
-                        const uint32_t t01 = __builtin_amdgcn_perm(a1, a0, sel);
-                        const uint32_t t23 = __builtin_amdgcn_perm(a3, a2, sel);
-                        return (int)__builtin_amdgcn_perm(t23, t01, 0x05040100u);
-                    };
-                    av[0] = col(w0.x, w1.x, w2.x, w3.x);
-                    av[1] = col(w0.y, w1.y, w2.y, w3.y);
-                    av[2] = col(w0.z, w1.z, w2.z, w3.z);
-                    av[3] = col(w0.w, w1.w, w2.w, w3.w);
-                }
-                const uint8_t* dsrc = &S.dense[pp + (g4 >> 1)][(g4 & 1) * VHALF];
+            // limb-r bytes of token pairs 4*g4 + 0..3 of page pair pq (a byte transpose).
+            // MFMA 0 takes features 0 and 1, MFMA 1 features 2 and 3, each of the pages
+            // g4/2 (pair 0) and g4/2 + 2 (pair 1): A and B registers line up as (pair 0,
+            // pair 1) of the first feature, then of the second.
+            const int row = lane & 15, hdr = row >> 2, g4 = lane >> 4, r = row & 3;
+            v4i av[2] = {v4i{0, 0, 0, 0}, v4i{0, 0, 0, 0}};
+            if (hdr < G) {
+                const uint32_t sel = (uint32_t)r | ((uint32_t)(r + 4) << 8);
+                auto col = [&](uint32_t a0, uint32_t a1, uint32_t a2, uint32_t a3) {
+                    const uint32_t t01 = __builtin_amdgcn_perm(a1, a0, sel);
+                    const uint32_t t23 = __builtin_amdgcn_perm(a3, a2, sel);
+                    return (int)__builtin_amdgcn_perm(t23, t01, 0x05040100u);
+                };
 #pragma unroll
-                for (int nt = 0; nt < 8; ++nt) {
-                    const int j = nt * 16 + (lane & 15);
-                    const uint32_t dw = *reinterpret_cast<const uint32_t*>(dsrc + j * 4);
-                    gacc[nt] = mfma(av, features(dw), gacc[nt]);
+                for (int pq = 0; pq < 2; ++pq) {
+                    const uint4* wp = &S.wv()[hdr][pq * 16 + g4 * 4];
+                    const uint4 w0 = wp[0], w1 = wp[1], w2 = wp[2], w3 = wp[3];
+                    av[pq][0] = col(w0.x, w1.x, w2.x, w3.x);
+                    av[pq][1] = col(w0.y, w1.y, w2.y, w3.y);
+                    av[pq][2] = col(w0.z, w1.z, w2.z, w3.z);
+                    av[pq][3] = col(w0.w, w1.w, w2.w, w3.w);
                 }
+            }
+            const v4i A0 = v4i{av[0][0], av[1][0], av[0][1], av[1][1]};
+            const v4i A1 = v4i{av[0][2], av[1][2], av[0][3], av[1][3]};
+            const uint8_t* dsrc = S.vflat() + vpos(g4 >> 1) + (g4 & 1) * 4;
+#pragma unroll
+            for (int nt = 0; nt < 8; ++nt) {
+                const int j = nt * 16 + (lane & 15);
+                const uint2 dd = make_uint2(*reinterpret_cast<const uint32_t*>(dsrc + j * 8),
+                                            *reinterpret_cast<const uint32_t*>(dsrc + 1024 + j * 8));
+                const v4i B0 = v4i{(int)dd.x, (int)dd.y, (int)(dd.x & 0x0f0f0f0fu), (int)(dd.y & 0x0f0f0f0fu)};
+                const v4i B1 = v4i{(int)(dd.x & 0x88888888u), (int)(dd.y & 0x88888888u), (int)(dd.x & 0x08080808u),
+                                   (int)(dd.y & 0x08080808u)};
+                gacc[nt] = mfma(A0, B0, gacc[nt]);
+                gacc[nt] = mfma(A1, B1, gacc[nt]);
             }
         }
         // the dense sums leave the accumulators before the correction walk, which then has
@@ -1114,7 +1153,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
 template <bool PG>
 static hipError_t launch_mfma(const AttnArgs& a, hipStream_t st) {
     const int G = a.Hq / a.H;
-    if (a.pages_per_split > 64) return hipErrorInvalidValue;
+    // a range spans at most 32 pages (the lane reads of the page table rely on it)
+    if (a.pages_per_split > 32 || a.pages_per_split * P > mfma_score_cap()) return hipErrorInvalidValue;
     const size_t shm = (size_t)G * a.pages_per_split * P * sizeof(float);
     const uint32_t grid = attn_grid(a);
     if (grid == 0) return hipErrorInvalidValue;
