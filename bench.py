@@ -332,8 +332,9 @@ def main():
     if args.ratio_sweep:
         return ratio_sweep(args)
     if args.gpus != 1 or world != 1:
-        print(json.dumps({"error": "this benchmark runs on exactly one GPU; multi-GPU runs are "
-                                   "not part of this build", "n_gpus": args.gpus}))
+        print(json.dumps({"error": "this benchmark runs on exactly one GPU: the library has no "
+                                   "multi-GPU path (sharding by sequence or KV head needs no "
+                                   "exchange and is left to the caller)", "n_gpus": args.gpus}))
         sys.exit(2)
 
     import numpy as np
