@@ -211,16 +211,21 @@ __global__ __launch_bounds__(D) void attn_combine_kernel(AttnArgs a) {
     const int64_t row = blockIdx.x;
     const int j = threadIdx.x;
     const float* pp = a.partial + row * a.n_splits * (D + 2);
-    float M = -INFINITY;
-    for (int k = 0; k < a.n_splits; ++k)
-        if (pp[k * (D + 2) + D + 1] > 0.0f) M = fmaxf(M, pp[k * (D + 2) + D]);
-    float num = 0.0f, den = 0.0f;
+    // One pass with a running maximum (the sums are rescaled when it grows), unrolled so
+    // that several ranges' loads are in flight together; ranges with l = 0 (past a
+    // sequence's end) are skipped.
+    float M = -INFINITY, num = 0.0f, den = 0.0f;
+#pragma unroll 4
     for (int k = 0; k < a.n_splits; ++k) {
-        const float l = pp[k * (D + 2) + D + 1];
-        if (!(l > 0.0f)) continue;
-        const float w = __expf(pp[k * (D + 2) + D] - M);
-        num += w * pp[k * (D + 2) + j];
-        den += w * l;
+        const float* pk = pp + k * (D + 2);
+        const float m = pk[D], l = pk[D + 1], o = pk[j];
+        if (l > 0.0f) {
+            const float Mn = fmaxf(M, m);
+            const float r = __expf(M - Mn), w = __expf(m - Mn);
+            num = fmaf(num, r, w * o);
+            den = fmaf(den, r, w * l);
+            M = Mn;
+        }
     }
     a.out[row * D + j] = (den > 0.0f) ? num / den : 0.0f;
 }
