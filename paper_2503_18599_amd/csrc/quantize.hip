@@ -1,13 +1,21 @@
 // Online KV quantization into the paged cache (Oaken Sec. 4.3-4.5, Sec. 5.2
-// quantization engine).
+// quantization engine and MMU).
 //
-// One workgroup covers the new tokens of one sequence that fall into one page, for
-// one KV head and one of K/V; each wave64 quantizes one token's vector.  Lane l owns
-// elements j = 64*c + l, so a wave's ballot over chunk c is exactly that chunk's
-// outlier mask: its popcount is the chunk count and mbcnt gives each outlier's slot
-// in the COO stream (the zero-remove step of the engine) without any branch.
-// Group selection is done with compares and selects, so waves never diverge on the
-// value distribution.
+// One wave writes one record segment: the new tokens of one sequence that fall into one
+// page, for one KV head and one of K/V (a workgroup holds four independent waves).  A
+// vector of d elements is spread over d/8 lanes with eight consecutive elements each
+// (one 16-byte load), so a wave quantizes 64 / (d/8) vectors at a time: for d = 128 the
+// four 16-lane rows of the wave hold four tokens.  Group minima and maxima are taken
+// over a lane's eight elements, then across the vector's lanes by DPP, with no LDS round
+// trip.  Group selection is compares and selects, so waves never diverge on the value
+// distribution.
+//
+// The lanes of a wave hold their vectors' elements in stream order (slot, then 64-value
+// chunk, then index), so a wave-wide prefix sum of per-lane outlier counts places every
+// COO entry in the record's stream: the engine's zero-remove step, without branches.
+// Outputs are assembled in LDS and leave in wide stores: K rows as dwords straight from
+// registers, metadata as dwords, V pages (channel-major) and COO streams in 16-byte
+// chunks when the segment starts the page.
 #include "oaken_internal.h"
 
 #include <hip/hip_fp16.h>
@@ -18,287 +26,368 @@
 namespace oaken {
 namespace {
 
-__device__ inline float half_bits_to_float(uint16_t b) {
-    return __half2float(__ushort_as_half(b));
+__device__ inline float half_bits_to_float(uint32_t b) {
+    return __half2float(__ushort_as_half((uint16_t)b));
 }
 
 __device__ inline uint16_t float_to_half_bits(float f) {
     return __half_as_ushort(__float2half_rn(f));
 }
 
-// Wave reductions: a DPP shift-scan within each row of 16 lanes leaves the row's result
-// in its lane 15; the four row results combine through readlane (no LDS round trips).
-template <typename Op>
-__device__ inline float wave_reduce(float v, float ident, Op op) {
-    const int id = __float_as_int(ident);
-    v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(id, __float_as_int(v), 0x111, 0xf, 0xf, false)));
-    v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(id, __float_as_int(v), 0x112, 0xf, 0xf, false)));
-    v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(id, __float_as_int(v), 0x114, 0xf, 0xf, false)));
-    v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(id, __float_as_int(v), 0x118, 0xf, 0xf, false)));
-    const int x = __float_as_int(v);
-    return op(op(__int_as_float(__builtin_amdgcn_readlane(x, 15)), __int_as_float(__builtin_amdgcn_readlane(x, 31))),
-              op(__int_as_float(__builtin_amdgcn_readlane(x, 47)), __int_as_float(__builtin_amdgcn_readlane(x, 63))));
+// (every lane of these permutations reads a lane of its own group)
+template <int C>
+__device__ inline int dpp_i(int v) {
+    return __builtin_amdgcn_mov_dpp(v, C, 0xf, 0xf, true);
 }
 
-__device__ inline float wave_min(float v) {
-    return wave_reduce(v, INFINITY, [](float p, float q) { return fminf(p, q); });
-}
+// Reductions over the N = 8 or 16 lanes of a vector (aligned lane groups): quad
+// butterflies, then the half-row and row mirrors.  Every lane of the group gets the
+// result.
+constexpr int kQuadXor1 = 0xb1, kQuadXor2 = 0x4e, kRowHalfMirror = 0x141, kRowMirror = 0x140;
 
-__device__ inline float wave_max(float v) {
-    return wave_reduce(v, -INFINITY, [](float p, float q) { return fmaxf(p, q); });
+template <int N>
+__device__ inline uint32_t group_min_u(uint32_t v) {
+    v = min(v, (uint32_t)dpp_i<kQuadXor1>((int)v));
+    v = min(v, (uint32_t)dpp_i<kQuadXor2>((int)v));
+    v = min(v, (uint32_t)dpp_i<kRowHalfMirror>((int)v));
+    if constexpr (N == 16) v = min(v, (uint32_t)dpp_i<kRowMirror>((int)v));
+    return v;
+}
+template <int N>
+__device__ inline int group_max_i(int v) {
+    v = max(v, dpp_i<kQuadXor1>(v));
+    v = max(v, dpp_i<kQuadXor2>(v));
+    v = max(v, dpp_i<kRowHalfMirror>(v));
+    if constexpr (N == 16) v = max(v, dpp_i<kRowMirror>(v));
+    return v;
+}
+// Sum over aligned groups of 8 lanes.
+__device__ inline int sum8(int v) {
+    v += dpp_i<kQuadXor1>(v);
+    v += dpp_i<kQuadXor2>(v);
+    v += dpp_i<kRowHalfMirror>(v);
+    return v;
 }
 
 // Inclusive prefix sum over the wave (DPP row scan, then the rows' totals).
 __device__ inline int wave_incl_scan(int x, int lane) {
-    x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false);
-    x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false);
-    x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false);
-    x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false);
+    x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false);   // row_shr:1
+    x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false);   // row_shr:2
+    x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false);   // row_shr:4
+    x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false);   // row_shr:8
     const int r0 = __builtin_amdgcn_readlane(x, 15), r1 = __builtin_amdgcn_readlane(x, 31);
     const int r2 = __builtin_amdgcn_readlane(x, 47);
     const int row = lane >> 4;
     return x + (row == 0 ? 0 : row == 1 ? r0 : row == 2 ? r0 + r1 : r0 + r1 + r2);
 }
 
+// The lanes of one wave hand LDS data to each other: LDS operations of a wave execute in
+// issue order, so only compiler fences are needed.
+__device__ inline void wave_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// One wave's staging area: the segment's COO bytes (from the segment's first entry),
+// V nibbles one byte per element, fp16 metadata and per-chunk counts by slot, and the
+// record's sparse page ids (on-demand pages).
+template <int D>
+struct WaveBuf {
+    __align__(16) uint8_t coo[kPage * D];
+    __align__(16) uint8_t vn[kPage][D];
+    __align__(16) uint16_t meta[kPage][6];
+    uint8_t cnt[kPage][D / 64];
+    int32_t tab[kPage * D / kSparsePage];
+};
+
+constexpr int kWavesPerGroup = 4;
+
 template <int D, bool PG>
-__global__ __launch_bounds__(1024) void quantize_kernel(QuantArgs a) {
-    constexpr int NC = D / 64;           // 64-value chunks per vector
+__global__ __launch_bounds__(64 * kWavesPerGroup) void quantize_kernel(QuantArgs a) {
+    constexpr int NC = D / 64;                 // 64-value chunks per vector
+    constexpr int LPV = D / 8;                 // lanes per vector
+    constexpr int VPP = 64 / LPV;              // vectors per pass
+    constexpr int NPASS = kPage / VPP;         // passes for a whole page
     constexpr Layout LY = PG ? make_layout_paged(kPage, D) : make_layout(kPage, D);
     constexpr int NT = kPage * D / kSparsePage;   // sparse pages a record can need
+    constexpr int CAP = kPage * D;                // COO capacity of a record
 
-    __shared__ uint8_t s_counts[kPage][NC];
-    __shared__ uint8_t s_vnib[kPage][D];
-    __shared__ __align__(16) uint8_t s_krow[kPage][D / 2];
-    __shared__ int s_tab[NT];            // the record's sparse page ids (on-demand pages)
+    __shared__ WaveBuf<D> bufs[kWavesPerGroup];
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    WaveBuf<D>& W = bufs[wave];
 
+    const int hw = (int)blockIdx.z * kWavesPerGroup + wave;   // (KV head, K|V)
+    if (hw >= 2 * a.H) return;
+    const int h = hw >> 1, which = hw & 1;
     const int s = blockIdx.y;
-    const int h = blockIdx.z >> 1;
-    const int which = blockIdx.z & 1;
-    const int wave = threadIdx.x >> 6;
-    const int lane = threadIdx.x & 63;
-
     const int row0 = a.cu_tokens[s];
     const int n_new = a.cu_tokens[s + 1] - row0;
     const int pos0 = a.start_pos[s];
     const int page = pos0 / kPage + (int)blockIdx.x;
     const int t_lo = max(pos0, page * kPage);
     const int t_hi = min(pos0 + n_new, (page + 1) * kPage);
-    if (n_new <= 0 || t_lo >= t_hi || page >= a.max_blocks) return;   // uniform per block
+    if (n_new <= 0 || t_lo >= t_hi || page >= a.max_blocks) return;   // uniform per wave
     const int blk = a.block_table[(int64_t)s * a.max_blocks + page];
     if (blk < 0 || blk >= a.num_blocks) return;
-
-    const int slot0 = t_lo - page * kPage;
-    const int nslots = t_hi - t_lo;
+    const int slot0 = t_lo - page * kPage;     // first slot written
+    const int nslots = t_hi - t_lo;            // 1 .. 16
     uint8_t* rec = a.pool + (((int64_t)blk * a.H + h) * 2 + which) * a.stride;
-    const bool active = wave < nslots;
-    const int slot = slot0 + wave;
 
-    // Reads that do not depend on this call's values go out first, so that their latency
-    // overlaps the quantization: the COO counts of the record's earlier slots, and (values,
-    // when the call starts at an odd slot) the bytes the previous token shares with it.
-    int pre_cnt = 0;
-    if (lane < slot0) {
+    // ---- loads: every pass's input first, then what this call keeps from the record --
+    const int r = lane / LPV, m = lane % LPV;  // vector within a pass, lane within the vector
+    const uint16_t* xsrc = which ? a.v_new : a.k_new;
+    const int64_t rbase = (int64_t)row0 + (t_lo - pos0);
+    uint4 xin[NPASS];
 #pragma unroll
-        for (int c = 0; c < NC; ++c) pre_cnt += rec[LY.counts + lane * NC + c];
+    for (int p = 0; p < NPASS; ++p) {
+        const int i = p * VPP + r;
+        const int64_t row = rbase + (i < nslots ? i : 0);   // (past the segment: its first row)
+        xin[p] = *reinterpret_cast<const uint4*>(xsrc + (row * a.H + h) * D + 8 * m);
     }
-    // (on-demand pages: the record's page table, for the pages it already holds)
+    // the COO bytes of the record's earlier slots: this segment's stream starts after them
+    int pre = 0;
+    if (slot0 > 0) {
+        const int c = lane < slot0 * NC ? (int)rec[LY.counts + lane] : 0;
+        pre = __builtin_amdgcn_readlane(wave_incl_scan(c, lane), 63);
+        pre = min(pre, CAP);
+    }
     const int tab_pre = (PG && lane < NT) ? reinterpret_cast<const int32_t*>(rec + LY.sparse)[lane] : 0;
-    uint8_t old_b[D / 64];
+    // V starting at an odd slot shares its first byte per channel with the slot before
+    uint32_t old_b[NC];
 #pragma unroll
-    for (int k = 0; k < D / 64; ++k) old_b[k] = 0;
-    if (which == 1 && (slot0 & 1) && wave == 0) {
+    for (int k = 0; k < NC; ++k) old_b[k] = 0;
+    if (which == 1 && (slot0 & 1)) {
 #pragma unroll
-        for (int k = 0; k < D / 64; ++k) old_b[k] = rec[LY.dense + (lane + 64 * k) * (kPage / 2) + (slot0 >> 1)];
+        for (int k = 0; k < NC; ++k) old_b[k] = rec[LY.dense + (lane + 64 * k) * (kPage / 2) + (slot0 >> 1)];
     }
 
-    // ---- quantize this wave's vector (Eq. 1-4) -------------------------------------
     const float* th = a.thr + (h * 2 + which) * 4;
     const float lo_o = th[0], lo_i = th[1], hi_i = th[2], hi_o = th[3];
 
-    float av[NC];
-    int grp[NC];
-    bool side[NC];
+    // ---- quantize, pass by pass (Eq. 1-4) ----------------------------------------
+    int off = pre;   // stream offset of the pass's first entry (wave-uniform)
+    const int npass = (nslots + VPP - 1) / VPP;
 #pragma unroll
-    for (int c = 0; c < NC; ++c) { av[c] = 0.0f; grp[c] = 1; side[c] = false; }
-    float mn[3] = {INFINITY, INFINITY, INFINITY};
-    float mx[3] = {-INFINITY, -INFINITY, -INFINITY};
-    if (active) {
-        const int row = row0 + (page * kPage + slot - pos0);
-        const uint16_t* x = (which ? a.v_new : a.k_new) + ((int64_t)row * a.H + h) * D;
+    for (int p = 0; p < NPASS; ++p) {
+        if (p >= npass) break;   // (uniform)
+        const int i = p * VPP + r;
+        const bool valid = i < nslots;
+        const int t = slot0 + i;
+        const uint32_t w4[4] = {xin[p].x, xin[p].y, xin[p].z, xin[p].w};
+
+        // group, side and shifted magnitude per element; group minima and maxima over the
+        // magnitudes' bit patterns (non-negative floats order as integers): an element of
+        // another group reads as 0xffffffff, the largest unsigned and the smallest signed
+        // key, so one key serves the unsigned minimum and the signed maximum
+        float mag[8];
+        bool outer[8], middle[8], side[8];
+        uint32_t kmin[3] = {~0u, ~0u, ~0u};
+        int kmax[3] = {-1, -1, -1};
 #pragma unroll
-        for (int c = 0; c < NC; ++c) {
-            const float xf = half_bits_to_float(x[c * 64 + lane]);
-            const bool outer = (xf < lo_o) || (xf > hi_o);
-            const bool middle = !outer && ((xf < lo_i) || (xf > hi_i));
-            const int g = outer ? 2 : (middle ? 1 : 0);
-            const bool sd = outer ? (xf > hi_o) : (middle ? (xf > hi_i) : (xf >= 0.0f));
-            const float shift = outer ? (sd ? hi_o : lo_o) : (middle ? (sd ? hi_i : lo_i) : 0.0f);
-            const float mag = (g == 0) ? fabsf(xf) : fabsf(xf - shift);
-            av[c] = mag;
-            grp[c] = g;
-            side[c] = sd;
-#pragma unroll
-            for (int k = 0; k < 3; ++k) {
-                mn[k] = (g == k) ? fminf(mn[k], mag) : mn[k];
-                mx[k] = (g == k) ? fmaxf(mx[k], mag) : mx[k];
-            }
+        for (int e = 0; e < 8; ++e) {
+            const float xf = half_bits_to_float((e & 1) ? (w4[e >> 1] >> 16) : (w4[e >> 1] & 0xffffu));
+            const bool c_ho = xf > hi_o, c_lo = xf < lo_o, c_hi = xf > hi_i, c_li = xf < lo_i;
+            const bool o = c_ho || c_lo;                 // Eq. 1, outer
+            const bool not_inner = c_hi || c_li;         // outer or middle
+            const float shift = c_lo ? lo_o : (c_ho ? hi_o : (c_hi ? hi_i : lo_i));
+            const float dv = not_inner ? xf - shift : xf;   // Eq. 4 (inner not shifted)
+            mag[e] = fabsf(dv);
+            // the side is the sign of the shifted value: non-zero for outer and middle
+            // values, and x >= 0 (-0 included) for inner ones
+            side[e] = !(dv < 0.0f);
+            outer[e] = o;
+            middle[e] = not_inner && !o;
+            const uint32_t mb = __float_as_uint(mag[e]);
+            const uint32_t ki = not_inner ? ~0u : mb, km = middle[e] ? mb : ~0u, ko = o ? mb : ~0u;
+            kmin[0] = min(kmin[0], ki); kmax[0] = max(kmax[0], (int)ki);
+            kmin[1] = min(kmin[1], km); kmax[1] = max(kmax[1], (int)km);
+            kmin[2] = min(kmin[2], ko); kmax[2] = max(kmax[2], (int)ko);
         }
-    }
-    float gmin[3], grange[3], gsig[3];
+        float gmin[3], grng[3];
 #pragma unroll
-    for (int k = 0; k < 3; ++k) {
-        float lo = wave_min(mn[k]);
-        float hi = wave_max(mx[k]);
-        if (!(hi >= lo)) { lo = 0.0f; hi = 0.0f; }   // empty group
-        const float levels = (k == 1) ? 7.0f : 15.0f;
-        gmin[k] = lo;
-        grange[k] = hi - lo;
-        gsig[k] = (grange[k] == 0.0f) ? 0.0f : levels / grange[k];
-    }
+        for (int g = 0; g < 3; ++g) {
+            const uint32_t lo = group_min_u<LPV>(kmin[g]);
+            const int hi = group_max_i<LPV>(kmax[g]);
+            const bool empty = hi < 0;                   // (0, 0) for an empty group
+            gmin[g] = empty ? 0.0f : __uint_as_float(lo);
+            grng[g] = empty ? 0.0f : __int_as_float(hi) - gmin[g];
+        }
+        // Eq. 2: lane 2g of the vector forms sigma_g = L/R, lane 2g+1 Delta_g = R/L (its
+        // metadata); one correctly rounded division per lane
+        const int g6 = (m >> 1) < 3 ? (m >> 1) : 0;
+        const bool is_delta = (m & 1) != 0;
+        const float Rg = g6 == 0 ? grng[0] : (g6 == 1 ? grng[1] : grng[2]);
+        const float Lg = g6 == 1 ? 7.0f : 15.0f;
+        float quo = (is_delta ? Rg : Lg) / (is_delta ? Lg : Rg);
+        if (!is_delta && Rg == 0.0f) quo = 0.0f;
+        const int vbase = lane & ~(LPV - 1);
+        float sig[3];
+#pragma unroll
+        for (int g = 0; g < 3; ++g) sig[g] = __shfl(quo, vbase + 2 * g, 64);
 
-    uint8_t nib[NC];
-    uint8_t coo[NC];
-    uint64_t omask[NC];
-#pragma unroll
-    for (int c = 0; c < NC; ++c) {
-        const int g = grp[c];
-        const int lv = (g == 1) ? 7 : 15;
-        const float gm = (g == 0) ? gmin[0] : ((g == 1) ? gmin[1] : gmin[2]);
-        const float gs = (g == 0) ? gsig[0] : ((g == 1) ? gsig[1] : gsig[2]);
-        const float sh = av[c] - gm;
-        const float sc = sh * gs;
-        int code = (int)rintf(sc);
-        code = min(max(code, 0), lv);
-        const int u = side[c] ? (lv + 1) + code : lv - code;
-        nib[c] = (uint8_t)(u & 15);
-        coo[c] = (uint8_t)(((u >> 4) << 7) | ((g == 2) << 6) | lane);
-        omask[c] = __ballot(active && g != 1);
-    }
-    if (active && lane == 0) {
-#pragma unroll
-        for (int c = 0; c < NC; ++c) s_counts[slot][c] = (uint8_t)__popcll(omask[c]);
-    }
-    __syncthreads();
-
-    // sparse start of this slot: the counts of the earlier slots (slots before this call's
-    // first one live in the record), as a prefix sum with lane = slot
-    int base = 0;
-    {
+        // Eq. 3 and the offset-binary code u = side ? 2^b + c : 2^b - 1 - c, whose low four
+        // bits are c ^ L ^ (side ? 15 : 0).  No clamp is needed: 0 <= a - Min <= R rounds
+        // to at most R, and R * fl(L / R) rounds to less than L + 1/2.
+        uint32_t nib[8], cb[8];
         int cnt = 0;
-        if (lane < kPage) {
-            if (lane < slot0) {
-                cnt = pre_cnt;
-            } else if (lane < slot0 + nslots) {
 #pragma unroll
-                for (int c = 0; c < NC; ++c) cnt += s_counts[lane][c];
-            }
+        for (int e = 0; e < 8; ++e) {
+            const float gm = outer[e] ? gmin[2] : (middle[e] ? gmin[1] : gmin[0]);
+            const float gs = outer[e] ? sig[2] : (middle[e] ? sig[1] : sig[0]);
+            const uint32_t ci = (uint32_t)rintf((mag[e] - gm) * gs);
+            nib[e] = ci ^ (middle[e] ? 7u : 15u) ^ (side[e] ? 15u : 0u);
+            const uint32_t c0 = outer[e] ? (0x40u | (uint32_t)((8 * m + e) & 63)) : (uint32_t)((8 * m + e) & 63);
+            cb[e] = side[e] ? (c0 | 0x80u) : c0;
+            cnt += (valid && !middle[e]) ? 1 : 0;
         }
-        const int incl = wave_incl_scan(cnt, lane);
-        base = __shfl(incl - cnt, slot < kPage ? slot : 0, 64);
-        if constexpr (PG) {
-            // Sparse pages on demand (Sec. 5.2 MMU): the record's COO stream now needs
-            // ceil(new_used / 256) pages; wave 0 pops the ones the record does not hold
-            // yet from the free list and enters them in its table (entry = 1 + page id,
-            // 0 = none held).  An empty list sets the overflow flag and leaves those pages
-            // out (their bytes are not written).
-            const int new_used = __shfl(incl, slot0 + nslots - 1, 64);
-            const int p_new = (new_used + kSparsePage - 1) / kSparsePage;
-            if (wave == 0) {
-                const bool need = lane < p_new && tab_pre == 0;
-                const uint64_t nm = __ballot(need);
-                const int k = __popcll(nm);
-                int t = 0;
-                if (k > 0 && lane == 0) {
-                    t = atomicSub(&a.sfree[0], k);
-                    if (t < k) {              // not enough pages: give the count back
-                        atomicAdd(&a.sfree[0], k);
-                        atomicOr(&a.sfree[1], 1);
-                    }
-                }
-                t = __shfl(t, 0, 64);
-                int entry = tab_pre;
-                if (need && t >= k && t <= a.spages) {   // (a consistent list never exceeds the pool)
-                    const int r = __popcll(nm & ((1ull << lane) - 1ull));
-                    entry = 1 + a.sfree[2 + t - k + r];
-                    reinterpret_cast<int32_t*>(rec + LY.sparse)[lane] = entry;
-                }
-                if (lane < NT) s_tab[lane] = entry - 1;
-            }
-            __syncthreads();
-        }
-    }
-    if (active) {
-        const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-        int off = base;
-#pragma unroll
-        for (int c = 0; c < NC; ++c) {
-            if ((omask[c] >> lane) & 1ull) {
-                const int o = off + __popcll(omask[c] & below);
-                if constexpr (PG) {
-                    const int id = s_tab[o / kSparsePage];
-                    if (id >= 0 && id < a.spages)
-                        a.spool[(int64_t)id * kSparsePage + (o % kSparsePage)] = coo[c];
-                } else {
-                    rec[LY.sparse + o] = coo[c];
-                }
-            }
-            off += __popcll(omask[c]);
-        }
-        if (lane < NC) rec[LY.counts + slot * NC + lane] = s_counts[slot][lane];
-        if (lane < 6) {
-            const int k = lane >> 1;
-            const float lv = (k == 1) ? 7.0f : 15.0f;
-            const float gm = (k == 0) ? gmin[0] : ((k == 1) ? gmin[1] : gmin[2]);
-            const float gr = (k == 0) ? grange[0] : ((k == 1) ? grange[1] : grange[2]);
-            const uint16_t hb = (lane & 1) ? float_to_half_bits(gr / lv) : float_to_half_bits(gm);
-            *reinterpret_cast<uint16_t*>(rec + LY.meta + slot * 12 + lane * 2) = hb;
-        }
+
+        // dense nibbles: K row dwords go out directly; V nibbles are staged by slot
         if (which == 0) {
-            // K: token-major, element j at byte slot*D/2 + j/2, low nibble = even j; the
-            // row is assembled in LDS and leaves in dwords below
+            uint32_t kw = 0;
 #pragma unroll
-            for (int c = 0; c < NC; ++c) {
-                const int hi_n = __builtin_amdgcn_update_dpp(0, (int)nib[c], 0x101, 0xf, 0xf, false);   // lane + 1
-                if ((lane & 1) == 0) s_krow[slot][(c * 64 + lane) / 2] = (uint8_t)(nib[c] | (hi_n << 4));
+            for (int e = 0; e < 8; ++e) kw |= nib[e] << (4 * e);
+            if (valid) *reinterpret_cast<uint32_t*>(rec + LY.dense + t * (D / 2) + 4 * m) = kw;
+        } else if (valid) {
+            const uint32_t lo = nib[0] | (nib[1] << 8) | (nib[2] << 16) | (nib[3] << 24);
+            const uint32_t hi = nib[4] | (nib[5] << 8) | (nib[6] << 16) | (nib[7] << 24);
+            *reinterpret_cast<uint2*>(&W.vn[t][8 * m]) = make_uint2(lo, hi);
+        }
+        // metadata: lane m < 6 holds field m of the slot: Min_g (even), Delta_g (odd)
+        if (valid && m < 6) W.meta[t][m] = float_to_half_bits(is_delta ? quo : gmin[g6]);
+
+        // COO entries: positions from a wave-wide prefix sum of the lanes' counts
+        const int incl = wave_incl_scan(cnt, lane);
+        const int c8 = sum8(cnt);   // entries of the lane's 64-value chunk
+        if (valid && (m & 7) == 0) W.cnt[t][m >> 3] = (uint8_t)c8;
+        int pos = off - pre + incl - cnt;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            if (valid && !middle[e]) {
+                if (pos < CAP) W.coo[pos] = (uint8_t)cb[e];
+                ++pos;
+            }
+        }
+        off += __builtin_amdgcn_readlane(incl, 63);
+    }
+    wave_sync();
+
+    // ---- stores ------------------------------------------------------------------
+    const int n = min(off, CAP) - pre;   // COO bytes of this segment
+    if (lane < nslots * NC) rec[LY.counts + slot0 * NC + lane] = W.cnt[slot0 + lane / NC][lane % NC];
+    if (lane < 3 * nslots)
+        reinterpret_cast<uint32_t*>(rec + LY.meta + slot0 * 12)[lane] =
+            reinterpret_cast<const uint32_t*>(&W.meta[slot0][0])[lane];
+    if (which == 1) {
+        if (slot0 == 0) {
+            // whole pairs: lane l writes channels 2l and 2l+1 (16 bytes); slots past the
+            // segment read as zero nibbles (writing a slot invalidates the later ones)
+            if (2 * lane < D) {
+                uint32_t wq[kPage];
+#pragma unroll
+                for (int tt = 0; tt < kPage; ++tt)
+                    wq[tt] = tt < nslots ? (uint32_t)*reinterpret_cast<const uint16_t*>(&W.vn[tt][2 * lane]) : 0u;
+                uint32_t d2[4];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    // pairs 2k and 2k+1: low byte channel 2l, high byte channel 2l+1
+                    const uint32_t c0 = wq[4 * k] | (wq[4 * k + 1] << 4);
+                    const uint32_t c1 = wq[4 * k + 2] | (wq[4 * k + 3] << 4);
+                    d2[k] = c0 | (c1 << 16);
+                }
+                uint4 ov;
+                ov.x = __builtin_amdgcn_perm(d2[1], d2[0], 0x06040200u);   // channel 2l, pairs 0-3
+                ov.y = __builtin_amdgcn_perm(d2[3], d2[2], 0x06040200u);   // pairs 4-7
+                ov.z = __builtin_amdgcn_perm(d2[1], d2[0], 0x07050301u);   // channel 2l+1
+                ov.w = __builtin_amdgcn_perm(d2[3], d2[2], 0x07050301u);
+                *reinterpret_cast<uint4*>(rec + LY.dense + 16 * lane) = ov;
             }
         } else {
+            // a segment starting inside the page: byte by byte, the first byte keeping the
+            // earlier slot's low nibble when the segment starts at an odd slot
+            const int p_lo = slot0 >> 1, p_hi = (slot0 + nslots - 1) >> 1;
 #pragma unroll
-            for (int c = 0; c < NC; ++c) s_vnib[slot][c * 64 + lane] = nib[c];
-        }
-    }
-    __syncthreads();
-
-    if (which == 0) {
-        // K rows of this call's slots: one contiguous, 4-byte aligned range
-        const uint32_t* src = reinterpret_cast<const uint32_t*>(&s_krow[slot0][0]);
-        uint32_t* dst = reinterpret_cast<uint32_t*>(rec + LY.dense + slot0 * (D / 2));
-        for (int i = threadIdx.x; i < nslots * (D / 8); i += blockDim.x) dst[i] = src[i];
-    } else {
-        // V: channel-major, element j of slot t at byte j*P/2 + t/2, low nibble = even t.
-        // The first pair (which may keep an earlier token's even nibble) is written by wave
-        // 0, one channel per lane; the later pairs by all threads, consecutive threads on
-        // consecutive bytes of a channel row.
-        const int p_lo = slot0 >> 1, p_hi = (slot0 + nslots - 1) >> 1;
-        if (wave == 0) {
-            const int te = 2 * p_lo, to = te + 1;
-            const bool has_e = te >= slot0;
-            const bool has_o = to < slot0 + nslots;
-#pragma unroll
-            for (int k = 0; k < D / 64; ++k) {
+            for (int k = 0; k < NC; ++k) {
                 const int j = lane + 64 * k;
-                const uint8_t lo_n = has_e ? s_vnib[te][j] : (uint8_t)(old_b[k] & 0x0f);
-                const uint8_t hi_n = has_o ? (uint8_t)(s_vnib[to][j] << 4) : (uint8_t)0;
-                rec[LY.dense + j * (kPage / 2) + p_lo] = (uint8_t)(lo_n | hi_n);
+                for (int q = p_lo; q <= p_hi; ++q) {
+                    const int te = 2 * q, to = te + 1;
+                    const uint32_t lo_n = te >= slot0 ? W.vn[te][j] : (old_b[k] & 0x0fu);
+                    const uint32_t hi_n = to < slot0 + nslots ? W.vn[to][j] : 0u;
+                    rec[LY.dense + j * (kPage / 2) + q] = (uint8_t)(lo_n | (hi_n << 4));
+                }
             }
         }
-        const int npairs = p_hi - p_lo;   // pairs after the first
-        for (int i = threadIdx.x; i < npairs * D; i += blockDim.x) {
-            const int j = i / npairs;
-            const int p = p_lo + 1 + i % npairs;
-            const int te = 2 * p, to = 2 * p + 1;
-            const bool has_o = to < slot0 + nslots;
-            rec[LY.dense + j * (kPage / 2) + p] = has_o ? (uint8_t)(s_vnib[te][j] | (s_vnib[to][j] << 4))
-                                                        : s_vnib[te][j];
+    }
+
+    // ---- COO stream ----------------------------------------------------------------
+    if constexpr (PG) {
+        // Sparse pages on demand (Sec. 5.2 MMU): the record's stream now needs
+        // ceil(used / 256) pages; the ones it does not hold yet are reserved from the
+        // free list with a compare-and-swap that only succeeds while enough pages are
+        // free (so the count never passes below what is really free), and entered in its
+        // table (entry = 1 + page id, 0 = none held).  A list without enough pages sets
+        // the overflow flag and leaves those pages out (their bytes are not written).
+        const int p_new = min(NT, (pre + n + kSparsePage - 1) / kSparsePage);
+        const bool need = lane < p_new && tab_pre == 0;
+        const uint64_t nm = __ballot(need);
+        const int k = __popcll(nm);
+        int top = -1;
+        if (k > 0 && lane == 0) {
+            int cur = __hip_atomic_load(&a.sfree[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            while (true) {
+                if (cur < k || cur > a.spages) {   // (a consistent list never exceeds the pool)
+                    atomicOr(&a.sfree[1], 1);
+                    break;
+                }
+                const int seen = atomicCAS(&a.sfree[0], cur, cur - k);
+                if (seen == cur) {
+                    top = cur;
+                    break;
+                }
+                cur = seen;   // another record took pages first: retry with the new count
+            }
+        }
+        top = __shfl(top, 0, 64);
+        int entry = tab_pre;
+        if (need && top >= k) {
+            const int rk = __popcll(nm & ((1ull << lane) - 1ull));
+            entry = 1 + a.sfree[2 + top - k + rk];
+            reinterpret_cast<int32_t*>(rec + LY.sparse)[lane] = entry;
+        }
+        if (lane < NT) W.tab[lane] = entry - 1;
+        wave_sync();
+    }
+    auto coo_dst = [&](int o) -> uint8_t* {
+        if constexpr (PG) {
+            const int id = W.tab[o / kSparsePage];
+            return (id >= 0 && id < a.spages) ? a.spool + (int64_t)id * kSparsePage + (o % kSparsePage) : nullptr;
+        } else {
+            return rec + LY.sparse + o;
+        }
+    };
+    if (n > 0) {
+        if ((pre & 15) == 0) {
+            // 16-byte chunks (never straddling a sparse page); bytes past the stream are
+            // written as zero
+            for (int c = lane; c * 16 < n; c += 64) {
+                uint4 v = *reinterpret_cast<const uint4*>(&W.coo[16 * c]);
+                const int nb = n - 16 * c;
+                if (nb < 16) {
+                    uint32_t* vw = reinterpret_cast<uint32_t*>(&v);
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int keep = min(max(nb - 4 * q, 0), 4);
+                        vw[q] = keep == 4 ? vw[q] : (vw[q] & ((1u << (8 * keep)) - 1u));
+                    }
+                }
+                uint8_t* dst = coo_dst(pre + 16 * c);
+                if (dst) *reinterpret_cast<uint4*>(dst) = v;
+            }
+        } else {
+            for (int b = lane; b < n; b += 64) {
+                uint8_t* dst = coo_dst(pre + b);
+                if (dst) *dst = W.coo[b];
+            }
         }
     }
 }
@@ -306,11 +395,10 @@ __global__ __launch_bounds__(1024) void quantize_kernel(QuantArgs a) {
 }  // namespace
 
 hipError_t launch_quantize(const QuantArgs& a, int d, int max_new_per_seq, hipStream_t st) {
-    const int waves = max(1, min(kPage, max_new_per_seq));
     // pages a run of n tokens can touch: (n + P - 2) / P + 1 (one for a single token)
     const int segs = (max_new_per_seq + kPage - 2) / kPage + 1;
-    dim3 grid(segs, a.n_seqs, a.H * 2);
-    dim3 block(64 * waves);
+    dim3 grid(segs, a.n_seqs, (2 * a.H + kWavesPerGroup - 1) / kWavesPerGroup);
+    dim3 block(64 * kWavesPerGroup);
     const bool pg = a.spool != nullptr;
     if (d == 64 && !pg)
         hipLaunchKernelGGL((quantize_kernel<64, false>), grid, block, 0, st, a);

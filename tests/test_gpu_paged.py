@@ -177,6 +177,56 @@ def test_paged_overflow_sets_flag(B, ref):
     assert cache.sparse_status() == (8, False)
 
 
+def test_paged_exact_pool_never_overflows(B, ref):
+    """A pool holding exactly the pages the records need: every concurrent reservation
+    succeeds (a reservation only takes pages while enough are free), the list ends empty
+    and the records are bit-exact."""
+    case = _case(ref, 4, n_seqs=5, ctx=1500, ctx_min=1)
+    want = case.oracle_pool(ref)
+    big, _ = _paged_cache(B, case)
+    _, tab, need = _assemble(ref, case, big)
+    n_need = int(need.sum())
+    del big
+    for _ in range(3):
+        cache, _ = _paged_cache(B, case, pages=n_need)
+        free, overflow = cache.sparse_status()
+        assert not overflow and free == 0, (free, overflow)
+        got, tab, _ = _assemble(ref, case, cache)
+        compare_pools(ref, case, got, want)
+        held = tab[tab > 0] - 1
+        assert np.unique(held).size == held.size == n_need
+
+
+def _free_list(cache):
+    fl = cache.sparse_free.cpu().numpy()
+    return int(fl[0]), fl[2:2 + int(fl[0])]
+
+
+def test_paged_overflow_then_release_restores_the_list(B, ref):
+    """An undersized pool overflows; after every block is released the free list holds
+    each page exactly once (no page handed to two records, none lost)."""
+    case = _case(ref, 4, n_seqs=5, ctx=1500, ctx_min=1)
+    pages = 200
+    cache, bt = _paged_cache(B, case, pages=pages)
+    free, overflow = cache.sparse_status()
+    assert overflow
+    tab = _tables(B, case, cache)
+    held = tab[tab > 0] - 1
+    assert np.unique(held).size == held.size, "a sparse page is held by two records"
+    assert free == pages - held.size
+    cache.release(torch.arange(case.num_blocks, dtype=torch.int32, device=DEV))
+    n, ids = _free_list(cache)
+    assert n == pages and np.array_equal(np.sort(ids), np.arange(pages))
+
+
+def _tables(B, case, cache):
+    """Every record's sparse page table (int32 [records][entries])."""
+    nt = P * case.d // SPB
+    recs = cache.pool.cpu().numpy().reshape(case.num_blocks * case.H * 2, cache.stride)
+    off = B.record_layout(case.d)["sparse"]
+    return np.ascontiguousarray(recs[:, off:off + 4 * nt]).view(np.int32)
+
+
 @pytest.mark.parametrize("cid,kw,window", [(2, dict(n_seqs=6, ctx=203), 0), (3, dict(n_seqs=3, ctx=2048), 0),
                                            (4, dict(n_seqs=5, ctx=1500, ctx_min=1), 0),
                                            (4, dict(n_seqs=5, ctx=1500, ctx_min=1), 513),
