@@ -32,7 +32,8 @@ def log(msg: str):
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed decode steps (default 20; 64 for the 32K-context workload)")
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", type=int, default=3, help="1..5 (3 = batch-256 Llama-2-13B layer)")
     ap.add_argument("--window", type=int, default=0,
@@ -49,7 +50,13 @@ def parse():
                     help="number-of-groups study: effective bits and error of each encoding variant")
     ap.add_argument("--prefill-chunk", type=int, default=0,
                     help="time chunked-prefill attention for the last N cached tokens of every sequence")
-    ap.add_argument("--cpu-sample-seqs", type=int, default=128)
+    ap.add_argument("--cold", type=int, default=-1,
+                    help="1: write a 1 GiB scratch buffer between steps (outside the timed events) so that "
+                         "no step finds the cache in the 256 MB Infinity Cache; 0: back to back; "
+                         "default: cold for the workloads whose cache is under 1 GB (2 and 5)")
+    ap.add_argument("--no-stream-probe", action="store_true")
+    ap.add_argument("--cpu-sample-seqs", type=int, default=0,
+                    help="sequences in the oracle's timed sample (default: 128, 4 for the 32K context)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after timing, run one plain copy of this size (counter calibration)")
@@ -324,6 +331,79 @@ def prefill_bench(args, w, cache, bt, lens, dev):
     print(json.dumps(res), flush=True)
 
 
+def alg_bytes_per_vector(d: int) -> int:
+    """Bytes of one (token, KV head, K|V) vector without its COO entries: d/2 dense nibbles,
+    d/64 count bytes, 12 bytes of fp16 metadata."""
+    return d // 2 + d // 64 + 12
+
+
+def outlier_prefix(cache, bt_cpu, n_seqs, max_pos):
+    """int64 [n_seqs][H][2][max_pos + 1]: COO entries of positions < p, per sequence, KV head
+    and K|V, from the records' counts."""
+    import torch
+    P, d, H = 16, cache.head_dim, cache.n_kv_heads
+    nc = d // 64
+    nblk = cache.num_blocks
+    rec = cache.pool.view(nblk, H, 2, cache.stride)
+    counts = rec[:, :, :, : P * nc].reshape(nblk, H, 2, P, nc).to(torch.int64).sum(-1).cpu()   # [blk,H,2,P]
+    n_pages = (max_pos + P - 1) // P
+    blocks = bt_cpu[:, :n_pages].to(torch.int64)                                               # [S, pages]
+    per_pos = counts[blocks].permute(0, 2, 3, 1, 4).reshape(n_seqs, H, 2, n_pages * P)[..., :max_pos]
+    out = torch.zeros(n_seqs, H, 2, max_pos + 1, dtype=torch.int64)
+    out[..., 1:] = torch.cumsum(per_pos, -1)
+    return out
+
+
+def attention_bytes(cache, prefix, lens, window, Hq, n_seqs):
+    """Algorithmic bytes of one attention launch over sequences of lengths `lens`: every key
+    and value vector a query sees (dense, counts, metadata, its COO bytes), the queries,
+    the outputs, the block-table entries and the lengths.  Split partials are overhead.
+    Returns (KV-stream bytes, all algorithmic bytes, COO entries, vectors, pages)."""
+    d, H = cache.head_dim, cache.n_kv_heads
+    n_vec, n_out, pages = 0, 0, 0
+    for s in range(n_seqs):
+        L = int(lens[s])
+        lo = max(0, L - window) if window else 0
+        n_vec += (L - lo) * H * 2
+        n_out += int((prefix[s, :, :, L] - prefix[s, :, :, lo]).sum())
+        pages += (L + 15) // 16 - lo // 16
+    kv = n_vec * alg_bytes_per_vector(d) + n_out
+    return kv, kv + n_seqs * Hq * d * (2 + 4) + pages * 4 + n_seqs * 4, n_out, n_vec, pages
+
+
+def stream_probe(cache, dev):
+    """Measured streaming-read bandwidth on this device: a 4 GiB contiguous read, and the
+    first 1456 bytes of every page record of the pool (counts, metadata, dense nibbles and
+    about the mean COO stream at a 10 % outlier share: what decode attention reads per
+    record)."""
+    import torch
+
+    from paper_2503_18599_amd import binding as B
+    res = {}
+    buf = torch.empty(4 << 30, dtype=torch.uint8, device=dev)
+    buf.fill_(1)
+    nrec_pool = cache.pool.numel() // cache.stride
+    per_rec = min(1456, cache.stride // 16 * 16)
+    for name, base, per, stride, n in (("plain_4gib", buf, 4096, 4096, (4 << 30) // 4096),
+                                       ("record_prefix", cache.pool, per_rec, cache.stride, nrec_pool)):
+        ck = torch.zeros(1, dtype=torch.int32, device=dev)
+        for _ in range(3):
+            B.probe_read(base, per, stride, n, ck)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        reps = 10
+        e0.record()
+        for _ in range(reps):
+            B.probe_read(base, per, stride, n, ck)
+        e1.record()
+        torch.cuda.synchronize()
+        t = e0.elapsed_time(e1) / reps / 1e3
+        res[name] = {"gbs": round(per * n / t / 1e9, 1), "bytes": per * n, "us": round(t * 1e6, 2)}
+        log(f"stream probe {name}: {per * n / 2**30:.2f} GiB in {t * 1e6:.1f} us = {per * n / t / 1e9:.0f} GB/s")
+    del buf
+    torch.cuda.empty_cache()
+    return res
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -349,34 +429,74 @@ def main():
     w = synth.WORKLOADS[args.workload]
     H, Hq, d = w.n_kv_heads, w.n_q_heads, w.head_dim
     n = w.n_seqs
-    log(f"workload {w.name}: B={n} Hq={Hq} Hkv={H} d={d} ctx={w.ctx_min}..{w.ctx}")
+    K = args.steps if args.steps is not None else (w.decode_steps if w.prefill else 20)
+    W = args.warmup
+    cold = bool(args.cold) if args.cold >= 0 else args.workload in (2, 5)
+    log(f"workload {w.name}: B={n} Hq={Hq} Hkv={H} d={d} ctx={w.ctx_min}..{w.ctx}; {K} steps, cold={cold}")
 
-    # ---- setup: thresholds, cache prefill (not timed) ----------------------------
+    # ---- setup: thresholds, cache prefill ----------------------------------------
     kc = synth.calibration_set(w, "k", dev)
     vc = synth.calibration_set(w, "v", dev)
     thr = B.calibrate_thresholds(kc, vc, 0.04, 0.06)
     del kc, vc
-    lens = synth.seq_lengths(w)
-    bt_cpu, nblk = synth.block_table(w, lens)
+    if w.prefill:
+        # the whole context is quantized by one prefill-time call (timed); the decode steps
+        # then append at positions ctx, ctx + 1, ...
+        L0 = torch.full((n,), w.ctx, dtype=torch.int32)
+        bt_cpu, nblk = synth.block_table(w, L0, extra_tokens=max(K, W) + 1)
+        pre = [w.ctx] * n
+        lens = L0 + 1                        # (the layer and chunked-prefill modes append one token)
+    else:
+        lens = synth.seq_lengths(w)          # incl. the token each decode step appends
+        bt_cpu, nblk = synth.block_table(w, lens)
+        pre = [int(L) - 1 for L in lens]
     bt = bt_cpu.to(dev)
-    # (on-demand sparse pages: room for two 256-byte pages per record; only what the COO
-    # streams need is taken)
     cache = B.Cache(nblk, H, d, thr, sparse_pages=2 * nblk * H * 2 if args.paged else 0)
     log(f"pool {cache.pool.numel() / 2**30:.2f} GiB, {nblk} pages")
-    chunk = 16
-    t0 = time.time()
-    for s0 in range(0, n, chunk):
-        ss = list(range(s0, min(n, s0 + chunk)))
-        pre = [int(lens[s]) - 1 for s in ss]
-        k = torch.cat([synth.kv_values_seq(w, "k", s, p, dev) for s, p in zip(ss, pre)])
-        v = torch.cat([synth.kv_values_seq(w, "v", s, p, dev) for s, p in zip(ss, pre)])
-        cu = torch.zeros(len(ss) + 1, dtype=torch.int32)
+    prefill_res = None
+    if w.prefill:
+        k_all = torch.cat([synth.kv_values_seq(w, "k", s, pre[s], dev) for s in range(n)])
+        v_all = torch.cat([synth.kv_values_seq(w, "v", s, pre[s], dev) for s in range(n)])
+        cu = torch.zeros(n + 1, dtype=torch.int32)
         cu[1:] = torch.cumsum(torch.tensor(pre, dtype=torch.int32), 0)
-        B.quantize_kv(cache, k, v, bt[s0:s0 + len(ss)].contiguous(),
-                      torch.zeros(len(ss), dtype=torch.int32, device=dev), cu.to(dev), max(pre))
-        del k, v
-    torch.cuda.synchronize()
-    log(f"prefill-quantized {int(lens.sum()) - n} tokens in {time.time() - t0:.1f}s")
+        cu_d, z = cu.to(dev), torch.zeros(n, dtype=torch.int32, device=dev)
+        B.quantize_kv(cache, k_all, v_all, bt, z, cu_d, max(pre))     # warm-up (same bytes again below)
+        torch.cuda.synchronize()
+        reps = 3
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        for e0, e1 in ev:
+            e0.record()
+            B.quantize_kv(cache, k_all, v_all, bt, z, cu_d, max(pre))
+            e1.record()
+        torch.cuda.synchronize()
+        t_pf = sum(a.elapsed_time(b) for a, b in ev) / reps / 1e3
+        n_vec = sum(pre) * H * 2
+        pfx = outlier_prefix(cache, bt_cpu, n, w.ctx)
+        n_out = int(pfx[:, :, :, w.ctx].sum())
+        in_b = n_vec * d * 2
+        out_b = n_vec * alg_bytes_per_vector(d) + n_out
+        gbs = (in_b + out_b) / t_pf / 1e9
+        prefill_res = {"tokens": sum(pre), "us": round(t_pf * 1e6, 1), "tokens_per_s": round(sum(pre) / t_pf, 1),
+                       "bytes_in": in_b, "bytes_out": out_b,
+                       "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                    "frac": round(gbs / HBM_PEAK_GBS, 4)}}
+        log(f"prefill quantization: {sum(pre)} tokens x {H} heads in {t_pf * 1e6:.1f} us ({gbs:.0f} GB/s)")
+        del k_all, v_all
+        torch.cuda.empty_cache()
+    else:
+        t0 = time.time()
+        chunk = 16
+        for s0 in range(0, n, chunk):
+            ss = list(range(s0, min(n, s0 + chunk)))
+            k = torch.cat([synth.kv_values_seq(w, "k", s, pre[s], dev) for s in ss])
+            v = torch.cat([synth.kv_values_seq(w, "v", s, pre[s], dev) for s in ss])
+            cu = torch.zeros(len(ss) + 1, dtype=torch.int32)
+            cu[1:] = torch.cumsum(torch.tensor([pre[s] for s in ss], dtype=torch.int32), 0)
+            B.quantize_kv(cache, k, v, bt[s0:s0 + len(ss)].contiguous(),
+                          torch.zeros(len(ss), dtype=torch.int32, device=dev), cu.to(dev), max(pre[s] for s in ss))
+            del k, v
+        torch.cuda.synchronize()
+        log(f"cache built: {sum(pre)} tokens (inputs drawn on the GPU) in {time.time() - t0:.1f}s")
     capacity = None
     if args.paged:
         free, overflow = cache.sparse_status()
@@ -394,41 +514,64 @@ def main():
     if args.prefill_chunk:
         return prefill_bench(args, w, cache, bt, lens, dev)
 
-    k_new = synth.new_token_values(w, "k", 0, dev)
-    v_new = synth.new_token_values(w, "v", 0, dev)
-    start = (lens - 1).to(torch.int32).to(dev)
+    # ---- decode steps ----------------------------------------------------------------
+    # step i appends one token per sequence at start_i and attends over lens_i tokens: a
+    # growing context for the prefill workload, the same last position otherwise
+    n_new = max(K, W)
+    if w.prefill:
+        starts = [torch.full((n,), w.ctx + i, dtype=torch.int32, device=dev) for i in range(n_new)]
+        lens_l = [torch.full((n,), w.ctx + i + 1, dtype=torch.int32) for i in range(n_new)]
+        k_new = [synth.new_token_values(w, "k", i, dev) for i in range(n_new)]
+        v_new = [synth.new_token_values(w, "v", i, dev) for i in range(n_new)]
+    else:
+        starts = [(lens - 1).to(torch.int32).to(dev)] * n_new
+        lens_l = [lens] * n_new
+        k_new = [synth.new_token_values(w, "k", 0, dev)] * n_new
+        v_new = [synth.new_token_values(w, "v", 0, dev)] * n_new
+    lens_d = [L.to(dev) for L in lens_l]
     cu1 = torch.arange(n + 1, dtype=torch.int32, device=dev)
     q = synth.queries(w, 0, dev)
-    lens_d = lens.to(dev)
-    max_len = int(lens.max())
+    max_len = max(int(L.max()) for L in lens_l)
     scale = float(np.float32(1.0 / math.sqrt(d)))
     out = torch.empty(n, Hq, d, dtype=torch.float32, device=dev)
     win = max(0, args.window)
     ws_bytes = B.attention_workspace_bytes(n, Hq, H, d, max_len, win)
     ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+    scratch = torch.empty(1 << 30, dtype=torch.uint8, device=dev) if cold else None
 
-    def step(ev=None):
-        B.quantize_kv(cache, k_new, v_new, bt, start, cu1, 1)
+    def step(i, ev=None):
         if ev is not None:
             ev[0].record()
-        B.decode_attention(cache, q, bt, lens_d, max_len, scale, out=out, workspace=ws, window=win)
+        B.quantize_kv(cache, k_new[i], v_new[i], bt, starts[i], cu1, 1)
         if ev is not None:
             ev[1].record()
+        B.decode_attention(cache, q, bt, lens_d[i], max_len, scale, out=out, workspace=ws, window=win)
+        if ev is not None:
+            ev[2].record()
 
-    for _ in range(args.warmup):
-        step()
+    for i in range(W):
+        if cold:
+            scratch.fill_(i & 0xff)
+        step(i)
     torch.cuda.synchronize()
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(args.steps)]
+    evs = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(3)) for _ in range(K)]
     torch.cuda.synchronize()
     t_start = time.perf_counter()
-    for i in range(args.steps):
-        step(evs[i])
+    for i in range(K):
+        if cold:
+            scratch.fill_((i + 7) & 0xff)   # outside the step's events
+        step(i, evs[i])
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
-    attn_ms = [a.elapsed_time(b) for a, b in evs]
-    attn_avg_s = sum(attn_ms) / len(attn_ms) / 1e3
-    log(f"{args.steps} steps in {elapsed * 1e3:.2f} ms; attention avg {attn_avg_s * 1e6:.1f} us")
+    quant_s = [a.elapsed_time(b) / 1e3 for a, b, _ in evs]
+    attn_s = [b.elapsed_time(c) / 1e3 for _, b, c in evs]
+    step_s = sum(quant_s) + sum(attn_s)
+    attn_avg_s = sum(attn_s) / K
+    log(f"{K} steps in {elapsed * 1e3:.2f} ms wall; events: quantize avg {sum(quant_s) / K * 1e6:.1f} us, "
+        f"attention avg {attn_avg_s * 1e6:.1f} us")
+    if cold:
+        del scratch
+        torch.cuda.empty_cache()
 
     if args.copy_probe_mib:
         src = torch.ones(args.copy_probe_mib * 2**20 // 4, dtype=torch.float32, device=dev)
@@ -437,103 +580,138 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    # ---- algorithmic bytes of one attention launch ----------------------------------
-    # per (token, KV head, K|V) vector: d/2 dense + d/64 counts + 12 meta + its COO bytes
-    P = 16
-    nc = d // 64
-    stride = cache.stride
-    rec = cache.pool.view(nblk, H, 2, stride)
-    counts = rec[:, :, :, : P * nc].reshape(nblk, H, 2, P, nc).to(torch.int32).sum(-1)  # [blk,H,2,P]
-    # (only the keys a query sees: with a sliding window, the last `win` of each sequence)
-    valid = torch.zeros(nblk, P, dtype=torch.bool)
-    seen = [min(int(L), win) if win else int(L) for L in lens]
-    n_pages_read = 0
-    for s in range(n):
-        L = int(lens[s])
-        lo = L - seen[s]
-        for pg in range(lo // P, (L + P - 1) // P):
-            t0_, t1_ = max(lo - pg * P, 0), min(P, L - pg * P)
-            valid[int(bt_cpu[s, pg]), t0_:t1_] = True
-            n_pages_read += 1
-    n_out = int((counts * valid.to(dev)[:, None, None, :]).sum())
-    n_vec = sum(seen) * H * 2
-    kv_bytes = n_vec * (d // 2 + nc + 12) + n_out
-    if args.paged:
-        kv_bytes += n_pages_read * H * 2 * 8   # each record's first two sparse page ids
-    aux_bytes = n * Hq * d * (2 + 4) + n_pages_read * 4 + n * 4
-    aux_bytes += 2 * ws_bytes          # split partials: written once, read once by the combine
-    alg_bytes = kv_bytes + aux_bytes
-    achieved = alg_bytes / attn_avg_s / 1e9
+    # ---- algorithmic bytes of the attention launches ---------------------------------
+    prefix = outlier_prefix(cache, bt_cpu, n, max_len)
+    kv_tot, alg_tot, out_tot, vec_tot = 0, 0, 0, 0
+    memo = {}
+    for i in range(K):
+        key = id(lens_l[i])
+        if key not in memo:
+            memo[key] = attention_bytes(cache, prefix, lens_l[i], win, Hq, n)
+        kv_i, alg_i, out_i, vec_i, pages_i = memo[key]
+        kv_tot += kv_i
+        alg_tot += alg_i + (pages_i * H * 2 * 8 if args.paged else 0)   # (paged: each record's first two page ids)
+        out_tot += out_i
+        vec_tot += vec_i
+    achieved = alg_tot / sum(attn_s) / 1e9
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": stored_traffic(w.name) if not (win or args.paged) else None,
-                "bytes_per_launch": alg_bytes, "kernel_us": round(attn_avg_s * 1e6, 2),
-                "outlier_fraction": round(n_out / (n_vec * d), 4)}
+                "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": stored_traffic(w.name) if not (win or args.paged or w.prefill) else None,
+                "bytes_per_launch": int(alg_tot / K), "kv_stream_bytes_per_launch": int(kv_tot / K),
+                "kernel_us": round(attn_avg_s * 1e6, 2),
+                "overhead_bytes_per_launch": {"split_partials_written_and_read": 2 * ws_bytes},
+                "outlier_fraction": round(out_tot / (vec_tot * d), 4)}
+    quant_res = {"us_per_step": round(sum(quant_s) / K * 1e6, 2),
+                 "attention_us_per_step": round(attn_avg_s * 1e6, 2)}
+
+    stream = None
+    if not args.no_stream_probe:
+        stream = stream_probe(cache, dev)
+        stream["attention_frac_of_plain"] = round(achieved / stream["plain_4gib"]["gbs"], 4)
+        stream["attention_frac_of_record_prefix"] = round(achieved / stream["record_prefix"]["gbs"], 4)
 
     # ---- CPU oracle on a bounded sample + sampled parity -------------------------------
     cpu = None
     parity = None
     if not args.no_cpu_baseline:
         import oracle
-        S = min(n, args.cpu_sample_seqs)
+        S = min(n, args.cpu_sample_seqs or (4 if w.prefill else 128))
         sample = list(range(0, n, max(1, n // S)))[:S]
         thr_np = thr.cpu().numpy()
-        lay = oracle.layout(P, d)
-        nb_s = [(int(lens[s]) + P - 1) // P for s in sample]
+        lay = oracle.layout(16, d)
+        last = K - 1
+        L_fin = [int(lens_l[last][s]) for s in sample]
+        nb_s = [(L + 15) // 16 for L in L_fin]
         bt_s = np.zeros((S, max(nb_s)), np.int32)
         off = 0
         for i, nb in enumerate(nb_s):
             bt_s[i, :nb] = np.arange(off, off + nb)
             off += nb
         pool_s = np.zeros(off * H * 2 * lay["stride"], np.uint8)
-        pre = np.array([int(lens[s]) - 1 for s in sample], np.int32)
-        kk = torch.cat([synth.kv_values_seq(w, "k", s, int(p), dev) for s, p in zip(sample, pre)]).cpu().numpy()
-        vv = torch.cat([synth.kv_values_seq(w, "v", s, int(p), dev) for s, p in zip(sample, pre)]).cpu().numpy()
-        cu = np.concatenate([[0], np.cumsum(pre)]).astype(np.int32)
-        oracle.quantize_kv(pool_s, off, P, H, d, thr_np, kk, vv, bt_s, np.zeros(S, np.int32), cu)
+        pre_s = np.array([pre[s] for s in sample], np.int32)
+        kk = torch.cat([synth.kv_values_seq(w, "k", s, int(p), dev) for s, p in zip(sample, pre_s)]).cpu().numpy()
+        vv = torch.cat([synth.kv_values_seq(w, "v", s, int(p), dev) for s, p in zip(sample, pre_s)]).cpu().numpy()
+        cu = np.concatenate([[0], np.cumsum(pre_s)]).astype(np.int32)
+        threads = oracle.max_threads()
+        t0 = time.perf_counter()
+        oracle.quantize_kv(pool_s, off, 16, H, d, thr_np, kk, vv, bt_s, np.zeros(S, np.int32), cu)
+        t_pre = time.perf_counter() - t0
         del kk, vv
-        kn = k_new.cpu().numpy()[sample]
-        vn = v_new.cpu().numpy()[sample]
+        ar = np.arange(S + 1, dtype=np.int32)
+        # decode steps before the last one (the prefill workload's growing context)
+        for i in range(last if w.prefill else 0):
+            oracle.quantize_kv(pool_s, off, 16, H, d, thr_np, k_new[i].cpu().numpy()[sample],
+                               v_new[i].cpu().numpy()[sample], bt_s, starts[i].cpu().numpy()[sample], ar)
+        kn = k_new[last].cpu().numpy()[sample]
+        vn = v_new[last].cpu().numpy()[sample]
+        st_s = starts[last].cpu().numpy()[sample]
         qs = q.cpu().numpy()[sample]
-        lens_s = np.array([int(lens[s]) for s in sample], np.int32)
-        log(f"oracle sample: {S} sequences built; timing one decode step")
+        lens_s = np.array(L_fin, np.int32)
+        log(f"oracle sample: {S} sequences built in {t_pre:.1f} s ({threads} threads); timing one decode step")
+
+        def one_step(idx):
+            oracle.quantize_kv(pool_s, off, 16, H, d, thr_np, kn[idx], vn[idx], bt_s[idx], st_s[idx],
+                               np.arange(len(idx) + 1, dtype=np.int32))
+            return oracle.decode_attention(pool_s, off, 16, H, d, thr_np, qs[idx], bt_s[idx], lens_s[idx], scale,
+                                           window=win)
+
         times = []
         for _ in range(3):   # median of three steps (re-quantizing the same slot is idempotent)
             t0 = time.perf_counter()
-            oracle.quantize_kv(pool_s, off, P, H, d, thr_np, kn, vn, bt_s, pre, np.arange(S + 1, dtype=np.int32))
-            want = oracle.decode_attention(pool_s, off, P, H, d, thr_np, qs, bt_s, lens_s, scale, window=win)
+            want = one_step(np.arange(S))
             times.append(time.perf_counter() - t0)
         cpu_s = sorted(times)[1]
-        cpu = {"value": round(S / cpu_s, 2), "unit": "tokens/s", "cores": oracle.max_threads(),
-               "kind": "oracle",
-               "sample": f"{S} of {n} sequences (full context, all {Hq} heads), one decode step "
-                         f"(quantize + attention), median of 3: {cpu_s:.2f} s"}
+        # one thread, on an eighth of the sample
+        S1 = max(1, S // 8)
+        oracle.set_threads(1)
+        t0 = time.perf_counter()
+        one_step(np.arange(S1))
+        cpu1_s = time.perf_counter() - t0
+        oracle.set_threads(threads)
+        cpu = {"value": round(S / cpu_s, 2), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+               "sample": f"{S} of {n} sequences (context {L_fin[0]}, all {Hq} heads), one decode step "
+                         f"(quantize + attention), median of 3: {cpu_s:.2f} s",
+               "one_thread": {"value": round(S1 / cpu1_s, 3), "unit": "tokens/s", "cores": 1,
+                              "sample": f"{S1} sequences, one decode step: {cpu1_s:.2f} s"}}
+        if w.prefill:
+            cpu["prefill_quantize_tokens_per_s"] = round(int(pre_s.sum()) / t_pre, 1)
         got = out.cpu().numpy()[sample]
         err = np.abs(got.astype(np.float64) - want)
         okm = err <= 2e-3 + 1e-2 * np.abs(want)
         parity = {"seqs": S, "max_abs": float(err.max()), "pass": bool(okm.all())}
-        log(f"oracle {cpu_s:.2f}s, parity max_abs={err.max():.2e} pass={bool(okm.all())}")
+        log(f"oracle {cpu_s:.2f}s ({threads} threads), {cpu1_s:.2f}s for {S1} at 1 thread; "
+            f"parity max_abs={err.max():.2e} pass={bool(okm.all())}")
 
+    value = n * K / (step_s if cold else elapsed)
     res = {
         "metric": "decode-attention tokens/sec + achieved HBM GB/s (% of peak) at batch 256",
-        "value": round(n * args.steps / elapsed, 1),
+        "value": round(value, 1),
         "unit": "tokens/s",
         "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(elapsed / args.steps * 1e3, 4),
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": round((step_s if cold else elapsed) / K * 1e3, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "i8mfma-4limb+f32",
         "data": "synthetic",
         "config": {"workload": f"{w.name}: batch {n}, {Hq} query / {H} KV heads, head_dim {d}, "
-                               f"context {w.ctx_min}..{w.ctx} incl. the new token, 16-token pages, "
-                               f"shuffled block table"
+                               + (f"context {w.ctx} quantized by one prefill call, then {K} decode steps "
+                                  f"(context {w.ctx + 1}..{w.ctx + K})" if w.prefill else
+                                  f"context {w.ctx_min}..{w.ctx} incl. the new token")
+                               + ", 16-token pages, shuffled block table"
                                + (f", sliding window {win}" if win else "")
                                + (", on-demand 256-byte sparse pages" if args.paged else "")
                                + "; step = quantize 1 token/seq + attention",
                    "global_batch": n, "seq_len": max_len, "parallelism": "single GPU"},
+        "timing": ("HIP events per step; a 1 GiB scratch write between steps (outside the events) evicts "
+                   "the 256 MB Infinity Cache" if cold else "wall clock over the steps, back to back")
+                  + f"; wall {elapsed / K * 1e3:.4f} ms/step",
         "roofline": roofline,
+        "step_breakdown": quant_res,
+        "stream_read": stream,
+        **({"prefill_quantize": prefill_res} if prefill_res else {}),
         "cpu_baseline": cpu,
         **({"capacity": capacity} if capacity else {}),
         "parity_sample": parity,

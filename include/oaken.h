@@ -247,6 +247,19 @@ int oaken_prefill_attention(const oaken_cache* cache, const void* q, int32_t n_q
                             int32_t sliding_window, float softmax_scale, float* out, void* workspace,
                             size_t workspace_bytes, void* stream);
 
+/*
+ * Measurement helper: a streaming-read probe, for reading the decode attention's achieved
+ * bandwidth against what plain loads reach on the same device.  Reads the first
+ * bytes_per_record bytes (a multiple of 16, at most 4096) of each of n_records records
+ * spaced record_stride bytes apart (a multiple of 16, >= bytes_per_record) from the
+ * 16-byte aligned device buffer base, and XORs every 32-bit word read into *checksum
+ * (device uint32, which the caller initialises).  A contiguous buffer is read with
+ * record_stride == bytes_per_record.  At most 2^31 - 1 chunks of 16 bytes (32 GiB) per
+ * call.  Asynchronous on stream.
+ */
+int oaken_probe_read(const void* base, int64_t bytes_per_record, int64_t record_stride, int64_t n_records,
+                     uint32_t* checksum, void* stream);
+
 /* Static description of a status code. */
 const char* oaken_status_string(int status);
 

@@ -60,6 +60,8 @@ def _load():
     lib.oaken_ref_decode_attention.restype = i32
     lib.oaken_ref_calibrate.argtypes = [P, P, i32, i32, i32, i32, f32, f32, P]
     lib.oaken_ref_calibrate.restype = i32
+    lib.oaken_ref_set_threads.argtypes = [i32]
+    lib.oaken_ref_set_threads.restype = None
     lib.oaken_ref_max_threads.argtypes = []
     lib.oaken_ref_max_threads.restype = i32
     lib.oaken_ref_variant_info.argtypes = [i32, P]
@@ -108,6 +110,11 @@ def layout(P: int, d: int) -> dict:
 
 def max_threads() -> int:
     return int(_load().oaken_ref_max_threads())
+
+
+def set_threads(n: int) -> None:
+    """Thread count of the oracle's parallel loops (for timing at 1 and at all cores)."""
+    _load().oaken_ref_set_threads(int(n))
 
 
 def quantize_vector(x, thr):

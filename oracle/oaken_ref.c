@@ -678,6 +678,17 @@ int oaken_ref_variant_dequantize(int variant, const uint8_t* nib, const uint8_t*
     return bad ? -1 : 0;
 }
 
+/* Thread count of the parallel loops (timing of the CPU baseline at 1 and at all
+   cores); n <= 0 leaves it unchanged. */
+void oaken_ref_set_threads(int n)
+{
+#ifdef _OPENMP
+    if (n > 0) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 int oaken_ref_max_threads(void)
 {
 #ifdef _OPENMP

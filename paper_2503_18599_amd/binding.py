@@ -91,6 +91,8 @@ def lib():
     L.oaken_variant_quantize.restype = ctypes.c_int
     L.oaken_variant_dequantize.argtypes = [i32, P, P, P, P, i32, i32, i32, P, P, P]
     L.oaken_variant_dequantize.restype = ctypes.c_int
+    L.oaken_probe_read.argtypes = [P, i64, i64, i64, P, P]
+    L.oaken_probe_read.restype = ctypes.c_int
     L.oaken_status_string.argtypes = [ctypes.c_int]
     L.oaken_status_string.restype = ctypes.c_char_p
     L.oaken_last_error.argtypes = []
@@ -283,6 +285,21 @@ def prefill_attention(cache: Cache, q: torch.Tensor, block_table: torch.Tensor, 
         n_seqs, n_tokens, int(max_seq_len), int(window), float(scale), _dev(out, torch.float32, "out"),
         workspace.data_ptr(), ws_bytes, _stream()))
     return out
+
+
+def probe_read(buf: torch.Tensor, bytes_per_record: int, record_stride: int, n_records: int,
+               checksum: torch.Tensor | None = None) -> torch.Tensor:
+    """Streaming-read probe over a uint8 device buffer: XOR of every 32-bit word of the
+    first bytes_per_record bytes of each record (int32 device scalar)."""
+    if buf.dtype != torch.uint8 or buf.device.type != "cuda":
+        raise TypeError("buf must be a uint8 GPU tensor")
+    if (n_records - 1) * record_stride + bytes_per_record > buf.numel():
+        raise ValueError("records extend past the buffer")
+    if checksum is None:
+        checksum = torch.zeros(1, dtype=torch.int32, device=buf.device)
+    _check(lib().oaken_probe_read(buf.data_ptr(), int(bytes_per_record), int(record_stride), int(n_records),
+                                  _dev(checksum, torch.int32, "checksum"), _stream()))
+    return checksum
 
 
 # --------------------------------------------------------------------------- #

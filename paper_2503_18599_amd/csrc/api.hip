@@ -413,6 +413,24 @@ int oaken_variant_dequantize(int32_t variant, const void* nib, const void* coo, 
                       "variant dequantize launch");
 }
 
+int oaken_probe_read(const void* base, int64_t bytes_per_record, int64_t record_stride, int64_t n_records,
+                     uint32_t* checksum, void* stream) {
+    if (!base || !checksum) return fail(OAKEN_ERR_INVALID_ARG, "probe base or checksum NULL");
+    if (bytes_per_record <= 0 || bytes_per_record > 4096 || bytes_per_record % 16 != 0)
+        return fail(OAKEN_ERR_INVALID_ARG, "bytes_per_record must be a multiple of 16 in [16, 4096]");
+    if (record_stride < bytes_per_record || record_stride % 16 != 0 || n_records <= 0)
+        return fail(OAKEN_ERR_INVALID_ARG, "record_stride must be a multiple of 16 >= bytes_per_record, n_records > 0");
+    if (reinterpret_cast<uintptr_t>(base) % 16 != 0) return fail(OAKEN_ERR_INVALID_ARG, "probe base not 16-byte aligned");
+    oaken::ProbeArgs a{};
+    a.base = static_cast<const uint8_t*>(base);
+    a.record_stride = record_stride;
+    a.n_records = n_records;
+    a.chunks = (int32_t)(bytes_per_record / 16);
+    a.checksum = checksum;
+    if (!oaken::prepare_probe(a)) return fail(OAKEN_ERR_INVALID_ARG, "probe reads 2^31 or more 16-byte chunks");
+    return hip_status(oaken::launch_probe_read(a, static_cast<hipStream_t>(stream)), "probe launch");
+}
+
 const char* oaken_status_string(int status) {
     switch (status) {
         case OAKEN_OK: return "ok";

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
+
 namespace oaken {
 
 constexpr int kPage = 16;         // tokens per page (block_size)
@@ -121,6 +123,17 @@ hipError_t launch_calibrate(const CalibArgs& a, hipStream_t st);
 hipError_t launch_attention(const AttnArgs& a, int d, hipStream_t st);
 hipError_t launch_token_map(const int32_t* cu_tokens, const int32_t* start_pos, int n_seqs, int n_tokens,
                             int32_t* tok_seq, int32_t* tok_pos, hipStream_t st);
+
+// Streaming-read probe (probe.hip).
+struct ProbeArgs {
+    const uint8_t* base;
+    int64_t record_stride, n_records;
+    int32_t chunks;               // 16-byte chunks read from the start of each record (<= 256)
+    uint32_t* checksum;           // XOR of every 32-bit word read
+    uint32_t total_chunks, magic, shift;   // set by prepare_probe
+};
+bool prepare_probe(ProbeArgs& a);   // false: more than 2^31 - 1 chunks
+hipError_t launch_probe_read(const ProbeArgs& a, hipStream_t st);
 
 // Group-count variants of the quantizer (variants.hip).
 struct VariantInfo {

@@ -100,3 +100,35 @@ def test_calibrate_validation(L):
     assert f(1, 1, 1, 8, 1, 64, float("nan"), 0.0, 1, 1, 1 << 20, None) == 1
     assert f(1, 1, 2, 8, 1, 64, 0.04, 0.06, 1, 1, 4, None) == 3
     assert L.oaken_calibrate_workspace_bytes(2, 1) == 2 * 1 * 2 * 3 * 4
+
+
+def test_probe_validation(L):
+    f = L.oaken_probe_read
+    assert f(None, 16, 16, 1, 0x1000, None) == 1
+    assert f(0x1000, 16, 16, 1, None, None) == 1
+    assert f(0x1000, 24, 32, 1, 0x2000, None) == 1        # not a multiple of 16
+    assert f(0x1000, 8192, 8192, 1, 0x2000, None) == 1    # more than 4 KiB per record
+    assert f(0x1000, 32, 16, 1, 0x2000, None) == 1        # stride shorter than the record
+    assert f(0x1000, 16, 16, 0, 0x2000, None) == 1
+    assert f(0x1008, 16, 16, 1, 0x2000, None) == 1        # base not 16-byte aligned
+    assert b"aligned" in L.oaken_last_error()
+
+
+def test_probe_chunk_limit(L):
+    # 2^31 chunks of 16 bytes are beyond one call
+    assert L.oaken_probe_read(0x1000, 4096, 4096, 1 << 23, 0x2000, None) == 1
+
+
+def test_probe_record_division_rule():
+    """The probe finds a chunk's record as (j * magic) >> (31 + l), l = ceil(log2 c),
+    magic = ceil(2^(31 + l) / c): equal to j // c for every 31-bit j (checked at the ends
+    of the range and on random values) and for every record length c of 1..256 chunks."""
+    import random
+    rng = random.Random(7)
+    for c in range(1, 257):
+        l = (c - 1).bit_length()
+        s = 31 + l
+        m = ((1 << s) + c - 1) // c
+        assert m < (1 << 32)
+        for j in [0, 1, c - 1, c, c + 1, (1 << 31) - 1, (1 << 31) - 2] + [rng.randrange(1 << 31) for _ in range(300)]:
+            assert (j * m) >> s == j // c, (c, j)
