@@ -248,6 +248,27 @@ int oaken_prefill_attention(const oaken_cache* cache, const void* q, int32_t n_q
                             size_t workspace_bytes, void* stream);
 
 /*
+ * Decode attention without allocation, for callers that cannot allocate device memory:
+ * code under HIP graph capture, tight serving loops, harnesses that forbid allocation.
+ * Same computation and arguments as oaken_decode_attention_window, minus the workspace:
+ * the split partials live in a scratch array that the library holds in static device
+ * memory on each GPU it runs on (OAKEN_NOALLOC_SCRATCH_BYTES per GPU, kept until the
+ * process ends; its address is looked up once per device on the first call there).
+ * The call allocates nothing.  Sizes whose partials,
+ * oaken_attention_workspace_bytes_window(...), exceed OAKEN_NOALLOC_SCRATCH_BYTES are
+ * rejected with OAKEN_ERR_WORKSPACE before anything is launched.  Every call on one GPU
+ * shares that GPU's scratch and leaves its partials there: calls that overlap on one GPU
+ * (other streams, other host threads) race, and the caller must order them.  Nothing in
+ * the scratch needs clearing: a call writes every partial it reads.
+ */
+#define OAKEN_NOALLOC_SCRATCH_BYTES (32u << 20)
+
+int oaken_decode_attention_noalloc(const oaken_cache* cache, const void* q, int32_t n_q_heads,
+                                   const int32_t* block_table, int32_t max_blocks_per_seq,
+                                   const int32_t* seq_lens, int32_t n_seqs, int32_t max_seq_len,
+                                   int32_t sliding_window, float softmax_scale, float* out, void* stream);
+
+/*
  * Measurement helper: a streaming-read probe, for reading the decode attention's achieved
  * bandwidth against what plain loads reach on the same device.  Reads the first
  * bytes_per_record bytes (a multiple of 16, at most 4096) of each of n_records records

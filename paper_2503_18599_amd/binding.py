@@ -91,6 +91,9 @@ def lib():
     L.oaken_variant_quantize.restype = ctypes.c_int
     L.oaken_variant_dequantize.argtypes = [i32, P, P, P, P, i32, i32, i32, P, P, P]
     L.oaken_variant_dequantize.restype = ctypes.c_int
+    L.oaken_decode_attention_noalloc.argtypes = [ctypes.POINTER(_CacheStruct), P, i32, P, i32, P, i32, i32, i32,
+                                                 f32, P, P]
+    L.oaken_decode_attention_noalloc.restype = ctypes.c_int
     L.oaken_probe_read.argtypes = [P, i64, i64, i64, P, P]
     L.oaken_probe_read.restype = ctypes.c_int
     L.oaken_status_string.argtypes = [ctypes.c_int]
@@ -260,6 +263,22 @@ def decode_attention(cache: Cache, q: torch.Tensor, block_table: torch.Tensor, s
             cache.struct, _dev(q, torch.float16, "q"), Hq, _dev(block_table, torch.int32, "block_table"),
             block_table.shape[1], _dev(seq_lens, torch.int32, "seq_lens"), n_seqs, int(max_seq_len),
             float(scale), _dev(out, torch.float32, "out"), ws_ptr, ws_bytes, _stream()))
+    return out
+
+
+def decode_attention_noalloc(cache: Cache, q: torch.Tensor, block_table: torch.Tensor, seq_lens: torch.Tensor,
+                             max_seq_len: int, scale: float, out: torch.Tensor, window: int = 0) -> torch.Tensor:
+    """decode_attention with the split partials in the library's static scratch: the call
+    allocates nothing (the caller passes `out`)."""
+    n_seqs, Hq, d = q.shape
+    if d != cache.head_dim or seq_lens.numel() != n_seqs or block_table.shape[0] != n_seqs:
+        raise ValueError("q / seq_lens / block_table shapes disagree")
+    if tuple(out.shape) != (n_seqs, Hq, d):
+        raise ValueError("out must be [n_seqs][n_q_heads][head_dim]")
+    _check(lib().oaken_decode_attention_noalloc(
+        cache.struct, _dev(q, torch.float16, "q"), Hq, _dev(block_table, torch.int32, "block_table"),
+        block_table.shape[1], _dev(seq_lens, torch.int32, "seq_lens"), n_seqs, int(max_seq_len), int(window),
+        float(scale), _dev(out, torch.float32, "out"), _stream()))
     return out
 
 

@@ -8,8 +8,18 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
+
+// Split partials of oaken_decode_attention_noalloc: static device memory, one copy per
+// GPU.  In host code `scratch` only stands for the symbol: its device address comes from
+// hipGetSymbolAddress, once per device, and only that address is passed to kernels.
+static __device__ __align__(256) uint8_t scratch[OAKEN_NOALLOC_SCRATCH_BYTES];
 
 namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
 
 thread_local char g_err[512] = "";
 
@@ -134,6 +144,28 @@ int attention_rows(const oaken_cache* cache, const void* q, int32_t n_q_heads, c
 }
 
 size_t round_up_sz(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// This device's scratch address (looked up on the device's first call); nullptr on error.
+void* scratch_address(int& err_status) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+        err_status = fail(OAKEN_ERR_HIP, "no usable current device for the scratch (%s)",
+                          e != hipSuccess ? hipGetErrorString(e) : "device index out of range");
+        return nullptr;
+    }
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p) {
+            err_status = fail(OAKEN_ERR_HIP, "scratch symbol lookup: %s", hipGetErrorString(e));
+            return nullptr;
+        }
+        g_scratch_ptr[dev] = p;
+    }
+    return g_scratch_ptr[dev];
+}
 
 }  // namespace
 
@@ -311,6 +343,27 @@ int oaken_decode_attention_window(const oaken_cache* cache, const void* q, int32
     if (!seq_lens) return fail(OAKEN_ERR_INVALID_ARG, "a device array argument is NULL");
     return attention_rows(cache, q, n_q_heads, block_table, max_blocks_per_seq, seq_lens, nullptr, nullptr, n_seqs,
                           max_seq_len, sliding_window, softmax_scale, out, workspace, workspace_bytes, stream);
+}
+
+int oaken_decode_attention_noalloc(const oaken_cache* cache, const void* q, int32_t n_q_heads,
+                                   const int32_t* block_table, int32_t max_blocks_per_seq,
+                                   const int32_t* seq_lens, int32_t n_seqs, int32_t max_seq_len,
+                                   int32_t sliding_window, float softmax_scale, float* out, void* stream) {
+    if (!seq_lens) return fail(OAKEN_ERR_INVALID_ARG, "a device array argument is NULL");
+    if (!cache) return fail(OAKEN_ERR_INVALID_ARG, "cache is NULL");
+    const size_t need = oaken_attention_workspace_bytes_window(n_seqs, n_q_heads, cache->n_kv_heads, cache->head_dim,
+                                                               max_seq_len, sliding_window);
+    if (need > (size_t)OAKEN_NOALLOC_SCRATCH_BYTES)
+        return fail(OAKEN_ERR_WORKSPACE, "split partials need %zu bytes, more than the %u-byte scratch", need,
+                    (unsigned)OAKEN_NOALLOC_SCRATCH_BYTES);
+    void* ws = nullptr;
+    if (need > 0) {
+        int st = OAKEN_OK;
+        ws = scratch_address(st);
+        if (!ws) return st;
+    }
+    return attention_rows(cache, q, n_q_heads, block_table, max_blocks_per_seq, seq_lens, nullptr, nullptr, n_seqs,
+                          max_seq_len, sliding_window, softmax_scale, out, ws, need, stream);
 }
 
 size_t oaken_prefill_attention_workspace_bytes(int32_t n_tokens, int32_t n_q_heads, int32_t n_kv_heads,
