@@ -243,11 +243,14 @@ struct Smem {
     __device__ float (&oc())[G][D] { return *reinterpret_cast<float (*)[G][D]>(tw_); }
 };
 
-// Wave-uniform description of a group of consecutive pages of one sequence.
+// A group of consecutive pages of one sequence: wave-uniform record pointers and valid
+// slots of its pages, and for each lane those of its own page (lane >> 4).
 struct Grp {
     const uint8_t* base[GRP];   // the page's record, or a valid stand-in record when absent
     int nval[GRP];              // valid slots per page (0 when absent or outside the range)
     int npg;
+    const uint8_t* mine;        // the record of the lane's page
+    int nv;                     // its valid slots
 };
 
 // The range's pages, one per lane (lane i: page p_begin + i; a range spans at most 32
@@ -270,7 +273,10 @@ __device__ __forceinline__ PageLanes page_lanes(const AttnArgs& a, const int32_t
 }
 
 // Group of pages g0 .. g0 + 3 of the range; `rec` is the pool plus `which` record strides.
-__device__ __forceinline__ Grp make_group(const PageLanes& pl, const uint8_t* rec, int p_begin, int g0, int p_end) {
+// Each lane takes its own page's entries from the page table by a lane permute (one LDS
+// crossbar read each), so per-page loads need no selection among the group's pointers.
+__device__ __forceinline__ Grp make_group(const PageLanes& pl, const uint8_t* rec, int p_begin, int g0, int p_end,
+                                          int lane) {
     Grp gr;
     gr.npg = max(0, min(GRP, p_end - g0));
 #pragma unroll
@@ -281,38 +287,41 @@ __device__ __forceinline__ Grp make_group(const PageLanes& pl, const uint8_t* re
         gr.base[pg] = rec + off;
         gr.nval[pg] = __builtin_amdgcn_readlane(pl.nval, li);
     }
+    const int src = (g0 - p_begin + (lane >> 4)) * 4;   // (a lane index below 64: byte address)
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_ds_bpermute(src, (int)pl.off_lo);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_ds_bpermute(src, (int)pl.off_hi);
+    gr.mine = rec + (((uint64_t)hi << 32) | lo);
+    gr.nv = __builtin_amdgcn_ds_bpermute(src, pl.nval);
     return gr;
 }
 
-template <typename T>
-__device__ __forceinline__ T pick4(int i, T a0, T a1, T a2, T a3) {
-    return i == 0 ? a0 : i == 1 ? a1 : i == 2 ? a2 : a3;
-}
 
 // Global loads are issued unconditionally, so the compiler never has to merge a loaded
 // and a default value (which would make it wait for the load right away and defeat the
 // prefetch).  Missing pages read a valid stand-in record whose bytes are never used:
-// every consumer masks by the page's valid-slot count.  A lane's page is a fixed lane
-// range, so its base pointer is a branch-free select of the group's uniform pointers.
+// every consumer masks by the page's valid-slot count.
 
-// One 16-byte chunk of the group's COO counts: lane l < 8 reads chunk l & 1 of page
-// l >> 1; the other lanes re-read the first chunk.
+// One 16-byte chunk of the group's COO counts: lanes 16 p and 16 p + 1 read the two chunks
+// of page p (the page's other lanes read the same bytes again).
 __device__ __forceinline__ uint4 count_chunk(const Grp& gr, int lane) {
-    const int l = lane < 2 * GRP ? lane : 0;
-    return ld16(pick4(l >> 1, gr.base[0], gr.base[1], gr.base[2], gr.base[3]) + (uint32_t)(l & 1) * 16u);
+    return ld16(gr.mine + (uint32_t)(lane & 1) * 16u);
+}
+// Stage the counts read by count_chunk into the head buffer.
+template <typename S_>
+__device__ __forceinline__ void stage_counts(S_& S, const uint4& hreg, int lane) {
+    if ((lane & 15) < 2) *reinterpret_cast<uint4*>(&S.head[lane >> 4][16 * (lane & 1)]) = hreg;
 }
 
 // With on-demand sparse pages: the first two entries of the sparse page table of the
 // lane's page (lane >> 4), which hold the bytes a staged page can use.
 __device__ __forceinline__ int2 page_tab(const Grp& gr, int lane) {
-    return *reinterpret_cast<const int2*>(pick4(lane >> 4, gr.base[0], gr.base[1], gr.base[2], gr.base[3]) + LY.sparse);
+    return *reinterpret_cast<const int2*>(gr.mine + LY.sparse);
 }
 
 // The metadata of the lane's token (lane = 16 * page + slot).  Stays in registers until
 // the group's token constants are formed.
 __device__ __forceinline__ Meta meta_words(const Grp& gr, int lane) {
-    const uint8_t* r = pick4(lane >> 4, gr.base[0], gr.base[1], gr.base[2], gr.base[3]);
-    const uint32_t* m = reinterpret_cast<const uint32_t*>(r + LY.meta + 12 * (lane & 15));
+    const uint32_t* m = reinterpret_cast<const uint32_t*>(gr.mine + LY.meta + 12 * (lane & 15));
     return Meta{m[0], m[1], m[2]};
 }
 
@@ -335,7 +344,7 @@ __device__ __forceinline__ Run unpack_run(uint32_t x) {
 template <int G>
 __device__ __forceinline__ int group_layout(Smem<G>& S, const Grp& gr, int lane, bool& fits, Run& run) {
     const int pg = lane >> 4, t = lane & 15;
-    const int nv = pick4(pg, gr.nval[0], gr.nval[1], gr.nval[2], gr.nval[3]);
+    const int nv = gr.nv;
     const int c0 = (t < nv) ? (int)S.head[pg][2 * t] : 0;
     const int c1 = (t < nv) ? (int)S.head[pg][2 * t + 1] : 0;
     const int tot = c0 + c1;
@@ -370,17 +379,16 @@ __device__ __forceinline__ void sparse_chunks(const AttnArgs& a, const Grp& gr, 
         r0 = ld16(p0 + ((int)o0 < used ? o0 : 0u));
         r1 = ld16((int)o1 < used ? p1 + o0 : p0);
     } else {
-        const uint8_t* r = pick4(lane >> 4, gr.base[0], gr.base[1], gr.base[2], gr.base[3]);
-        r0 = ld16(r + LY.sparse + ((int)o0 < used ? o0 : 0u));
-        r1 = ld16(r + LY.sparse + ((int)o1 < used ? o1 : 0u));
+        r0 = ld16(gr.mine + LY.sparse + ((int)o0 < used ? o0 : 0u));
+        r1 = ld16(gr.mine + LY.sparse + ((int)o1 < used ? o1 : 0u));
     }
 }
 
-// COO byte `off` of page pg's stream, read from HBM (groups whose pages exceed their
+// COO byte `off` of the lane's page stream, read from HBM (groups whose pages exceed their
 // staging slot).
 template <bool PG>
-__device__ __forceinline__ uint32_t coo_byte(const AttnArgs& a, const Grp& gr, int pg, int off) {
-    const uint8_t* r = pick4(pg, gr.base[0], gr.base[1], gr.base[2], gr.base[3]);
+__device__ __forceinline__ uint32_t coo_byte(const AttnArgs& a, const Grp& gr, int off) {
+    const uint8_t* r = gr.mine;
     if constexpr (PG) {
         const int32_t entry = reinterpret_cast<const int32_t*>(r + LY.sparse)[off / kSparsePage];
         return sparse_page(a, entry)[off % kSparsePage];
@@ -561,12 +569,12 @@ __device__ __forceinline__ void key_corrections(Smem<G>& S, const AttnArgs& a, f
         }
     } else {
         for (int kk = 0; kk < r.cnt; ++kk) {
-            const uint32_t b = coo_byte<PG>(a, gr, pg, r.st + kk);
+            const uint32_t b = coo_byte<PG>(a, gr, r.st + kk);
             const uint32_t ch = (b & 63u) | (kk >= r.c0 ? 64u : 0u);
             entry(ch << QS, (ch >> 3) * 4u, (ch & 7u) * 4u, ((b >> 2) & 0x30u) ^ (swz & 0xffu));
         }
     }
-    const int nv = pick4(pg, gr.nval[0], gr.nval[1], gr.nval[2], gr.nval[3]);
+    const int nv = gr.nv;
     if (t < nv) {
 #pragma unroll
         for (int hd = 0; hd < G; ++hd) sc[hd * cap + tok0 + lane] += scale * corr[hd];
@@ -586,7 +594,7 @@ __device__ __forceinline__ void value_corrections(Smem<G>& S, const AttnArgs& a,
     const uint32_t nsh = (uint32_t)(t & 7) * 4u;
     const uint32_t occ = off_of(S, &S.oci(0, 0));                     // + 4 * channel (+ 4 D * head)
     float pt[G];
-    const int nv = pick4(pg, gr.nval[0], gr.nval[1], gr.nval[2], gr.nval[3]);
+    const int nv = gr.nv;
 #pragma unroll
     for (int hd = 0; hd < G; ++hd) pt[hd] = (G > 1 && t < nv) ? sc[hd * cap + tok0 + lane] : 1.0f;
     auto add = [&](uint32_t x, float delta) {
@@ -649,7 +657,7 @@ __device__ __forceinline__ void value_corrections(Smem<G>& S, const AttnArgs& a,
         }
     } else {
         for (int kk = 0; kk < r.cnt; ++kk) {
-            const uint32_t b = coo_byte<PG>(a, gr, pg, r.st + kk);
+            const uint32_t b = coo_byte<PG>(a, gr, r.st + kk);
             const uint32_t ch = (b & 63u) | (kk >= r.c0 ? 64u : 0u);
             entry(ch * 4u, ((b >> 2) & 0x30u) ^ (swz & 0xffu));
         }
@@ -701,7 +709,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
     }
 
     // the first key group's counts and metadata are needed before anything else
-    Grp gc = make_group(pl, krec, p_begin, p_begin, p_end);
+    Grp gc = make_group(pl, krec, p_begin, p_begin, p_end, lane);
     uint4 hreg = count_chunk(gc, lane);
     int2 tab_c = paged ? page_tab(gc, lane) : int2{0, 0};   // (on-demand sparse pages)
     Meta mreg = meta_words(gc, lane);
@@ -723,7 +731,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         ssum[hd] = a.scale * sum;
         sfix[hd] = ldexpf(a.scale, -(sh + 7));
     }
-    if (lane < 2 * GRP) *reinterpret_cast<uint4*>(&S.head[0][16 * lane]) = hreg;
+    stage_counts(S, hreg, lane);
     wave_sync();
 
     // Key-pass A operand: row = 8*(head%2) + 4*type + limb, type 0 -> sum q u, 1 -> sum q h.
@@ -801,7 +809,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         for (int pg = 0; pg < GRP; ++pg) dreg[pg] = ld16(gc.base[pg] + koff);
         sparse_chunks<PG>(a, gc, tab_c, used, lane, sreg0, sreg1);
     }
-    Grp gn = make_group(pl, krec, p_begin, p_begin + GRP, p_end);
+    Grp gn = make_group(pl, krec, p_begin, p_begin + GRP, p_end, lane);
     hreg = count_chunk(gn, lane);
     int2 tab_n = paged ? page_tab(gn, lane) : int2{0, 0};
     for (int g0 = p_begin; g0 < p_end; g0 += GRP) {
@@ -873,7 +881,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         Grp gnn;
         int2 tab_nn = tab_n;
         {
-            if (lane < 2 * GRP) *reinterpret_cast<uint4*>(&S.head[0][16 * lane]) = hreg;
+            stage_counts(S, hreg, lane);
             wave_sync();
             Run r;
             const int used = group_layout(S, gn, lane, fits_n, r);
@@ -881,7 +889,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
             wave_sync();
             sparse_chunks<PG>(a, gn, tab_n, used, lane, sreg0, sreg1);
             mreg = meta_words(gn, lane);
-            gnn = make_group(pl, krec, p_begin, g0 + 2 * GRP, p_end);
+            gnn = make_group(pl, krec, p_begin, g0 + 2 * GRP, p_end, lane);
             hreg = count_chunk(gnn, lane);
             if constexpr (PG) tab_nn = page_tab(gnn, lane);
         }
@@ -897,7 +905,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
     }
 
     // the first value group's heads go out before the softmax
-    gc = make_group(pl, vrec, p_begin, p_begin, p_end);
+    gc = make_group(pl, vrec, p_begin, p_begin, p_end, lane);
     hreg = count_chunk(gc, lane);
     if constexpr (PG) tab_c = page_tab(gc, lane);
     mreg = meta_words(gc, lane);
@@ -922,7 +930,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         S.oci(hd, lane) = 0;
         S.oci(hd, lane + 64) = 0;
     }
-    if (lane < 2 * GRP) *reinterpret_cast<uint4*>(&S.head[0][16 * lane]) = hreg;
+    stage_counts(S, hreg, lane);
     wave_sync();
 
     // ---- pass 2: values ------------------------------------------------------------
@@ -947,7 +955,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         for (int pg = 0; pg < GRP; ++pg) dreg[pg] = ld16(gc.base[pg] + voff);
         sparse_chunks<PG>(a, gc, tab_c, used, lane, sreg0, sreg1);
     }
-    gn = make_group(pl, vrec, p_begin, p_begin + GRP, p_end);
+    gn = make_group(pl, vrec, p_begin, p_begin + GRP, p_end, lane);
     hreg = count_chunk(gn, lane);
     if constexpr (PG) tab_n = page_tab(gn, lane);
     for (int g0 = p_begin; g0 < p_end; g0 += GRP) {
@@ -968,7 +976,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         int fsh;
         {
             const int pg = lane >> 4, t = lane & 15;
-            const int nv = pick4(pg, gc.nval[0], gc.nval[1], gc.nval[2], gc.nval[3]);
+            const int nv = gc.nv;
             const bool vt = t < nv;
             const Tok T = token_consts(mreg, tv);
             float p0 = 0.0f, cx[G], gx[G], mx = 0.0f;
@@ -1020,7 +1028,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         Grp gnn;
         int2 tab_nn = tab_n;
         {
-            if (lane < 2 * GRP) *reinterpret_cast<uint4*>(&S.head[0][16 * lane]) = hreg;
+            stage_counts(S, hreg, lane);
             wave_sync();
             Run r;
             const int used = group_layout(S, gn, lane, fits_n, r);
@@ -1028,7 +1036,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
             wave_sync();
             sparse_chunks<PG>(a, gn, tab_n, used, lane, sreg0, sreg1);
             mreg = meta_words(gn, lane);
-            gnn = make_group(pl, vrec, p_begin, g0 + 2 * GRP, p_end);
+            gnn = make_group(pl, vrec, p_begin, g0 + 2 * GRP, p_end, lane);
             hreg = count_chunk(gnn, lane);
             if constexpr (PG) tab_nn = page_tab(gnn, lane);
         }
