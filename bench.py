@@ -283,10 +283,11 @@ def variant_sweep(args):
                       "variants": rows}), flush=True)
 
 
-def prefill_bench(args, w, cache, bt, lens, dev):
+def prefill_bench(args, w, cache, bt, lens, dev, bt_cpu):
     """Chunked-prefill attention: the last C cached tokens of every sequence attend causally
-    over their prefixes (each query token reads its own prefix; the query heads of a KV
-    head share the reads)."""
+    over their prefixes.  A row block (up to 64 rows of query token x query head of one KV
+    head) reads each page of its keys once, so the bytes of one pass over every chunk's
+    visible prefix are the algorithmic bytes when a chunk fits one row block."""
     import numpy as np
     import torch
 
@@ -303,31 +304,47 @@ def prefill_bench(args, w, cache, bt, lens, dev):
     max_len = int(lens.max())
     scale = float(np.float32(1.0 / math.sqrt(d)))
     out = torch.empty(n_tok, Hq, d, dtype=torch.float32, device=dev)
-    ws = torch.empty(max(1, int(B.lib().oaken_prefill_attention_workspace_bytes(n_tok, Hq, H, d, max_len, 0))),
+    win = max(0, args.window)
+    ws = torch.empty(max(1, int(B.lib().oaken_prefill_attention_workspace_bytes(n_tok, Hq, H, d, max_len, win))),
                      dtype=torch.uint8, device=dev)
     args_d = (bt, start.to(dev), cu.to(dev), max_len, scale)
     for _ in range(args.warmup):
-        B.prefill_attention(cache, q, *args_d, out=out, workspace=ws)
+        B.prefill_attention(cache, q, *args_d, window=win, out=out, workspace=ws)
     torch.cuda.synchronize()
+    steps = args.steps or 20
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
-    for _ in range(args.steps):
-        B.prefill_attention(cache, q, *args_d, out=out, workspace=ws)
+    for _ in range(steps):
+        B.prefill_attention(cache, q, *args_d, window=win, out=out, workspace=ws)
     e1.record()
     torch.cuda.synchronize()
-    t = e0.elapsed_time(e1) / args.steps / 1e3
-    # bytes streamed: each query token reads (position + 1) keys and values of every KV head
-    pos1 = torch.cat([torch.arange(int(start[s]) + 1, int(cached[s]) + 1) for s in range(n)]).to(torch.int64)
-    vec = 2 * H * int(pos1.sum())
-    kv_bytes = vec * (d // 2 + d // 64 + 12 + 0.1 * d)   # 10 % outliers: one COO byte each
-    log(f"prefill attention: {n_tok} query tokens in {t * 1e6:.1f} us")
+    t = e0.elapsed_time(e1) / steps / 1e3
+    # one pass over each chunk's visible keys: positions [lo, last] of every KV head
+    prefix = outlier_prefix(cache, bt_cpu, n, max_len)
+    tpb = 64 // (Hq // H)                                # query tokens per row block
+    one_pass, passes = 0, 0
+    for s in range(n):
+        last = int(cached[s]) - 1
+        lo = max(0, int(start[s]) + 1 - win) if win else 0
+        if int(clen[s]) == 0:
+            continue
+        vec = (last + 1 - lo) * H * 2
+        one_pass += vec * alg_bytes_per_vector(d) + int((prefix[s, :, :, last + 1] - prefix[s, :, :, lo]).sum())
+        passes += (int(clen[s]) + tpb - 1) // tpb
+    one_pass += n_tok * Hq * d * (2 + 4)
+    gbs = one_pass / t / 1e9
+    log(f"prefill attention: {n_tok} query tokens in {t * 1e6:.1f} us; one pass over the chunks' prefixes "
+        f"{one_pass / 1e9:.3f} GB = {gbs:.0f} GB/s ({passes} row blocks for {n} chunks)")
     res = {"metric": "chunked-prefill attention query tokens/sec", "value": round(n_tok / t, 1), "unit": "tokens/s",
-           "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(t * 1e3, 4),
-           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+           "n_gpus": 1, "steps": steps, "warmup": args.warmup, "ms_per_step": round(t * 1e3, 4),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32-mfma", "data": "synthetic",
            "config": {"workload": f"{w.name}: {n} sequences, chunks of the last {args.prefill_chunk} cached tokens "
-                                  f"({n_tok} query tokens), {Hq}/{H} heads, d {d}, context {w.ctx_min}..{w.ctx}",
+                                  f"({n_tok} query tokens), {Hq}/{H} heads, d {d}, context {w.ctx_min}..{w.ctx}"
+                                  + (f", sliding window {win}" if win else ""),
                       "global_batch": n, "seq_len": max_len, "parallelism": "single GPU"},
-           "kv_read_gbs": round(kv_bytes / t / 1e9, 1)}
+           "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                        "frac": round(gbs / HBM_PEAK_GBS, 4), "bytes_one_pass": one_pass,
+                        "row_blocks_per_chunk": round(passes / max(1, sum(1 for s in range(n) if int(clen[s]) > 0)), 3)}}
     print(json.dumps(res), flush=True)
 
 
@@ -512,7 +529,7 @@ def main():
     if args.layer:
         return layer_bench(args, w, cache, bt, lens, dev)
     if args.prefill_chunk:
-        return prefill_bench(args, w, cache, bt, lens, dev)
+        return prefill_bench(args, w, cache, bt, lens, dev, bt_cpu)
 
     # ---- decode steps ----------------------------------------------------------------
     # step i appends one token per sequence at start_i and attends over lens_i tokens: a

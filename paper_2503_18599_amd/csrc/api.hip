@@ -87,10 +87,10 @@ int hip_status(hipError_t e, const char* what) {
     return fail(OAKEN_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
-// Attention over n_rows query rows: sequences (seq_lens) or prefill tokens (tok_seq/tok_pos).
+// Decode attention over n_rows sequences.
 int attention_rows(const oaken_cache* cache, const void* q, int32_t n_q_heads, const int32_t* block_table,
-                   int32_t max_blocks_per_seq, const int32_t* seq_lens, const int32_t* tok_seq,
-                   const int32_t* tok_pos, int32_t n_rows, int32_t max_seq_len, int32_t sliding_window,
+                   int32_t max_blocks_per_seq, const int32_t* seq_lens, int32_t n_rows, int32_t max_seq_len,
+                   int32_t sliding_window,
                    float softmax_scale, float* out, void* workspace, size_t workspace_bytes, void* stream) {
     int st = check_cache(cache);
     if (st != OAKEN_OK) return st;
@@ -122,8 +122,6 @@ int attention_rows(const oaken_cache* cache, const void* q, int32_t n_q_heads, c
     a.q = static_cast<const uint16_t*>(q);
     a.block_table = block_table;
     a.seq_lens = seq_lens;
-    a.tok_seq = tok_seq;
-    a.tok_pos = tok_pos;
     a.out = out;
     a.partial = static_cast<float*>(workspace);
     a.stride = cache->record_stride;
@@ -341,7 +339,7 @@ int oaken_decode_attention_window(const oaken_cache* cache, const void* q, int32
                                   int32_t sliding_window, float softmax_scale, float* out,
                                   void* workspace, size_t workspace_bytes, void* stream) {
     if (!seq_lens) return fail(OAKEN_ERR_INVALID_ARG, "a device array argument is NULL");
-    return attention_rows(cache, q, n_q_heads, block_table, max_blocks_per_seq, seq_lens, nullptr, nullptr, n_seqs,
+    return attention_rows(cache, q, n_q_heads, block_table, max_blocks_per_seq, seq_lens, n_seqs,
                           max_seq_len, sliding_window, softmax_scale, out, workspace, workspace_bytes, stream);
 }
 
@@ -362,19 +360,33 @@ int oaken_decode_attention_noalloc(const oaken_cache* cache, const void* q, int3
         ws = scratch_address(st);
         if (!ws) return st;
     }
-    return attention_rows(cache, q, n_q_heads, block_table, max_blocks_per_seq, seq_lens, nullptr, nullptr, n_seqs,
+    return attention_rows(cache, q, n_q_heads, block_table, max_blocks_per_seq, seq_lens, n_seqs,
                           max_seq_len, sliding_window, softmax_scale, out, ws, need, stream);
 }
 
+namespace {
+// Prefill workspace: [split partials][row blocks: int2 per query token][row-block count]
+struct PrefillWs {
+    size_t part, blocks, count, total;
+};
+PrefillWs prefill_ws(int32_t n_tokens, int32_t n_q_heads, int32_t head_dim, const oaken::PrefillPlan& p) {
+    PrefillWs w{};
+    w.part = p.n_splits > 1 ? round_up_sz((size_t)n_tokens * n_q_heads * p.n_splits * (head_dim + 2) * sizeof(float), 256)
+                            : 0;
+    w.blocks = round_up_sz((size_t)n_tokens * 2 * sizeof(int32_t), 256);
+    w.count = 256;
+    w.total = w.part + w.blocks + w.count;
+    return w;
+}
+}  // namespace
+
 size_t oaken_prefill_attention_workspace_bytes(int32_t n_tokens, int32_t n_q_heads, int32_t n_kv_heads,
                                                int32_t head_dim, int32_t max_seq_len, int32_t sliding_window) {
-    if (n_tokens <= 0) return 0;
-    const size_t part = oaken_attention_workspace_bytes_window(n_tokens, n_q_heads, n_kv_heads, head_dim,
-                                                               max_seq_len, sliding_window);
-    if (part == 0 && !(n_q_heads > 0 && n_kv_heads > 0 && n_q_heads % n_kv_heads == 0 && supported_dim(head_dim) &&
-                       max_seq_len > 0))
+    if (n_tokens <= 0 || n_q_heads <= 0 || n_kv_heads <= 0 || n_q_heads % n_kv_heads != 0 ||
+        n_q_heads / n_kv_heads > 8 || !supported_dim(head_dim) || max_seq_len <= 0 || sliding_window < 0)
         return 0;
-    return round_up_sz(part, 256) + 2 * round_up_sz((size_t)n_tokens * 4, 256);
+    const oaken::PrefillPlan p = oaken::plan_prefill(n_tokens, n_q_heads, n_kv_heads, max_seq_len, sliding_window);
+    return prefill_ws(n_tokens, n_q_heads, head_dim, p).total;
 }
 
 int oaken_prefill_attention(const oaken_cache* cache, const void* q, int32_t n_q_heads,
@@ -382,27 +394,67 @@ int oaken_prefill_attention(const oaken_cache* cache, const void* q, int32_t n_q
                             const int32_t* cu_tokens, int32_t n_seqs, int32_t n_tokens, int32_t max_seq_len,
                             int32_t sliding_window, float softmax_scale, float* out, void* workspace,
                             size_t workspace_bytes, void* stream) {
-    if (!start_pos || !cu_tokens) return fail(OAKEN_ERR_INVALID_ARG, "a device array argument is NULL");
-    if (n_seqs <= 0 || n_tokens <= 0) return fail(OAKEN_ERR_INVALID_ARG, "n_seqs and n_tokens must be positive");
-    const size_t need = oaken_prefill_attention_workspace_bytes(n_tokens, n_q_heads, cache ? cache->n_kv_heads : 0,
-                                                                cache ? cache->head_dim : 0, max_seq_len,
-                                                                sliding_window);
-    if (need == 0) return fail(OAKEN_ERR_INVALID_ARG, "unsupported sizes");
-    if (!workspace || workspace_bytes < need)
-        return fail(OAKEN_ERR_WORKSPACE, "prefill attention workspace %zu < %zu bytes", workspace_bytes, need);
-    // workspace: [split partials][token -> sequence][token -> position]
-    const size_t part = need - 2 * round_up_sz((size_t)n_tokens * 4, 256);
-    int32_t* tok_seq = reinterpret_cast<int32_t*>(static_cast<uint8_t*>(workspace) + part);
-    int32_t* tok_pos = reinterpret_cast<int32_t*>(static_cast<uint8_t*>(workspace) + part +
-                                                  round_up_sz((size_t)n_tokens * 4, 256));
-    const hipStream_t st = static_cast<hipStream_t>(stream);
-    int rc = check_cache(cache);
-    if (rc != OAKEN_OK) return rc;
-    rc = hip_status(oaken::launch_token_map(cu_tokens, start_pos, n_seqs, n_tokens, tok_seq, tok_pos, st),
-                    "token map launch");
-    if (rc != OAKEN_OK) return rc;
-    return attention_rows(cache, q, n_q_heads, block_table, max_blocks_per_seq, nullptr, tok_seq, tok_pos, n_tokens,
-                          max_seq_len, sliding_window, softmax_scale, out, part ? workspace : nullptr, part, stream);
+    int st = check_cache(cache);
+    if (st != OAKEN_OK) return st;
+    if (!q || !block_table || !start_pos || !cu_tokens || !out)
+        return fail(OAKEN_ERR_INVALID_ARG, "a device array argument is NULL");
+    if (n_seqs <= 0 || n_tokens <= 0 || max_seq_len <= 0 || max_blocks_per_seq <= 0 || n_q_heads <= 0)
+        return fail(OAKEN_ERR_INVALID_ARG, "sizes must be positive");
+    if (n_q_heads % cache->n_kv_heads != 0)
+        return fail(OAKEN_ERR_INVALID_ARG, "n_q_heads %d not a multiple of n_kv_heads %d", n_q_heads,
+                    cache->n_kv_heads);
+    if (n_q_heads / cache->n_kv_heads > 8) return fail(OAKEN_ERR_UNSUPPORTED, "more than 8 query heads per KV head");
+    if ((int64_t)max_blocks_per_seq * oaken::kPage < max_seq_len)
+        return fail(OAKEN_ERR_INVALID_ARG, "block table too narrow for max_seq_len");
+    if (!std::isfinite(softmax_scale)) return fail(OAKEN_ERR_INVALID_ARG, "softmax_scale not finite");
+    if (sliding_window < 0) return fail(OAKEN_ERR_INVALID_ARG, "sliding_window must be >= 0");
+    const oaken::PrefillPlan p = oaken::plan_prefill(n_tokens, n_q_heads, cache->n_kv_heads, max_seq_len,
+                                                     sliding_window);
+    const PrefillWs w = prefill_ws(n_tokens, n_q_heads, cache->head_dim, p);
+    if (!workspace || workspace_bytes < w.total)
+        return fail(OAKEN_ERR_WORKSPACE, "prefill attention workspace %zu < %zu bytes", workspace_bytes, w.total);
+    uint8_t* ws = static_cast<uint8_t*>(workspace);
+    oaken::PrefillArgs a{};
+    a.pool = static_cast<const uint8_t*>(cache->pool);
+    a.thr = cache->thresholds;
+    a.q = static_cast<const uint16_t*>(q);
+    a.block_table = block_table;
+    a.start_pos = start_pos;
+    a.cu_tokens = cu_tokens;
+    a.row_blocks = reinterpret_cast<const int2*>(ws + w.part);
+    a.n_row_blocks = reinterpret_cast<const int32_t*>(ws + w.part + w.blocks);
+    a.out = out;
+    a.partial = w.part ? reinterpret_cast<float*>(ws) : nullptr;
+    a.stride = cache->record_stride;
+    a.num_blocks = cache->num_blocks;
+    a.H = cache->n_kv_heads;
+    a.Hq = n_q_heads;
+    a.max_blocks = max_blocks_per_seq;
+    a.n_seqs = n_seqs;
+    a.n_tokens = n_tokens;
+    a.max_seq_len = max_seq_len;
+    a.tokens_per_block = p.tokens_per_block;
+    // (every row block holds at least one token; a sequence starts a new block)
+    a.max_row_blocks = (int32_t)std::min<int64_t>(n_tokens, (n_tokens + p.tokens_per_block - 1) / p.tokens_per_block +
+                                                                (int64_t)n_seqs);
+    a.pages_per_split = p.pages_per_split;
+    a.n_splits = p.n_splits;
+    a.window = sliding_window;
+    a.scale = softmax_scale;
+    a.spool = static_cast<const uint8_t*>(cache->sparse_pool);
+    a.spages = cache->sparse_pages;
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    int rc = hip_status(oaken::launch_prefill(a, cache->head_dim, reinterpret_cast<int2*>(ws + w.part),
+                                              reinterpret_cast<int32_t*>(ws + w.part + w.blocks), s),
+                        "prefill attention launch");
+    if (rc != OAKEN_OK || p.n_splits == 1) return rc;
+    oaken::AttnArgs c{};
+    c.out = out;
+    c.partial = a.partial;
+    c.Hq = n_q_heads;
+    c.n_seqs = n_tokens;
+    c.n_splits = p.n_splits;
+    return hip_status(oaken::launch_combine(c, cache->head_dim, s), "prefill combine launch");
 }
 
 int oaken_variant_info(int32_t variant, int32_t* out) {

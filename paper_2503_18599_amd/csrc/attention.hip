@@ -99,10 +99,7 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
     const int split = tile.split, h = tile.h, s = tile.s;
     const int G = a.Hq / a.H;
     const int tid = threadIdx.x;
-    // row s: a sequence (decode), or a query token of a prefill chunk
-    const int srow = a.tok_seq ? a.tok_seq[s] : s;
-    int L = a.tok_seq ? a.tok_pos[s] + 1 : a.seq_lens[s];
-    L = max(0, min(L, min(a.max_seq_len, a.max_blocks * kPage)));
+    const int L = max(0, min(a.seq_lens[s], min(a.max_seq_len, a.max_blocks * kPage)));
     const int n_pages = (L + kPage - 1) / kPage;
     // a sliding window hides keys before lo; the ranges start at its first page
     const int lo = (a.window > 0 && L > a.window) ? L - a.window : 0;
@@ -121,7 +118,7 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
 
     // ---- pass 1: scores ---------------------------------------------------------
     for (int p = p_begin; p < p_end; ++p) {
-        const int blk = a.block_table[(int64_t)srow * a.max_blocks + p];
+        const int blk = a.block_table[(int64_t)s * a.max_blocks + p];
         const bool ok = blk >= 0 && blk < a.num_blocks;
         if (ok) stage_record<D>(a.pool + (((int64_t)blk * a.H + h) * 2 + 0) * a.stride, s_rec, s_cls, s_meta);
         const int t = tid / 16, part = tid % 16;
@@ -171,7 +168,7 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
     float o[kMaxG];
     for (int g = 0; g < kMaxG; ++g) o[g] = 0.0f;
     for (int p = p_begin; p < p_end; ++p) {
-        const int blk = a.block_table[(int64_t)srow * a.max_blocks + p];
+        const int blk = a.block_table[(int64_t)s * a.max_blocks + p];
         const bool ok = blk >= 0 && blk < a.num_blocks;
         if (ok) stage_record<D>(a.pool + (((int64_t)blk * a.H + h) * 2 + 1) * a.stride, s_rec, s_cls, s_meta);
         if (ok) {
@@ -230,26 +227,7 @@ __global__ __launch_bounds__(D) void attn_combine_kernel(AttnArgs a) {
     a.out[row * D + j] = (den > 0.0f) ? num / den : 0.0f;
 }
 
-// Prefill chunks: row i of the token list belongs to the sequence s with
-// cu_tokens[s] <= i < cu_tokens[s+1] and sits at position start_pos[s] + i - cu_tokens[s].
-__global__ __launch_bounds__(256) void token_map_kernel(const int32_t* cu_tokens, const int32_t* start_pos,
-                                                        int n_seqs, int n_tokens, int32_t* tok_seq, int32_t* tok_pos) {
-    const int s = blockIdx.x;
-    const int lo = max(0, cu_tokens[s]), hi = min(n_tokens, cu_tokens[s + 1]);
-    for (int i = lo + (int)threadIdx.x; i < hi; i += blockDim.x) {
-        tok_seq[i] = s;
-        tok_pos[i] = start_pos[s] + (i - cu_tokens[s]);
-    }
-}
-
 }  // namespace
-
-hipError_t launch_token_map(const int32_t* cu_tokens, const int32_t* start_pos, int n_seqs, int n_tokens,
-                            int32_t* tok_seq, int32_t* tok_pos, hipStream_t st) {
-    hipLaunchKernelGGL(token_map_kernel, dim3(n_seqs), dim3(256), 0, st, cu_tokens, start_pos, n_seqs, n_tokens,
-                       tok_seq, tok_pos);
-    return hipGetLastError();
-}
 
 SplitPlan plan_splits(int32_t n_seqs, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
                       int32_t max_seq_len) {
@@ -269,6 +247,16 @@ SplitPlan plan_splits(int32_t n_seqs, int32_t n_q_heads, int32_t n_kv_heads, int
     sp.pages_per_split = pps;
     sp.n_splits = (max_pages + pps - 1) / pps;
     return sp;
+}
+
+hipError_t launch_combine(const AttnArgs& a, int d, hipStream_t st) {
+    if (d == 64)
+        hipLaunchKernelGGL(attn_combine_kernel<64>, dim3(a.n_seqs * a.Hq), dim3(64), 0, st, a);
+    else if (d == 128)
+        hipLaunchKernelGGL(attn_combine_kernel<128>, dim3(a.n_seqs * a.Hq), dim3(128), 0, st, a);
+    else
+        return hipErrorInvalidValue;
+    return hipGetLastError();
 }
 
 hipError_t launch_attention(const AttnArgs& a, int d, hipStream_t st) {

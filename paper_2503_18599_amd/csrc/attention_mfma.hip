@@ -673,11 +673,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
     const int lane = threadIdx.x;
     const AttnTile tile = attn_tile(a);
     const int split = tile.split, h = tile.h, s = tile.s;
-    // row s: a sequence (decode), or a query token of a prefill chunk, which sees its
-    // sequence's keys up to its own position
-    const int srow = a.tok_seq ? a.tok_seq[s] : s;
-    const int Ls = a.tok_seq ? a.tok_pos[s] + 1 : a.seq_lens[s];
-    const int L = max(0, min(Ls, min(a.max_seq_len, a.max_blocks * P)));
+    const int L = max(0, min(a.seq_lens[s], min(a.max_seq_len, a.max_blocks * P)));
     const int n_pages = (L + P - 1) / P;
     // a sliding window hides keys before lo; the ranges start at its first page
     const int lo = (a.window > 0 && L > a.window) ? L - a.window : 0;
@@ -695,7 +691,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         }
         return;
     }
-    const int32_t* btab = a.block_table + (int64_t)srow * a.max_blocks;
+    const int32_t* btab = a.block_table + (int64_t)s * a.max_blocks;
     constexpr bool paged = PG;   // on-demand sparse pages
     const PageLanes pl = page_lanes(a, btab, p_begin, p_end, L, h, lane);
     const uint8_t* const krec = a.pool;
@@ -975,7 +971,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         int vsh;   // one fixed-point shift for every head of the group
         int fsh;
         {
-            const int pg = lane >> 4, t = lane & 15;
+            const int t = lane & 15;
             const int nv = gc.nv;
             const bool vt = t < nv;
             const Tok T = token_consts(mreg, tv);

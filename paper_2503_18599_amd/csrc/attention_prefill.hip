@@ -1,0 +1,444 @@
+// Chunked-prefill attention over the quantized cache (the prefill stage also reads the KV
+// cache, Sec. 2.1; the sliding window of Sec. 6.1 applies per query).
+//
+// A workgroup takes a block of up to 64 query rows: consecutive query tokens of one
+// sequence's chunk times the query heads of one KV head.  It reads every page of the
+// keys those rows can see once, whatever the number of rows: each page record is staged
+// in LDS, dequantized into an fp32 tile (middle values from the dense nibbles, then the
+// COO entries overwrite their elements with their true values: the engine's zero-insert
+// and merge of Sec. 5.2), and the tile is contracted with all rows on the matrix cores in
+// fp32 (v_mfma_f32_16x16x4_f32), with an online softmax across the pages.  Long prefixes
+// are split into page ranges whose partials the decode attention's log-sum-exp combine
+// merges.
+//
+// The four waves split the channels: each forms every row's partial scores over a quarter
+// of the key channels (the partials meet in LDS) and, after the softmax (which every wave
+// computes), the outputs of a quarter of the value channels, so the matrix-core work is
+// shared evenly whatever the number of rows.  The next page's record bytes are requested
+// while the current page is processed.  MFMA operand layout (16x16x4, fp32): lane l holds
+// A[l & 15][k] and B[k][l & 15] with k = l >> 4 of each 4-wide step; the result holds rows
+// 4 (l >> 4) .. + 3 of column l & 15.  Contraction indices are assigned so that a lane's
+// operands are contiguous in LDS: step s of lane group g takes channel (d / 16) g + s of
+// the wave's quarter of the scores and token 4 g + s of the value product.  Both products
+// are formed transposed (keys and values as the A operand, queries and probabilities as
+// B), so a query row lives on the four lanes q + 16 g of column q.
+#include "oaken_internal.h"
+
+#include <hip/hip_fp16.h>
+
+namespace oaken {
+namespace {
+
+constexpr int kRowsPerBlock = 64;
+constexpr int kPfThreads = 256;
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float h2f(uint32_t b) { return __half2float(__ushort_as_half((uint16_t)b)); }
+
+__device__ __forceinline__ f4 mfma4(float a, float b, f4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// Maximum and sum over the lane pairs q, q ^ 16 and then q, q ^ 32 (the four lanes q + 16 g
+// hold the four quarters of one query row's scores).  v_permlane16_swap with both operands
+// v returns the even rows' values in one result and the odd rows' in the other, so their
+// combination is the pair's (likewise for the halves and v_permlane32_swap).
+__device__ __forceinline__ float max4(float v) {
+    const int x = __float_as_int(v);
+    const auto a = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+    const int y = __float_as_int(fmaxf(__int_as_float(a[0]), __int_as_float(a[1])));
+    const auto b = __builtin_amdgcn_permlane32_swap(y, y, false, false);
+    return fmaxf(__int_as_float(b[0]), __int_as_float(b[1]));
+}
+__device__ __forceinline__ float sum4(float v) {
+    const int x = __float_as_int(v);
+    const auto a = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+    const int y = __float_as_int(__int_as_float(a[0]) + __int_as_float(a[1]));
+    const auto b = __builtin_amdgcn_permlane32_swap(y, y, false, false);
+    return __int_as_float(b[0]) + __int_as_float(b[1]);
+}
+
+// Offsets of a record's fields and its staging area (the COO stream is staged right after
+// the counts, metadata, dense nibbles and, with on-demand sparse pages, the page table).
+template <int D, bool PG>
+struct PfLayout {
+    static constexpr Layout LY = PG ? make_layout_paged(kPage, D) : make_layout(kPage, D);
+    static constexpr int NC = D / 64;
+    static constexpr int NT = kPage * D / kSparsePage;               // page-table entries
+    static constexpr int PRE = (int)LY.sparse + (PG ? 4 * NT : 0);   // staged prefix bytes
+    static constexpr int CAP = kPage * D;                            // COO capacity
+    static constexpr int STAGE = PRE + CAP;
+};
+
+constexpr int kWaves = kPfThreads / 64;
+constexpr int kMaxRowTiles = kRowsPerBlock / 16;
+
+template <int D, bool PG>
+struct PfSmem {
+    float kt[kPage][D + 4];                          // keys, token-major
+    float vt[D][kPage + 4];                          // values, channel-major
+    f4 sp[kWaves][kMaxRowTiles][64];                 // per wave: partial scores over its channels
+    float tokc[2][kPage][8];                         // per record (K, V) and slot: Min, Delta of
+                                                     // inner, middle, outer
+    int used[2];                                     // COO bytes of each record
+    __align__(16) uint8_t rec[2][PfLayout<D, PG>::STAGE];
+    uint8_t owner[2][PfLayout<D, PG>::CAP];          // per COO byte: its (slot, chunk) bucket
+};
+
+// The record bytes a thread prefetches for the next page: chunk c of record w holds bytes
+// [16 c, 16 c + 16) of the record's prefix, or of its COO stream past the prefix.  Fixed
+// records also take the first WIN stream bytes in the same pass (the stream follows the
+// dense nibbles); with on-demand sparse pages the stream is read once the page table is in.
+template <int D, bool PG>
+struct PfPrefetch {
+    static constexpr int WIN = PG ? 0 : (D == 128 ? 256 : 128);
+    static constexpr int CH = PfLayout<D, PG>::PRE / 16 + WIN / 16;   // chunks per record
+};
+
+template <int D, bool PG>
+__global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(3))) void prefill_kernel(PrefillArgs a) {
+    using PL = PfLayout<D, PG>;
+    using PF = PfPrefetch<D, PG>;
+    constexpr Layout LY = PL::LY;
+    constexpr int NC = PL::NC;
+    constexpr int CPW = D / kWaves;    // channels of each wave (scores and outputs)
+    constexpr int KSW = CPW / 4;       // 4-wide contraction steps of a wave's scores
+    constexpr int NCT = CPW / 16;      // 16-wide output tiles of a wave
+    static_assert(PL::PRE % 16 == 0 && 2 * PF::CH <= kPfThreads, "one prefetch chunk per thread");
+
+    __shared__ PfSmem<D, PG> S;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 4;
+    if ((int)blockIdx.x >= *a.n_row_blocks) return;   // (uniform)
+    const int h = blockIdx.y, split = blockIdx.z;
+    const int2 blk = a.row_blocks[blockIdx.x];
+    const int s = blk.x, i0 = blk.y;
+    const int tok0 = a.cu_tokens[s];
+    const int C = a.cu_tokens[s + 1] - tok0;
+    const int start = a.start_pos[s];
+    const int G = a.Hq / a.H;
+    const int i_end = min(C, i0 + a.tokens_per_block);
+    const int n_rows = max(0, (i_end - i0) * G);
+    const int R = (n_rows + 15) / 16;                 // 16-row tiles
+    const int p_last = start + i_end - 1;
+    const int lo_first = a.window > 0 ? max(0, start + i0 + 1 - a.window) : 0;
+    const int pg_first = lo_first / kPage + split * a.pages_per_split;
+    const int pg_end = min(p_last / kPage + 1, lo_first / kPage + (split + 1) * a.pages_per_split);
+    const float* th = a.thr + h * 8;
+    const float tk[4] = {th[0], th[1], th[2], th[3]}, tv[4] = {th[4], th[5], th[6], th[7]};
+
+    // ---- rows ------------------------------------------------------------------------
+    // Transposed products: scores S^T = K Q^T and outputs O^T = V^T P^T, so that the lanes
+    // holding a query row's scores (column lane & 15 of the result) also hold its
+    // probabilities as the B operand of the value product and its outputs, and the softmax
+    // state of that row.  B operand (queries, scaled): row tile rt, query row lane & 15,
+    // this wave's channels CPW w + KSW g + k.
+    float bq[kMaxRowTiles][KSW];
+#pragma unroll
+    for (int rt = 0; rt < kMaxRowTiles; ++rt) {
+        const int ra = 16 * rt + (lane & 15);
+        const bool ok = ra < n_rows;
+        const int i = i0 + (ok ? ra / G : 0), hd = ok ? ra % G : 0;
+        const uint16_t* qp = a.q + ((int64_t)(tok0 + i) * a.Hq + h * G + hd) * D + CPW * wave + KSW * g;
+#pragma unroll
+        for (int k = 0; k < KSW; ++k) bq[rt][k] = ok ? a.scale * h2f(qp[k]) : 0.0f;
+    }
+    // this lane's query row in each tile, its position and window start
+    int rpos[kMaxRowTiles], rlo[kMaxRowTiles];
+    bool rok[kMaxRowTiles];
+#pragma unroll
+    for (int rt = 0; rt < kMaxRowTiles; ++rt) {
+        const int rc = 16 * rt + (lane & 15);
+        rok[rt] = rc < n_rows;
+        rpos[rt] = start + i0 + (rok[rt] ? rc / G : 0);
+        rlo[rt] = a.window > 0 ? max(0, rpos[rt] + 1 - a.window) : 0;
+    }
+    float m[kMaxRowTiles], l[kMaxRowTiles];
+    f4 o[kMaxRowTiles][NCT];   // O^T: channels CPW w + 16 n + 4 g + r of the lane's query row
+#pragma unroll
+    for (int rt = 0; rt < kMaxRowTiles; ++rt) {
+        m[rt] = -INFINITY;
+        l[rt] = 0.0f;
+#pragma unroll
+        for (int n = 0; n < NCT; ++n) o[rt][n] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+    }
+
+    const int32_t* btab = a.block_table + (int64_t)s * a.max_blocks;
+    auto record = [&](int b, int w) { return a.pool + (((int64_t)b * a.H + h) * 2 + w) * a.stride; };
+    auto valid_block = [&](int b) { return b >= 0 && b < a.num_blocks; };
+    const int pw_ = tid / PF::CH, pc_ = tid % PF::CH;   // this thread's prefetch chunk
+    auto prefetch = [&](int pg) -> uint4 {
+        if (pg >= pg_end || tid >= 2 * PF::CH) return make_uint4(0, 0, 0, 0);
+        const int b = btab[pg];
+        if (!valid_block(b)) return make_uint4(0, 0, 0, 0);
+        return *reinterpret_cast<const uint4*>(record(b, pw_) + 16 * pc_);
+    };
+
+    uint4 cur = prefetch(pg_first);
+    for (int pg = pg_first; pg < pg_end; ++pg) {
+        const int b = btab[pg];
+        // (1) stage this page's prefetched bytes, request the next page's
+        if (tid < 2 * PF::CH) *reinterpret_cast<uint4*>(&S.rec[pw_][16 * pc_]) = cur;
+        cur = prefetch(pg + 1);
+        __syncthreads();
+        if (!valid_block(b)) continue;   // (uniform; a precondition violation reads nothing)
+
+        // (2) wave 0: each record's (slot, chunk) buckets, their stream offsets (a DPP prefix
+        //     sum: K buckets on lanes 0.., V buckets on lanes 32..) and the bucket owning each
+        //     stream byte; wave 1: per-slot dequantization constants
+        if (wave == 0) {
+            const int w = lane >> 5, bk = lane & 31;
+            const int cnt = bk < kPage * NC ? (int)S.rec[w][LY.counts + bk] : 0;
+            int x = cnt;
+            x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false);   // row_shr:1
+            x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false);   // row_shr:2
+            x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false);   // row_shr:4
+            x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false);   // row_shr:8
+            x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);   // row_bcast:15 into rows 1, 3
+            const int st = x - cnt;
+            if (bk == 31) S.used[w] = min(x, PL::CAP);
+            for (int k = 0; k < cnt && st + k < PL::CAP; ++k) S.owner[w][st + k] = (uint8_t)bk;
+        } else if (wave == 1 && lane < 2 * kPage) {
+            const int w = lane / kPage, t = lane % kPage;
+            const uint16_t* mt = reinterpret_cast<const uint16_t*>(S.rec[w] + LY.meta + 12 * t);
+#pragma unroll
+            for (int k = 0; k < 6; ++k) S.tokc[w][t][k] = h2f(mt[k]);
+        }
+        __syncthreads();
+
+        // (3) stream bytes past the prefetched window (and, with on-demand sparse pages, the
+        //     whole stream, through the page table)
+        if (PG || S.used[0] > PF::WIN || S.used[1] > PF::WIN) {
+            const int c0 = PF::WIN / 16;
+            const int nk = max(0, (S.used[0] + 15) / 16 - c0), nv = max(0, (S.used[1] + 15) / 16 - c0);
+            for (int c = tid; c < nk + nv; c += kPfThreads) {
+                const int w = c >= nk, cc = c0 + (c - w * nk);
+                const uint8_t* src;
+                if constexpr (PG) {
+                    const int32_t e = reinterpret_cast<const int32_t*>(S.rec[w] + LY.sparse)[(16 * cc) / kSparsePage] - 1;
+                    src = a.spool + (int64_t)((e >= 0 && e < a.spages) ? e : 0) * kSparsePage + (16 * cc) % kSparsePage;
+                } else {
+                    src = record(b, w) + LY.sparse + 16 * cc;
+                }
+                *reinterpret_cast<uint4*>(&S.rec[w][PL::PRE + 16 * cc]) = *reinterpret_cast<const uint4*>(src);
+            }
+        }
+        // middle reading of every nibble into the tiles
+        {
+            // keys: thread = (slot, 8 channels); dense byte t * d/2 + j/2, low nibble = even j
+            constexpr int GPT = D / 8;
+            if (tid < kPage * GPT) {
+                const int t = tid / GPT, cg = tid % GPT;
+                const uint32_t dw = *reinterpret_cast<const uint32_t*>(&S.rec[0][LY.dense + t * (D / 2) + 4 * cg]);
+                const float mn = S.tokc[0][t][2], dl = S.tokc[0][t][3];
+                float x[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const uint32_t u = (dw >> (4 * e)) & 15u;
+                    const bool hi = u >= 8;
+                    const float mag = mn + (float)(hi ? u - 8 : 7 - u) * dl;
+                    x[e] = hi ? tk[2] + mag : tk[1] - mag;
+                }
+                *reinterpret_cast<float4*>(&S.kt[t][8 * cg]) = make_float4(x[0], x[1], x[2], x[3]);
+                *reinterpret_cast<float4*>(&S.kt[t][8 * cg + 4]) = make_float4(x[4], x[5], x[6], x[7]);
+            }
+            // values: thread = (channel j, 8 slots); dense byte j * 8 + t/2, low nibble = even t
+            if (tid < 2 * D) {
+                const int j = tid >> 1, t0 = 8 * (tid & 1);
+                const uint32_t dw = *reinterpret_cast<const uint32_t*>(&S.rec[1][LY.dense + j * (kPage / 2) + (t0 >> 1)]);
+                float x[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const uint32_t u = (dw >> (4 * e)) & 15u;
+                    const bool hi = u >= 8;
+                    const float mag = S.tokc[1][t0 + e][2] + (float)(hi ? u - 8 : 7 - u) * S.tokc[1][t0 + e][3];
+                    x[e] = hi ? tv[2] + mag : tv[1] - mag;
+                }
+                *reinterpret_cast<float4*>(&S.vt[j][t0]) = make_float4(x[0], x[1], x[2], x[3]);
+                *reinterpret_cast<float4*>(&S.vt[j][t0 + 4]) = make_float4(x[4], x[5], x[6], x[7]);
+            }
+        }
+        __syncthreads();
+
+        // (4) COO entries replace their elements' middle readings by their true values
+        //     (thread = entry of either record's stream)
+        {
+            const int uk = S.used[0], utot = uk + S.used[1];
+            for (int e = tid; e < utot; e += kPfThreads) {
+                const int w = e >= uk, ee = e - w * uk;
+                const uint8_t* r = S.rec[w];
+                const int bk = S.owner[w][ee], t = bk / NC, c = bk % NC;
+                const uint32_t en = r[PL::PRE + ee];
+                const int j = 64 * c + (int)(en & 63u);
+                const uint32_t byte = w ? r[LY.dense + j * (kPage / 2) + (t >> 1)] : r[LY.dense + t * (D / 2) + (j >> 1)];
+                const uint32_t n = (byte >> (4 * (w ? (t & 1) : (j & 1)))) & 15u;
+                const bool side = (en >> 7) != 0, outer = ((en >> 6) & 1u) != 0;
+                const float* thw = w ? tv : tk;
+                const float cf = (float)(side ? n : 15u - n);
+                const float mag = outer ? S.tokc[w][t][4] + cf * S.tokc[w][t][5] : S.tokc[w][t][0] + cf * S.tokc[w][t][1];
+                const float x = outer ? (side ? thw[3] + mag : thw[0] - mag) : (side ? mag : -mag);
+                if (w) S.vt[j][t] = x;
+                else S.kt[t][j] = x;
+            }
+        }
+        __syncthreads();
+
+        // (5) partial scores of every row tile over this wave's channels: lane (g, query
+        //     row q) gets S^T[4 g + r][q] over channels CPW w .. + CPW
+        {
+            const float* krow = &S.kt[lane & 15][CPW * wave + KSW * g];
+            float ka[KSW];
+#pragma unroll
+            for (int k = 0; k < KSW; k += 4) {
+                const float4 v = *reinterpret_cast<const float4*>(krow + k);
+                ka[k] = v.x; ka[k + 1] = v.y; ka[k + 2] = v.z; ka[k + 3] = v.w;
+            }
+#pragma unroll
+            for (int rt = 0; rt < kMaxRowTiles; ++rt) {
+                if (rt >= R) break;
+                f4 sc = f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+                for (int k = 0; k < KSW; ++k) sc = mfma4(ka[k], bq[rt][k], sc);
+                S.sp[wave][rt][lane] = sc;
+            }
+        }
+        __syncthreads();
+
+        // (6) whole scores (the waves' partials summed), online softmax of the lane's query
+        //     row over the page's 16 keys (four here, the other twelve on lanes +-16, +-32),
+        //     then the value product over this wave's output channels
+#pragma unroll
+        for (int rt = 0; rt < kMaxRowTiles; ++rt) {
+            if (rt >= R) break;
+            f4 sc = S.sp[0][rt][lane];
+#pragma unroll
+            for (int w = 1; w < kWaves; ++w) sc += S.sp[w][rt][lane];
+            float v[4];
+            float mx = -INFINITY;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int kp = pg * kPage + 4 * g + r;   // key position
+                const bool vis = rok[rt] && kp <= rpos[rt] && kp >= rlo[rt];
+                v[r] = vis ? sc[r] : -INFINITY;
+                mx = fmaxf(mx, v[r]);
+            }
+            mx = max4(mx);
+            const float mn = fmaxf(m[rt], mx);
+            const float alpha = (mn == -INFINITY) ? 1.0f : __expf(m[rt] - mn);
+            float p[4], ps = 0.0f;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                p[r] = (v[r] == -INFINITY) ? 0.0f : __expf(v[r] - mn);
+                ps += p[r];
+            }
+            ps = sum4(ps);
+            l[rt] = l[rt] * alpha + ps;
+            m[rt] = mn;
+            // O^T += V^T P^T: A = the value tile's channels (row) x tokens 4 g + s, B = this
+            // lane's probabilities
+#pragma unroll
+            for (int n = 0; n < NCT; ++n) {
+                o[rt][n] *= alpha;
+                const float4 va = *reinterpret_cast<const float4*>(&S.vt[CPW * wave + 16 * n + (lane & 15)][4 * g]);
+                o[rt][n] = mfma4(va.x, p[0], o[rt][n]);
+                o[rt][n] = mfma4(va.y, p[1], o[rt][n]);
+                o[rt][n] = mfma4(va.z, p[2], o[rt][n]);
+                o[rt][n] = mfma4(va.w, p[3], o[rt][n]);
+            }
+        }
+        // (the next page's staging and tiles wait at its first barrier for every wave)
+    }
+
+    // ---- outputs (this wave's channels), or this range's partials ------------------------
+#pragma unroll
+    for (int rt = 0; rt < kMaxRowTiles; ++rt) {
+        if (rt >= R || !rok[rt]) continue;
+        const int rc = 16 * rt + (lane & 15);
+        const int64_t row = (int64_t)(tok0 + i0 + rc / G) * a.Hq + h * G + rc % G;
+        if (a.n_splits == 1) {
+            const float inv = l[rt] > 0.0f ? 1.0f / l[rt] : 0.0f;
+#pragma unroll
+            for (int n = 0; n < NCT; ++n)
+                *reinterpret_cast<float4*>(&a.out[row * D + CPW * wave + 16 * n + 4 * g]) =
+                    make_float4(o[rt][n][0] * inv, o[rt][n][1] * inv, o[rt][n][2] * inv, o[rt][n][3] * inv);
+        } else {
+            float* pp = a.partial + (row * a.n_splits + split) * (D + 2);
+#pragma unroll
+            for (int n = 0; n < NCT; ++n)
+                for (int r = 0; r < 4; ++r) pp[CPW * wave + 16 * n + 4 * g + r] = o[rt][n][r];
+            if (wave == 0 && g == 0) {
+                pp[D] = m[rt];
+                pp[D + 1] = l[rt];
+            }
+        }
+    }
+}
+
+// Row blocks: sequence s's chunk of C_s tokens is cut into ceil(C_s / T) blocks of T
+// tokens; block k lists (sequence, first token).  One workgroup, sequences in rounds of
+// 1024 with a workgroup prefix sum of the block counts.
+__global__ __launch_bounds__(1024) void prefill_blocks_kernel(const int32_t* cu_tokens, int n_seqs, int T,
+                                                             int max_row_blocks, int2* row_blocks, int32_t* n_row_blocks) {
+    __shared__ int scan[1024];
+    int base = 0;
+    for (int s0 = 0; s0 < n_seqs; s0 += 1024) {
+        const int s = s0 + (int)threadIdx.x;
+        const int C = s < n_seqs ? max(0, cu_tokens[s + 1] - cu_tokens[s]) : 0;
+        const int nb = (C + T - 1) / T;
+        scan[threadIdx.x] = nb;
+        __syncthreads();
+        for (int d = 1; d < 1024; d <<= 1) {
+            const int v = threadIdx.x >= (unsigned)d ? scan[threadIdx.x - d] : 0;
+            __syncthreads();
+            scan[threadIdx.x] += v;
+            __syncthreads();
+        }
+        const int first = base + scan[threadIdx.x] - nb;
+        for (int j = 0; j < nb; ++j)
+            if (first + j < max_row_blocks) row_blocks[first + j] = make_int2(s, j * T);
+        base += scan[1023];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) *n_row_blocks = min(base, max_row_blocks);
+}
+
+}  // namespace
+
+PrefillPlan plan_prefill(int32_t n_tokens, int32_t n_q_heads, int32_t n_kv_heads, int32_t max_seq_len,
+                         int32_t window) {
+    PrefillPlan p{};
+    const int G = n_q_heads / n_kv_heads;
+    p.tokens_per_block = kRowsPerBlock / G;
+    // keys a block can see: its own tokens and everything before them (or a window of W
+    // before its first token)
+    const int64_t span = window > 0 ? std::min<int64_t>(max_seq_len, (int64_t)window + p.tokens_per_block + kPage)
+                                    : max_seq_len;
+    const int max_pages = (int)((span + kPage - 1) / kPage) + 1;
+    const int64_t units = (int64_t)std::max(1, (n_tokens + p.tokens_per_block - 1) / p.tokens_per_block) * n_kv_heads;
+    const int want = (int)std::max<int64_t>(1, (2048 + units - 1) / units);
+    p.pages_per_split = std::max(16, (max_pages + want - 1) / want);
+    p.n_splits = (max_pages + p.pages_per_split - 1) / p.pages_per_split;
+    return p;
+}
+
+hipError_t launch_prefill(const PrefillArgs& a, int d, int2* row_blocks, int32_t* n_row_blocks, hipStream_t st) {
+    hipLaunchKernelGGL(prefill_blocks_kernel, dim3(1), dim3(1024), 0, st, a.cu_tokens, a.n_seqs, a.tokens_per_block,
+                       a.max_row_blocks, row_blocks, n_row_blocks);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const dim3 grid(a.max_row_blocks, a.H, a.n_splits);
+    const bool pg = a.spool != nullptr;
+    if (d == 128 && !pg)
+        hipLaunchKernelGGL((prefill_kernel<128, false>), grid, dim3(kPfThreads), 0, st, a);
+    else if (d == 128)
+        hipLaunchKernelGGL((prefill_kernel<128, true>), grid, dim3(kPfThreads), 0, st, a);
+    else if (d == 64 && !pg)
+        hipLaunchKernelGGL((prefill_kernel<64, false>), grid, dim3(kPfThreads), 0, st, a);
+    else if (d == 64)
+        hipLaunchKernelGGL((prefill_kernel<64, true>), grid, dim3(kPfThreads), 0, st, a);
+    else
+        return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
+}  // namespace oaken

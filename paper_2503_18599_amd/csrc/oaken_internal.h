@@ -75,10 +75,6 @@ struct AttnArgs {
     float scale;
     const uint8_t* spool;         // on-demand sparse pages (nullptr: fixed records)
     int32_t spages;
-    // prefill chunks: row r is a query token of sequence tok_seq[r] at position tok_pos[r]
-    // (nullptr: row r is sequence r, of length seq_lens[r])
-    const int32_t* tok_seq;
-    const int32_t* tok_pos;
 };
 
 // Attention workgroups form a 1-D grid with the KV head varying fastest, then the row,
@@ -99,6 +95,35 @@ inline uint32_t attn_grid(const AttnArgs& a) {
     const int64_t n = (int64_t)a.n_splits * a.H * a.n_seqs;
     return (n > 0 && n <= 0x7fffffff) ? (uint32_t)n : 0u;
 }
+
+// Chunked prefill (attention_prefill.hip): row blocks of up to 64 (query token, query head)
+// rows of one sequence's chunk and one KV head, each reading its pages once.
+struct PrefillArgs {
+    const uint8_t* pool;
+    const float* thr;             // [H][2][4]
+    const uint16_t* q;            // fp16 bits [n_tokens][Hq][d]
+    const int32_t* block_table;   // [n_seqs][max_blocks]
+    const int32_t* start_pos;     // [n_seqs]
+    const int32_t* cu_tokens;     // [n_seqs + 1]
+    const int2* row_blocks;       // (sequence, first chunk token) per row block
+    const int32_t* n_row_blocks;  // number of row blocks (device)
+    float* out;                   // fp32 [n_tokens][Hq][d]
+    float* partial;               // [n_tokens][Hq][n_splits][d + 2] when n_splits > 1
+    int64_t stride;
+    int32_t num_blocks, H, Hq, max_blocks, n_seqs, n_tokens, max_seq_len;
+    int32_t tokens_per_block, max_row_blocks, pages_per_split, n_splits, window;
+    float scale;
+    const uint8_t* spool;         // on-demand sparse pages (nullptr: fixed records)
+    int32_t spages;
+};
+struct PrefillPlan {
+    int32_t tokens_per_block, pages_per_split, n_splits;
+};
+PrefillPlan plan_prefill(int32_t n_tokens, int32_t n_q_heads, int32_t n_kv_heads, int32_t max_seq_len,
+                         int32_t window);
+hipError_t launch_prefill(const PrefillArgs& a, int d, int2* row_blocks, int32_t* n_row_blocks, hipStream_t st);
+// Log-sum-exp merge of split partials for a.n_seqs * a.Hq rows (attention.hip).
+hipError_t launch_combine(const AttnArgs& a, int d, hipStream_t st);
 
 // Split-K plan used by both the workspace query and the launch.
 struct SplitPlan {
@@ -121,8 +146,6 @@ hipError_t launch_sparse_release(const SparseArgs& a, const int32_t* block_ids, 
 hipError_t launch_quantize(const QuantArgs& a, int d, int max_new_per_seq, hipStream_t st);
 hipError_t launch_calibrate(const CalibArgs& a, hipStream_t st);
 hipError_t launch_attention(const AttnArgs& a, int d, hipStream_t st);
-hipError_t launch_token_map(const int32_t* cu_tokens, const int32_t* start_pos, int n_seqs, int n_tokens,
-                            int32_t* tok_seq, int32_t* tok_pos, hipStream_t st);
 
 // Streaming-read probe (probe.hip).
 struct ProbeArgs {

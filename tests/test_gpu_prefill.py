@@ -78,7 +78,10 @@ def test_prefill_attention_paged(B, ref):
 
 
 def test_prefill_last_token_is_decode(B, ref):
-    """The last query of a chunk sees the whole sequence: its output is decode attention's."""
+    """The last query of a chunk sees the whole sequence: its output is decode attention's
+    (the two kernels compute differently -- fp32 matrix cores over dequantized tiles here,
+    integer limbs and COO corrections there -- so they agree within the attention
+    tolerance)."""
     case = Case(synth.scaled(synth.WORKLOADS[4], n_seqs=4, ctx=300, ctx_min=20))
     case.calibrate_oracle(ref)
     n, Hq, d = case.n_seqs, case.Hq, case.d
@@ -91,4 +94,5 @@ def test_prefill_last_token_is_decode(B, ref):
     dec = B.decode_attention(cache, q, bt, case.lens.to(DEV), int(case.lens.max()), 0.09)
     pre = B.prefill_attention(cache, q, bt, (case.lens - 1).to(torch.int32).to(DEV),
                               torch.arange(n + 1, dtype=torch.int32).to(DEV), int(case.lens.max()), 0.09)
-    assert torch.allclose(dec, pre, rtol=1e-5, atol=1e-6)
+    ok, max_abs, max_rel = attention_tolerance(pre.cpu().numpy(), dec.cpu().numpy())
+    assert ok, (max_abs, max_rel)
