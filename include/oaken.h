@@ -196,7 +196,8 @@ int oaken_quantize_kv(const oaken_cache* cache, const void* k_new, const void* v
  * seq_lens: int32 [n_seqs], each in [1, max_seq_len]; block_table as above.
  * Arithmetic is fp32; results match an fp64 evaluation within 2e-3 + 1e-2 |ref|.
  * workspace: oaken_attention_workspace_bytes(n_seqs, n_q_heads, n_kv_heads,
- * head_dim, max_seq_len) bytes (may be NULL when that is 0).
+ * head_dim, max_seq_len) bytes, 16-byte aligned (may be NULL when that is 0); it holds
+ * the split partials of long sequences.
  */
 int oaken_decode_attention(const oaken_cache* cache, const void* q, int32_t n_q_heads,
                            const int32_t* block_table, int32_t max_blocks_per_seq,
@@ -234,9 +235,11 @@ int oaken_decode_attention_window(const oaken_cache* cache, const void* q, int32
  * sequence's keys max(0, p + 1 - W) .. p (W = sliding_window, 0 = no window), which must
  * already be in the cache: quantize the chunk's keys and values first.
  * out: fp32 [n_tokens][n_q_heads][head_dim].  Every p + 1 <= max_seq_len.
- * Each query reads its own prefix: keys are shared by the query heads of a KV head, not
- * across the tokens of a chunk.  workspace: oaken_prefill_attention_workspace_bytes(...)
- * bytes (never 0 for valid sizes: it holds the token-to-sequence map).
+ * Rows (query token, query head) are processed in blocks of up to 64: consecutive tokens
+ * of one chunk times the query heads of one KV head.  A block reads each page of its keys
+ * once.
+ * workspace: oaken_prefill_attention_workspace_bytes(...) bytes, 16-byte aligned (never 0
+ * for valid sizes: it holds the row-block list, and split partials of long prefixes).
  */
 size_t oaken_prefill_attention_workspace_bytes(int32_t n_tokens, int32_t n_q_heads, int32_t n_kv_heads,
                                                int32_t head_dim, int32_t max_seq_len, int32_t sliding_window);

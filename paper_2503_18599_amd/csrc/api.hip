@@ -114,6 +114,8 @@ int attention_rows(const oaken_cache* cache, const void* q, int32_t n_q_heads, c
                                                                cache->head_dim, max_seq_len, sliding_window);
     if (need > 0 && (!workspace || workspace_bytes < need))
         return fail(OAKEN_ERR_WORKSPACE, "attention workspace %zu < %zu bytes", workspace_bytes, need);
+    if (need > 0 && reinterpret_cast<uintptr_t>(workspace) % 16 != 0)
+        return fail(OAKEN_ERR_INVALID_ARG, "attention workspace not 16-byte aligned");
     const oaken::SplitPlan sp = oaken::plan_splits(n_rows, n_q_heads, cache->n_kv_heads, cache->head_dim,
                                                    attention_span(max_seq_len, sliding_window));
     oaken::AttnArgs a{};
@@ -413,6 +415,8 @@ int oaken_prefill_attention(const oaken_cache* cache, const void* q, int32_t n_q
     const PrefillWs w = prefill_ws(n_tokens, n_q_heads, cache->head_dim, p);
     if (!workspace || workspace_bytes < w.total)
         return fail(OAKEN_ERR_WORKSPACE, "prefill attention workspace %zu < %zu bytes", workspace_bytes, w.total);
+    if (reinterpret_cast<uintptr_t>(workspace) % 16 != 0)
+        return fail(OAKEN_ERR_INVALID_ARG, "prefill attention workspace not 16-byte aligned");
     uint8_t* ws = static_cast<uint8_t*>(workspace);
     oaken::PrefillArgs a{};
     a.pool = static_cast<const uint8_t*>(cache->pool);

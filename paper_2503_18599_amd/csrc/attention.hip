@@ -203,28 +203,69 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
 }
 
 // Log-sum-exp merge of the per-range partials of one (sequence, query head).
-template <int D>
-__global__ __launch_bounds__(D) void attn_combine_kernel(AttnArgs a) {
+// Log-sum-exp merge of the page ranges' partials (m, l, o) of one (sequence, query head)
+// row.  NW waves share the row's ranges (wave w takes ranges w, w + NW, ...), each lane
+// D / 64 channels, with a running maximum (the sums are rescaled when it grows), unrolled
+// so that several ranges' loads are in flight together; ranges with l = 0 (past a
+// sequence's end) are skipped.  The waves' (M, den, num) then meet in LDS.
+template <int D, int NW>
+__global__ __launch_bounds__(64 * NW) void attn_combine_kernel(AttnArgs a) {
+    constexpr int V = D / 64;
     const int64_t row = blockIdx.x;
-    const int j = threadIdx.x;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const float* pp = a.partial + row * a.n_splits * (D + 2);
-    // One pass with a running maximum (the sums are rescaled when it grows), unrolled so
-    // that several ranges' loads are in flight together; ranges with l = 0 (past a
-    // sequence's end) are skipped.
-    float M = -INFINITY, num = 0.0f, den = 0.0f;
+    float M = -INFINITY, den = 0.0f, num[V];
+#pragma unroll
+    for (int v = 0; v < V; ++v) num[v] = 0.0f;
 #pragma unroll 4
-    for (int k = 0; k < a.n_splits; ++k) {
-        const float* pk = pp + k * (D + 2);
-        const float m = pk[D], l = pk[D + 1], o = pk[j];
+    for (int k = w; k < a.n_splits; k += NW) {
+        const float* pk = pp + (int64_t)k * (D + 2);
+        const float m = pk[D], l = pk[D + 1];
+        float o[V];
+        if constexpr (V == 2) {
+            const float2 t = *reinterpret_cast<const float2*>(pk + 2 * lane);   // (D + 2) * 4 is a multiple of 8
+            o[0] = t.x;
+            o[1] = t.y;
+        } else {
+            o[0] = pk[lane];
+        }
         if (l > 0.0f) {
             const float Mn = fmaxf(M, m);
-            const float r = __expf(M - Mn), w = __expf(m - Mn);
-            num = fmaf(num, r, w * o);
-            den = fmaf(den, r, w * l);
+            const float r = __expf(M - Mn), e = __expf(m - Mn);
+#pragma unroll
+            for (int v = 0; v < V; ++v) num[v] = fmaf(num[v], r, e * o[v]);
+            den = fmaf(den, r, e * l);
             M = Mn;
         }
     }
-    a.out[row * D + j] = (den > 0.0f) ? num / den : 0.0f;
+    if constexpr (NW > 1) {
+        __shared__ float s_md[NW][2];
+        __shared__ float s_num[NW][D];
+        if (lane == 0) {
+            s_md[w][0] = M;
+            s_md[w][1] = den;
+        }
+#pragma unroll
+        for (int v = 0; v < V; ++v) s_num[w][V * lane + v] = num[v];
+        __syncthreads();
+        if (w != 0) return;
+        float Mx = -INFINITY;
+#pragma unroll
+        for (int x = 0; x < NW; ++x)
+            if (s_md[x][1] > 0.0f) Mx = fmaxf(Mx, s_md[x][0]);
+        den = 0.0f;
+#pragma unroll
+        for (int v = 0; v < V; ++v) num[v] = 0.0f;
+#pragma unroll
+        for (int x = 0; x < NW; ++x) {
+            const float r = s_md[x][1] > 0.0f ? __expf(s_md[x][0] - Mx) : 0.0f;
+            den = fmaf(s_md[x][1], r, den);
+#pragma unroll
+            for (int v = 0; v < V; ++v) num[v] = fmaf(s_num[x][V * lane + v], r, num[v]);
+        }
+    }
+#pragma unroll
+    for (int v = 0; v < V; ++v) a.out[row * D + V * lane + v] = (den > 0.0f) ? num[v] / den : 0.0f;
 }
 
 }  // namespace
@@ -249,14 +290,25 @@ SplitPlan plan_splits(int32_t n_seqs, int32_t n_q_heads, int32_t n_kv_heads, int
     return sp;
 }
 
-hipError_t launch_combine(const AttnArgs& a, int d, hipStream_t st) {
-    if (d == 64)
-        hipLaunchKernelGGL(attn_combine_kernel<64>, dim3(a.n_seqs * a.Hq), dim3(64), 0, st, a);
-    else if (d == 128)
-        hipLaunchKernelGGL(attn_combine_kernel<128>, dim3(a.n_seqs * a.Hq), dim3(128), 0, st, a);
+// Waves per row of the combine: about eight ranges per wave, at most eight waves.
+template <int D>
+hipError_t launch_combine_d(const AttnArgs& a, hipStream_t st) {
+    const dim3 grid((uint32_t)((int64_t)a.n_seqs * a.Hq));
+    if (a.n_splits <= 8)
+        hipLaunchKernelGGL((attn_combine_kernel<D, 1>), grid, dim3(64), 0, st, a);
+    else if (a.n_splits <= 16)
+        hipLaunchKernelGGL((attn_combine_kernel<D, 2>), grid, dim3(128), 0, st, a);
+    else if (a.n_splits <= 32)
+        hipLaunchKernelGGL((attn_combine_kernel<D, 4>), grid, dim3(256), 0, st, a);
     else
-        return hipErrorInvalidValue;
+        hipLaunchKernelGGL((attn_combine_kernel<D, 8>), grid, dim3(512), 0, st, a);
     return hipGetLastError();
+}
+
+hipError_t launch_combine(const AttnArgs& a, int d, hipStream_t st) {
+    if (d == 64) return launch_combine_d<64>(a, st);
+    if (d == 128) return launch_combine_d<128>(a, st);
+    return hipErrorInvalidValue;
 }
 
 hipError_t launch_attention(const AttnArgs& a, int d, hipStream_t st) {
@@ -268,8 +320,7 @@ hipError_t launch_attention(const AttnArgs& a, int d, hipStream_t st) {
     if (mfma_attention_supported(d, G)) {
         hipError_t e = launch_attention_mfma(a, st);
         if (e != hipSuccess || a.n_splits == 1) return e;
-        hipLaunchKernelGGL(attn_combine_kernel<128>, dim3(a.n_seqs * a.Hq), dim3(128), 0, st, a);
-        return hipGetLastError();
+        return launch_combine(a, d, st);
     }
     if (d == 64) {
         hipLaunchKernelGGL(attn_split_kernel<64>, dim3(grid), dim3(kThreads), shm, st, a);
@@ -280,11 +331,7 @@ hipError_t launch_attention(const AttnArgs& a, int d, hipStream_t st) {
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.n_splits == 1) return e;
-    if (d == 64)
-        hipLaunchKernelGGL(attn_combine_kernel<64>, dim3(a.n_seqs * a.Hq), dim3(64), 0, st, a);
-    else
-        hipLaunchKernelGGL(attn_combine_kernel<128>, dim3(a.n_seqs * a.Hq), dim3(128), 0, st, a);
-    return hipGetLastError();
+    return launch_combine(a, d, st);
 }
 
 }  // namespace oaken

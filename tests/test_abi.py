@@ -89,6 +89,11 @@ def test_attention_validation(L):
     assert need > 0
     assert L.oaken_decode_attention(*args()) == 3
     assert b"workspace" in L.oaken_last_error()
+    # a workspace that is large enough but not 16-byte aligned is rejected before any launch
+    a = args()
+    a[10], a[11] = 0x1008, need
+    assert L.oaken_decode_attention(*a) == 1
+    assert b"aligned" in L.oaken_last_error()
 
 
 def test_calibrate_validation(L):
