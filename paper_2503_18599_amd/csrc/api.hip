@@ -109,7 +109,7 @@ int attention_rows(const oaken_cache* cache, const void* q, int32_t n_q_heads, c
     if (sliding_window < 0) return fail(OAKEN_ERR_INVALID_ARG, "sliding_window must be >= 0");
     if (cache->sparse_pool && !oaken::mfma_attention_supported(cache->head_dim, n_q_heads / cache->n_kv_heads))
         return fail(OAKEN_ERR_UNSUPPORTED,
-                    "on-demand sparse pages need head_dim 128 and 1, 2 or 4 query heads per KV head");
+                    "on-demand sparse pages need head_dim 128");
     const size_t need = oaken_attention_workspace_bytes_window(n_rows, n_q_heads, cache->n_kv_heads,
                                                                cache->head_dim, max_seq_len, sliding_window);
     if (need > 0 && (!workspace || workspace_bytes < need))

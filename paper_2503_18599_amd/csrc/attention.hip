@@ -273,13 +273,14 @@ __global__ __launch_bounds__(64 * NW) void attn_combine_kernel(AttnArgs a) {
 SplitPlan plan_splits(int32_t n_seqs, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
                       int32_t max_seq_len) {
     const int G = n_q_heads / n_kv_heads;
+    const bool mfma = mfma_attention_supported(head_dim, G);
     const int max_pages = (max_seq_len + kPage - 1) / kPage;
-    const int64_t units = (int64_t)n_seqs * n_kv_heads;
+    const int64_t units = (int64_t)n_seqs * n_kv_heads * (mfma ? G / mfma_wave_heads(G) : 1);
     const int64_t target = 4096;   // workgroups that keep 256 CUs busy
     int want = (int)((target + units - 1) / units);
     int pps = (max_pages + want - 1) / want;
     pps = max(pps, 8);
-    if (mfma_attention_supported(head_dim, G))
+    if (mfma)
         pps = min(pps, mfma_score_cap() / kPage);
     else
         pps = min(pps, kScoreCap / (kPage * G));
@@ -311,13 +312,17 @@ hipError_t launch_combine(const AttnArgs& a, int d, hipStream_t st) {
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_attention(const AttnArgs& a, int d, hipStream_t st) {
+hipError_t launch_attention(const AttnArgs& args, int d, hipStream_t st) {
+    AttnArgs a = args;
     const int G = a.Hq / a.H;
-    if (G > kMaxG) return hipErrorInvalidValue;
+    if (G < 1 || G > kMaxG) return hipErrorInvalidValue;
+    const bool mfma = mfma_attention_supported(d, G);
+    a.wave_heads = mfma ? mfma_wave_heads(G) : G;
+    a.head_parts = G / a.wave_heads;
     const size_t shm = (size_t)G * a.pages_per_split * kPage * sizeof(float);
     const uint32_t grid = attn_grid(a);
     if (grid == 0) return hipErrorInvalidValue;
-    if (mfma_attention_supported(d, G)) {
+    if (mfma) {
         hipError_t e = launch_attention_mfma(a, st);
         if (e != hipSuccess || a.n_splits == 1) return e;
         return launch_combine(a, d, st);

@@ -1,5 +1,7 @@
 // Decode attention over the Oaken-quantized cache on CDNA4 int8 matrix cores
-// (head_dim 128; 1, 2 or 4 query heads per KV head).
+// (head_dim 128; a workgroup takes 1, 2 or 4 query heads of one KV head, and a KV head
+// with more query heads, or a number that is not one of these, is split over several
+// workgroups that read the same pages).
 //
 // Dequantization is split into a dense part that runs on MFMA and a sparse part that
 // runs on the vector units, mirroring the paper's dense/sparse split (Sec. 4.5) and
@@ -673,6 +675,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
     const int lane = threadIdx.x;
     const AttnTile tile = attn_tile(a);
     const int split = tile.split, h = tile.h, s = tile.s;
+    const int qh0 = h * (a.Hq / a.H) + tile.part * G;   // the workgroup's first query head
     const int L = max(0, min(a.seq_lens[s], min(a.max_seq_len, a.max_blocks * P)));
     const int n_pages = (L + P - 1) / P;
     // a sliding window hides keys before lo; the ranges start at its first page
@@ -685,7 +688,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
     // which the combine skips) and nothing else
     if (n_tok <= 0 && a.n_splits > 1) {
         if (lane < G) {
-            float* pp = a.partial + (((int64_t)s * a.Hq + h * G + lane) * a.n_splits + split) * (D + 2);
+            float* pp = a.partial + (((int64_t)s * a.Hq + qh0 + lane) * a.n_splits + split) * (D + 2);
             pp[D] = -INFINITY;
             pp[D + 1] = 0.0f;
         }
@@ -714,7 +717,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
     float ssum[G], sfix[G];
 #pragma unroll
     for (int hd = 0; hd < G; ++hd) {
-        const uint16_t* qp = a.q + ((int64_t)s * a.Hq + h * G + hd) * D;
+        const uint16_t* qp = a.q + ((int64_t)s * a.Hq + qh0 + hd) * D;
         const float x0 = h2f(qp[lane]), x1 = h2f(qp[lane + 64]);
         S.q16()[lane][hd] = __ushort_as_half(qp[lane]);
         S.q16()[lane + 64][hd] = __ushort_as_half(qp[lane + 64]);
@@ -1129,7 +1132,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
     wave_sync();
     if (hq < G || G == 1) {
         const int hd = G == 1 ? 0 : hq;
-        const int64_t row = (int64_t)s * a.Hq + h * G + hd;
+        const int64_t row = (int64_t)s * a.Hq + qh0 + hd;
         const float l = S.l[hd];
 #pragma unroll
         for (int nt = 0; nt < NO; ++nt) {
@@ -1156,7 +1159,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
 // module with the fixed-record kernel it changes the fixed kernel's register allocation.
 template <bool PG>
 static hipError_t launch_mfma(const AttnArgs& a, hipStream_t st) {
-    const int G = a.Hq / a.H;
+    const int G = a.wave_heads;
+    if (G * a.head_parts != a.Hq / a.H) return hipErrorInvalidValue;
     // a range spans at most 32 pages (the lane reads of the page table rely on it)
     if (a.pages_per_split > 32 || a.pages_per_split * P > mfma_score_cap()) return hipErrorInvalidValue;
     const size_t shm = (size_t)G * a.pages_per_split * P * sizeof(float);
@@ -1176,7 +1180,10 @@ static hipError_t launch_mfma(const AttnArgs& a, hipStream_t st) {
 #ifdef OAKEN_ATTN_PAGED_TU
 hipError_t launch_attention_mfma_paged(const AttnArgs& a, hipStream_t st) { return launch_mfma<true>(a, st); }
 #else
-bool mfma_attention_supported(int d, int G) { return d == D && (G == 1 || G == 2 || G == 4); }
+bool mfma_attention_supported(int d, int G) { return d == D && G >= 1 && G <= 8; }
+
+// G = 8 and 4 take four heads per workgroup, 6 and 2 two, the odd counts one.
+int mfma_wave_heads(int G) { return G % 4 == 0 ? 4 : (G % 2 == 0 ? 2 : 1); }
 
 int mfma_score_cap() { return 512; }
 

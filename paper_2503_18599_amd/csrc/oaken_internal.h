@@ -75,24 +75,31 @@ struct AttnArgs {
     float scale;
     const uint8_t* spool;         // on-demand sparse pages (nullptr: fixed records)
     int32_t spages;
+    // A KV head's G = Hq / H query heads are split over head_parts workgroups of
+    // wave_heads heads each (head_parts * wave_heads = G); set by launch_attention.
+    int32_t wave_heads, head_parts;
 };
 
-// Attention workgroups form a 1-D grid with the KV head varying fastest, then the row,
-// then the page range.  Workgroups are handed to the eight XCDs round-robin by linear id,
-// so every XCD receives the same heads of every row and range: an equal share of the
-// work even when sequence lengths vary (with the range fastest, XCD k would get ranges k
-// and k + 8 of every sequence, and the late ranges exist only for long sequences).  Early
-// ranges go out first, so the short or empty last ranges fill the tail.
+// Attention workgroups form a 1-D grid with the KV head varying fastest, then the part of
+// its query heads, then the row, then the page range.  Workgroups are handed to the eight
+// XCDs round-robin by linear id, so every XCD receives the same heads of every row and
+// range: an equal share of the work even when sequence lengths vary (with the range
+// fastest, XCD k would get ranges k and k + 8 of every sequence, and the late ranges exist
+// only for long sequences).  Early ranges go out first, so the short or empty last ranges
+// fill the tail.  The parts of one KV head are H workgroups apart: with H a multiple of 8
+// they run on the same XCD, whose L2 then serves the pages a second part reads.
 struct AttnTile {
-    int split, h, s;
+    int split, h, s, part;
 };
 __device__ __forceinline__ AttnTile attn_tile(const AttnArgs& a) {
-    const uint32_t id = blockIdx.x, hs = id / (uint32_t)a.H;   // the grid fits 31 bits
-    return AttnTile{(int)(hs / (uint32_t)a.n_seqs), (int)(id % (uint32_t)a.H), (int)(hs % (uint32_t)a.n_seqs)};
+    const uint32_t hv_n = (uint32_t)(a.H * a.head_parts);
+    const uint32_t id = blockIdx.x, hs = id / hv_n, hv = id % hv_n;   // the grid fits 31 bits
+    return AttnTile{(int)(hs / (uint32_t)a.n_seqs), (int)(hv % (uint32_t)a.H), (int)(hs % (uint32_t)a.n_seqs),
+                    (int)(hv / (uint32_t)a.H)};
 }
 // Workgroups of an attention launch; 0 when the grid would not fit one dimension.
 inline uint32_t attn_grid(const AttnArgs& a) {
-    const int64_t n = (int64_t)a.n_splits * a.H * a.n_seqs;
+    const int64_t n = (int64_t)a.n_splits * a.H * a.head_parts * a.n_seqs;
     return (n > 0 && n <= 0x7fffffff) ? (uint32_t)n : 0u;
 }
 
@@ -178,8 +185,10 @@ struct VariantArgs {
 hipError_t launch_variant_quantize(const VariantArgs& a, int d, hipStream_t st);
 hipError_t launch_variant_dequantize(const VariantArgs& a, int d, hipStream_t st);
 
-// Matrix-core decode attention (head_dim 128; 1, 2 or 4 query heads per KV head).
+// Matrix-core decode attention (head_dim 128; 1..8 query heads per KV head, taken 1, 2 or 4
+// per workgroup).
 bool mfma_attention_supported(int d, int G);
+int mfma_wave_heads(int G);      // query heads per workgroup for G heads per KV head
 int mfma_score_cap();   // tokens per query head in one workgroup's page range
 hipError_t launch_attention_mfma(const AttnArgs& a, hipStream_t st);
 hipError_t launch_attention_mfma_paged(const AttnArgs& a, hipStream_t st);   // on-demand sparse pages

@@ -1,10 +1,11 @@
 """GPU parity for every head shape the C ABI accepts.
 
 The attention entry points take head_dim 64 or 128 and 1..8 query heads per KV head
-(G).  head_dim 128 with G in {1, 2, 4} runs the matrix-core kernel; every other shape runs
-the vector-unit kernel.  The workload tests cover G = 1 and 4; this module adds G = 2 on
-the matrix cores (fixed records and on-demand sparse pages), G = 3 and 8 at head_dim 128
-and G = 2, 4 and 8 at head_dim 64 on the vector units: decode attention over ragged
+(G).  head_dim 128 runs the matrix-core kernel, which takes 1, 2 or 4 query heads per
+workgroup (G = 3 as three workgroups of one head, G = 8 as two of four); head_dim 64 runs
+the vector-unit kernel.  The workload tests cover G = 1 and 4; this module adds G = 2
+(fixed records and on-demand sparse pages), 3 and 8 at head_dim 128 and G = 2, 4 and 8
+at head_dim 64: decode attention over ragged
 lengths (one token, page multiples, ragged tails, several page ranges per sequence so the
 split combine runs), sliding windows, and chunked prefill, each against the oracle
 within |gpu - ref| <= 2e-3 + 1e-2 |ref|.
@@ -83,10 +84,12 @@ def test_decode_attention_head_shapes(B, ref, shape, window):
     assert ok, (max_abs, max_rel)
 
 
+@pytest.mark.parametrize("shape", ["g2-d128", "g3-d128", "g8-d128"])
 @pytest.mark.parametrize("window", [0, 100])
-def test_decode_attention_g2_sparse_pages(B, ref, window):
-    """G = 2 on the matrix cores with on-demand sparse pages."""
-    case = _case(ref, "g2-d128")
+def test_decode_attention_sparse_pages_head_shapes(B, ref, shape, window):
+    """G = 2, 3 and 8 on the matrix cores (one, three and two workgroups per KV head) with
+    on-demand sparse pages."""
+    case = _case(ref, shape)
     pool_ref = case.oracle_pool(ref)
     cache, bt = _cache(B, case, sparse_pages=2 * case.num_blocks * case.H * 2 + 16)
     assert not cache.sparse_status()[1]
