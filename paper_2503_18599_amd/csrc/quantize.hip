@@ -89,6 +89,88 @@ __device__ inline void wave_sync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Codes of the eight elements a lane holds of one vector (Eq. 1-4), the vector spread over
+// LPV aligned lanes with eight consecutive elements each (m = lane within the vector).
+struct LaneCodes {
+    uint32_t nib[8];   // the dense nibble (low 4 bits of the code)
+    uint32_t cb[8];    // the COO byte of an inner or outer value
+    bool middle[8];
+    int n_out;         // inner and outer values among the eight
+    float meta;        // lanes m < 6: field m of the vector's metadata (Min_g, Delta_g)
+};
+
+template <int LPV>
+__device__ inline LaneCodes quantize_lane(const uint32_t (&w4)[4], float lo_o, float lo_i, float hi_i, float hi_o,
+                                          int m, int lane) {
+    LaneCodes R;
+    // group, side and shifted magnitude per element; group minima and maxima over the
+    // magnitudes' bit patterns (non-negative floats order as integers): an element of
+    // another group reads as 0xffffffff, the largest unsigned and the smallest signed
+    // key, so one key serves the unsigned minimum and the signed maximum
+    float mag[8];
+    bool outer[8], side[8];
+    uint32_t kmin[3] = {~0u, ~0u, ~0u};
+    int kmax[3] = {-1, -1, -1};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const float xf = half_bits_to_float((e & 1) ? (w4[e >> 1] >> 16) : (w4[e >> 1] & 0xffffu));
+        const bool c_ho = xf > hi_o, c_lo = xf < lo_o, c_hi = xf > hi_i, c_li = xf < lo_i;
+        const bool o = c_ho || c_lo;                 // Eq. 1, outer
+        const bool not_inner = c_hi || c_li;         // outer or middle
+        const float shift = c_lo ? lo_o : (c_ho ? hi_o : (c_hi ? hi_i : lo_i));
+        const float dv = not_inner ? xf - shift : xf;   // Eq. 4 (inner not shifted)
+        mag[e] = fabsf(dv);
+        // the side is the sign of the shifted value: non-zero for outer and middle
+        // values, and x >= 0 (-0 included) for inner ones
+        side[e] = !(dv < 0.0f);
+        outer[e] = o;
+        R.middle[e] = not_inner && !o;
+        const uint32_t mb = __float_as_uint(mag[e]);
+        const uint32_t ki = not_inner ? ~0u : mb, km = R.middle[e] ? mb : ~0u, ko = o ? mb : ~0u;
+        kmin[0] = min(kmin[0], ki); kmax[0] = max(kmax[0], (int)ki);
+        kmin[1] = min(kmin[1], km); kmax[1] = max(kmax[1], (int)km);
+        kmin[2] = min(kmin[2], ko); kmax[2] = max(kmax[2], (int)ko);
+    }
+    float gmin[3], grng[3];
+#pragma unroll
+    for (int g = 0; g < 3; ++g) {
+        const uint32_t lo = group_min_u<LPV>(kmin[g]);
+        const int hi = group_max_i<LPV>(kmax[g]);
+        const bool empty = hi < 0;                   // (0, 0) for an empty group
+        gmin[g] = empty ? 0.0f : __uint_as_float(lo);
+        grng[g] = empty ? 0.0f : __int_as_float(hi) - gmin[g];
+    }
+    // Eq. 2: lane 2g of the vector forms sigma_g = L/R, lane 2g+1 Delta_g = R/L (its
+    // metadata); one correctly rounded division per lane
+    const int g6 = (m >> 1) < 3 ? (m >> 1) : 0;
+    const bool is_delta = (m & 1) != 0;
+    const float Rg = g6 == 0 ? grng[0] : (g6 == 1 ? grng[1] : grng[2]);
+    const float Lg = g6 == 1 ? 7.0f : 15.0f;
+    float quo = (is_delta ? Rg : Lg) / (is_delta ? Lg : Rg);
+    if (!is_delta && Rg == 0.0f) quo = 0.0f;
+    const int vbase = lane & ~(LPV - 1);
+    float sig[3];
+#pragma unroll
+    for (int g = 0; g < 3; ++g) sig[g] = __shfl(quo, vbase + 2 * g, 64);
+    R.meta = is_delta ? quo : gmin[g6];
+
+    // Eq. 3 and the offset-binary code u = side ? 2^b + c : 2^b - 1 - c, whose low four
+    // bits are c ^ L ^ (side ? 15 : 0).  No clamp is needed: 0 <= a - Min <= R rounds
+    // to at most R, and R * fl(L / R) rounds to less than L + 1/2.
+    R.n_out = 0;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const float gm = outer[e] ? gmin[2] : (R.middle[e] ? gmin[1] : gmin[0]);
+        const float gs = outer[e] ? sig[2] : (R.middle[e] ? sig[1] : sig[0]);
+        const uint32_t ci = (uint32_t)rintf((mag[e] - gm) * gs);
+        R.nib[e] = ci ^ (R.middle[e] ? 7u : 15u) ^ (side[e] ? 15u : 0u);
+        const uint32_t c0 = outer[e] ? (0x40u | (uint32_t)((8 * m + e) & 63)) : (uint32_t)((8 * m + e) & 63);
+        R.cb[e] = side[e] ? (c0 | 0x80u) : c0;
+        R.n_out += R.middle[e] ? 0 : 1;
+    }
+    return R;
+}
+
 // One wave's staging area: the segment's COO bytes (from the segment's first entry),
 // V nibbles one byte per element, fp16 metadata and per-chunk counts by slot, and the
 // record's sparse page ids (on-demand pages).
@@ -176,71 +258,9 @@ __global__ __launch_bounds__(64 * kWavesPerGroup) void quantize_kernel(QuantArgs
         const int t = slot0 + i;
         const uint32_t w4[4] = {xin[p].x, xin[p].y, xin[p].z, xin[p].w};
 
-        // group, side and shifted magnitude per element; group minima and maxima over the
-        // magnitudes' bit patterns (non-negative floats order as integers): an element of
-        // another group reads as 0xffffffff, the largest unsigned and the smallest signed
-        // key, so one key serves the unsigned minimum and the signed maximum
-        float mag[8];
-        bool outer[8], middle[8], side[8];
-        uint32_t kmin[3] = {~0u, ~0u, ~0u};
-        int kmax[3] = {-1, -1, -1};
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const float xf = half_bits_to_float((e & 1) ? (w4[e >> 1] >> 16) : (w4[e >> 1] & 0xffffu));
-            const bool c_ho = xf > hi_o, c_lo = xf < lo_o, c_hi = xf > hi_i, c_li = xf < lo_i;
-            const bool o = c_ho || c_lo;                 // Eq. 1, outer
-            const bool not_inner = c_hi || c_li;         // outer or middle
-            const float shift = c_lo ? lo_o : (c_ho ? hi_o : (c_hi ? hi_i : lo_i));
-            const float dv = not_inner ? xf - shift : xf;   // Eq. 4 (inner not shifted)
-            mag[e] = fabsf(dv);
-            // the side is the sign of the shifted value: non-zero for outer and middle
-            // values, and x >= 0 (-0 included) for inner ones
-            side[e] = !(dv < 0.0f);
-            outer[e] = o;
-            middle[e] = not_inner && !o;
-            const uint32_t mb = __float_as_uint(mag[e]);
-            const uint32_t ki = not_inner ? ~0u : mb, km = middle[e] ? mb : ~0u, ko = o ? mb : ~0u;
-            kmin[0] = min(kmin[0], ki); kmax[0] = max(kmax[0], (int)ki);
-            kmin[1] = min(kmin[1], km); kmax[1] = max(kmax[1], (int)km);
-            kmin[2] = min(kmin[2], ko); kmax[2] = max(kmax[2], (int)ko);
-        }
-        float gmin[3], grng[3];
-#pragma unroll
-        for (int g = 0; g < 3; ++g) {
-            const uint32_t lo = group_min_u<LPV>(kmin[g]);
-            const int hi = group_max_i<LPV>(kmax[g]);
-            const bool empty = hi < 0;                   // (0, 0) for an empty group
-            gmin[g] = empty ? 0.0f : __uint_as_float(lo);
-            grng[g] = empty ? 0.0f : __int_as_float(hi) - gmin[g];
-        }
-        // Eq. 2: lane 2g of the vector forms sigma_g = L/R, lane 2g+1 Delta_g = R/L (its
-        // metadata); one correctly rounded division per lane
-        const int g6 = (m >> 1) < 3 ? (m >> 1) : 0;
-        const bool is_delta = (m & 1) != 0;
-        const float Rg = g6 == 0 ? grng[0] : (g6 == 1 ? grng[1] : grng[2]);
-        const float Lg = g6 == 1 ? 7.0f : 15.0f;
-        float quo = (is_delta ? Rg : Lg) / (is_delta ? Lg : Rg);
-        if (!is_delta && Rg == 0.0f) quo = 0.0f;
-        const int vbase = lane & ~(LPV - 1);
-        float sig[3];
-#pragma unroll
-        for (int g = 0; g < 3; ++g) sig[g] = __shfl(quo, vbase + 2 * g, 64);
-
-        // Eq. 3 and the offset-binary code u = side ? 2^b + c : 2^b - 1 - c, whose low four
-        // bits are c ^ L ^ (side ? 15 : 0).  No clamp is needed: 0 <= a - Min <= R rounds
-        // to at most R, and R * fl(L / R) rounds to less than L + 1/2.
-        uint32_t nib[8], cb[8];
-        int cnt = 0;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const float gm = outer[e] ? gmin[2] : (middle[e] ? gmin[1] : gmin[0]);
-            const float gs = outer[e] ? sig[2] : (middle[e] ? sig[1] : sig[0]);
-            const uint32_t ci = (uint32_t)rintf((mag[e] - gm) * gs);
-            nib[e] = ci ^ (middle[e] ? 7u : 15u) ^ (side[e] ? 15u : 0u);
-            const uint32_t c0 = outer[e] ? (0x40u | (uint32_t)((8 * m + e) & 63)) : (uint32_t)((8 * m + e) & 63);
-            cb[e] = side[e] ? (c0 | 0x80u) : c0;
-            cnt += (valid && !middle[e]) ? 1 : 0;
-        }
+        const LaneCodes Q = quantize_lane<LPV>(w4, lo_o, lo_i, hi_i, hi_o, m, lane);
+        const uint32_t(&nib)[8] = Q.nib;
+        const int cnt = valid ? Q.n_out : 0;
 
         // dense nibbles: K row dwords go out directly; V nibbles are staged by slot
         if (which == 0) {
@@ -254,7 +274,7 @@ __global__ __launch_bounds__(64 * kWavesPerGroup) void quantize_kernel(QuantArgs
             *reinterpret_cast<uint2*>(&W.vn[t][8 * m]) = make_uint2(lo, hi);
         }
         // metadata: lane m < 6 holds field m of the slot: Min_g (even), Delta_g (odd)
-        if (valid && m < 6) W.meta[t][m] = float_to_half_bits(is_delta ? quo : gmin[g6]);
+        if (valid && m < 6) W.meta[t][m] = float_to_half_bits(Q.meta);
 
         // COO entries: positions from a wave-wide prefix sum of the lanes' counts
         const int incl = wave_incl_scan(cnt, lane);
@@ -263,8 +283,8 @@ __global__ __launch_bounds__(64 * kWavesPerGroup) void quantize_kernel(QuantArgs
         int pos = off - pre + incl - cnt;
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-            if (valid && !middle[e]) {
-                if (pos < CAP) W.coo[pos] = (uint8_t)cb[e];
+            if (valid && !Q.middle[e]) {
+                if (pos < CAP) W.coo[pos] = (uint8_t)Q.cb[e];
                 ++pos;
             }
         }
@@ -392,14 +412,128 @@ __global__ __launch_bounds__(64 * kWavesPerGroup) void quantize_kernel(QuantArgs
     }
 }
 
+// Sum over the N = 8 or 16 lanes of a vector (aligned lane groups); every lane gets it.
+template <int N>
+__device__ inline int group_sum(int v) {
+    v += dpp_i<kQuadXor1>(v);
+    v += dpp_i<kQuadXor2>(v);
+    v += dpp_i<kRowHalfMirror>(v);
+    if constexpr (N == 16) v += dpp_i<kRowMirror>(v);
+    return v;
+}
+// Inclusive prefix sum over the N lanes of a vector (m = lane within it): row shifts, each
+// added only where its source lies in the same vector.
+template <int N>
+__device__ inline int group_incl_scan(int x, int m) {
+    int y;
+    y = __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false);   // row_shr:1
+    x += m >= 1 ? y : 0;
+    y = __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false);   // row_shr:2
+    x += m >= 2 ? y : 0;
+    y = __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false);   // row_shr:4
+    x += m >= 4 ? y : 0;
+    if constexpr (N == 16) {
+        y = __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false);   // row_shr:8
+        x += m >= 8 ? y : 0;
+    }
+    return x;
+}
+
+// One new token per sequence (the decode step), fixed-capacity records: every vector
+// (sequence, KV head, K|V) on its own d/8 lanes, so a wave quantizes 64 / (d/8) vectors
+// at once instead of one.  Same codes, stream order and record writes as quantize_kernel
+// for a segment of one slot; the vector's COO offset comes from a prefix sum over its
+// own lanes and the record's counts of the earlier slots.  All lanes stay active through
+// the lane exchanges; vectors without a token only skip their loads and stores.
+template <int D>
+__global__ __launch_bounds__(256) void quantize_token_kernel(QuantArgs a) {
+    constexpr int NC = D / 64, LPV = D / 8, VPW = 64 / LPV;
+    constexpr Layout LY = make_layout(kPage, D);
+    constexpr int CAP = kPage * D;
+    const int lane = threadIdx.x & 63, r = lane / LPV, m = lane % LPV;
+    const int64_t v = ((int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6)) * VPW + r;
+    const int nhw = 2 * a.H;
+    bool ok = v < (int64_t)a.n_seqs * nhw;
+    const int s = ok ? (int)(v / nhw) : 0, hw = ok ? (int)(v % nhw) : 0;
+    const int h = hw >> 1, which = hw & 1;
+    const int row = a.cu_tokens[s];
+    ok = ok && a.cu_tokens[s + 1] - row == 1;
+    const int pos = a.start_pos[s];
+    const int page = pos / kPage, slot = pos % kPage;
+    ok = ok && pos >= 0 && page < a.max_blocks;
+    const int blk = ok ? a.block_table[(int64_t)s * a.max_blocks + page] : 0;
+    ok = ok && blk >= 0 && blk < a.num_blocks;
+    uint8_t* rec = a.pool + (((int64_t)(ok ? blk : 0) * a.H + h) * 2 + which) * a.stride;
+
+    uint4 x = make_uint4(0, 0, 0, 0);
+    if (ok) x = *reinterpret_cast<const uint4*>((which ? a.v_new : a.k_new) + ((int64_t)row * a.H + h) * D + 8 * m);
+    // COO bytes of the record's earlier slots (2 count bytes per lane cover 2 * LPV >= slot * NC)
+    int c = 0;
+    if (ok) {
+        const int b0 = 2 * m, b1 = 2 * m + 1;
+        c = (b0 < slot * NC ? (int)rec[LY.counts + b0] : 0) + (b1 < slot * NC ? (int)rec[LY.counts + b1] : 0);
+    }
+    const int pre = min(group_sum<LPV>(c), CAP);
+    uint32_t old_b = 0;   // V at an odd slot shares its bytes with the slot before
+    const float* th = a.thr + hw * 4;
+    const float lo_o = th[0], lo_i = th[1], hi_i = th[2], hi_o = th[3];
+
+    const uint32_t w4[4] = {x.x, x.y, x.z, x.w};
+    const LaneCodes Q = quantize_lane<LPV>(w4, lo_o, lo_i, hi_i, hi_o, m, lane);
+    const int cnt = Q.n_out;
+    const int incl = group_incl_scan<LPV>(cnt, m);
+    const int c8 = group_sum<8>(cnt);   // entries of the lane's 64-value chunk
+    if (!ok) return;   // (no lane exchange below)
+
+    if (which == 0) {
+        uint32_t kw = 0;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) kw |= Q.nib[e] << (4 * e);
+        *reinterpret_cast<uint32_t*>(rec + LY.dense + slot * (D / 2) + 4 * m) = kw;
+    } else {
+        // channel-major: channel j's byte slot / 2, low nibble the even slot; writing an
+        // even slot clears the odd one after it
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            uint8_t* bp = rec + LY.dense + (8 * m + e) * (kPage / 2) + (slot >> 1);
+            if (slot & 1) old_b = *bp;
+            *bp = (uint8_t)((slot & 1) ? ((old_b & 0x0fu) | (Q.nib[e] << 4)) : Q.nib[e]);
+        }
+    }
+    if (m < 6) reinterpret_cast<uint16_t*>(rec + LY.meta + slot * 12)[m] = float_to_half_bits(Q.meta);
+    if ((m & 7) == 0) rec[LY.counts + slot * NC + (m >> 3)] = (uint8_t)c8;
+    int p = pre + incl - cnt;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        if (!Q.middle[e]) {
+            if (p < CAP) rec[LY.sparse + p] = (uint8_t)Q.cb[e];
+            ++p;
+        }
+    }
+}
+
 }  // namespace
 
 hipError_t launch_quantize(const QuantArgs& a, int d, int max_new_per_seq, hipStream_t st) {
+    const bool pg = a.spool != nullptr;
+    if (max_new_per_seq == 1 && !pg) {
+        // the decode step: one vector per d/8 lanes
+        const int64_t nvec = (int64_t)a.n_seqs * 2 * a.H;
+        const int per_block = 4 * (64 / (d / 8));
+        const int64_t blocks = (nvec + per_block - 1) / per_block;
+        if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+        if (d == 64)
+            hipLaunchKernelGGL(quantize_token_kernel<64>, dim3((uint32_t)blocks), dim3(256), 0, st, a);
+        else if (d == 128)
+            hipLaunchKernelGGL(quantize_token_kernel<128>, dim3((uint32_t)blocks), dim3(256), 0, st, a);
+        else
+            return hipErrorInvalidValue;
+        return hipGetLastError();
+    }
     // pages a run of n tokens can touch: (n + P - 2) / P + 1 (one for a single token)
     const int segs = (max_new_per_seq + kPage - 2) / kPage + 1;
     dim3 grid(segs, a.n_seqs, (2 * a.H + kWavesPerGroup - 1) / kWavesPerGroup);
     dim3 block(64 * kWavesPerGroup);
-    const bool pg = a.spool != nullptr;
     if (d == 64 && !pg)
         hipLaunchKernelGGL((quantize_kernel<64, false>), grid, block, 0, st, a);
     else if (d == 128 && !pg)

@@ -137,6 +137,36 @@ def test_quantize_edge_thresholds(B, ref):
     compare_pools(ref, case, cache.pool.cpu().numpy(), want)
 
 
+@pytest.mark.parametrize("cid", [2, 1])
+def test_quantize_edge_thresholds_token_by_token(B, ref, cid):
+    """The decode-step path (one new token per sequence per call) under the same edge
+    thresholds: every value an outlier (each record's COO stream fills its capacity one
+    slot at a time), a collapsed inner interval, constant and zero vectors; head_dim 128
+    and 64, even and odd slots."""
+    w = synth.scaled(synth.WORKLOADS[cid], n_seqs=3, ctx=37)
+    case = Case(w)
+    H = case.H
+    thr = np.zeros((H, 2, 4), np.float32)
+    thr[:, :, 0], thr[:, :, 1], thr[:, :, 2], thr[:, :, 3] = -np.inf, -np.inf, np.inf, np.inf
+    thr[1::2] = np.array([-1.0, 0.0, 0.0, 1.0], np.float32)
+    case.thr = thr
+    case.k[3] = 0.0
+    case.v[5] = 1.5
+    case.k[7, :, : case.d // 2] = -2.0
+    want = case.oracle_pool(ref)
+    cache, bt = _gpu_cache(B, case, prefill=False)
+    lens = case.lens
+    for step in range(int(lens.max())):
+        act = step < lens
+        cnt = act.to(torch.int32)
+        cu = torch.zeros(case.n_seqs + 1, dtype=torch.int32)
+        cu[1:] = torch.cumsum(cnt, 0)
+        sel = (case.cu[:-1] + step)[act]
+        B.quantize_kv(cache, case.k[sel].to(DEV), case.v[sel].to(DEV), bt,
+                      torch.full((case.n_seqs,), step, dtype=torch.int32, device=DEV), cu.to(DEV), 1)
+    compare_pools(ref, case, cache.pool.cpu().numpy(), want)
+
+
 @pytest.mark.parametrize("name", list(CASES))
 def test_attention_matches_oracle(B, ref, name):
     case = _case(ref, name)
