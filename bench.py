@@ -23,6 +23,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+MFMA_F32_PEAK_TFS = 157.3   # dense fp32 matrix-core peak of the MI355X
 
 
 def log(msg: str):
@@ -333,8 +334,23 @@ def prefill_bench(args, w, cache, bt, lens, dev, bt_cpu):
         passes += (int(clen[s]) + tpb - 1) // tpb
     one_pass += n_tok * Hq * d * (2 + 4)
     gbs = one_pass / t / 1e9
+    # matrix-core work: each (query token, query head) row takes 2d flops per visible key for
+    # its scores and 2d for its output
+    flops = 0
+    for s in range(n):
+        for i in range(int(clen[s])):
+            p = int(start[s]) + i
+            flops += 4 * d * Hq * (min(p + 1, win) if win else p + 1)
+    tfs = flops / t / 1e12
     log(f"prefill attention: {n_tok} query tokens in {t * 1e6:.1f} us; one pass over the chunks' prefixes "
-        f"{one_pass / 1e9:.3f} GB = {gbs:.0f} GB/s ({passes} row blocks for {n} chunks)")
+        f"{one_pass / 1e9:.3f} GB = {gbs:.0f} GB/s ({passes} row blocks for {n} chunks); "
+        f"{flops / 1e9:.1f} GFLOP = {tfs:.1f} TFLOP/s on fp32 matrix cores")
+    hbm = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+           "frac": round(gbs / HBM_PEAK_GBS, 4), "bytes_one_pass": one_pass}
+    mfma = {"bound": "mfma", "achieved": round(tfs, 2), "peak": MFMA_F32_PEAK_TFS, "unit": "TFLOP/s",
+            "frac": round(tfs / MFMA_F32_PEAK_TFS, 4), "flops": flops}
+    # the resource nearer to saturation is the roofline; the other is reported beside it
+    roof, other = (mfma, hbm) if mfma["frac"] > hbm["frac"] else (hbm, mfma)
     res = {"metric": "chunked-prefill attention query tokens/sec", "value": round(n_tok / t, 1), "unit": "tokens/s",
            "n_gpus": 1, "steps": steps, "warmup": args.warmup, "ms_per_step": round(t * 1e3, 4),
            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32-mfma", "data": "synthetic",
@@ -342,9 +358,9 @@ def prefill_bench(args, w, cache, bt, lens, dev, bt_cpu):
                                   f"({n_tok} query tokens), {Hq}/{H} heads, d {d}, context {w.ctx_min}..{w.ctx}"
                                   + (f", sliding window {win}" if win else ""),
                       "global_batch": n, "seq_len": max_len, "parallelism": "single GPU"},
-           "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                        "frac": round(gbs / HBM_PEAK_GBS, 4), "bytes_one_pass": one_pass,
-                        "row_blocks_per_chunk": round(passes / max(1, sum(1 for s in range(n) if int(clen[s]) > 0)), 3)}}
+           "roofline": dict(roof, traffic=None,
+                            row_blocks_per_chunk=round(passes / max(1, sum(1 for s in range(n) if int(clen[s]) > 0)), 3)),
+           "roofline_other": other}
     print(json.dumps(res), flush=True)
 
 
