@@ -24,6 +24,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 MFMA_F32_PEAK_TFS = 157.3   # dense fp32 matrix-core peak of the MI355X
+MFMA_F16_PEAK_TFS = 2500.0  # dense fp16 matrix-core peak of the MI355X
 
 
 def log(msg: str):
@@ -322,7 +323,11 @@ def prefill_bench(args, w, cache, bt, lens, dev, bt_cpu):
     t = e0.elapsed_time(e1) / steps / 1e3
     # one pass over each chunk's visible keys: positions [lo, last] of every KV head
     prefix = outlier_prefix(cache, bt_cpu, n, max_len)
-    tpb = 64 // (Hq // H)                                # query tokens per row block
+    # query tokens per row block: blocks of 64 rows, or of 128 on the fp16 matrix cores when
+    # the chunks hold more rows per KV head than 64 (head_dim 128; the library's rule)
+    G = Hq // H
+    wide = d == 128 and G * -(-n_tok // n) > 64
+    tpb = (128 if wide else 64) // G
     one_pass, passes = 0, 0
     for s in range(n):
         last = int(cached[s]) - 1
@@ -342,22 +347,28 @@ def prefill_bench(args, w, cache, bt, lens, dev, bt_cpu):
             p = int(start[s]) + i
             flops += 4 * d * Hq * (min(p + 1, win) if win else p + 1)
     tfs = flops / t / 1e12
+    # the 64-row blocks contract on fp32 matrix cores; the 128-row blocks on fp16 ones, each
+    # real operand as a high and a low fp16 part (2 products per score term, 3 per output
+    # term: executed flops are 2.5x the algorithmic ones)
+    peak = MFMA_F16_PEAK_TFS if wide else MFMA_F32_PEAK_TFS
     log(f"prefill attention: {n_tok} query tokens in {t * 1e6:.1f} us; one pass over the chunks' prefixes "
         f"{one_pass / 1e9:.3f} GB = {gbs:.0f} GB/s ({passes} row blocks for {n} chunks); "
-        f"{flops / 1e9:.1f} GFLOP = {tfs:.1f} TFLOP/s on fp32 matrix cores")
+        f"{flops / 1e9:.1f} GFLOP = {tfs:.1f} TFLOP/s on {'fp16' if wide else 'fp32'} matrix cores")
     hbm = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
            "frac": round(gbs / HBM_PEAK_GBS, 4), "bytes_one_pass": one_pass}
-    mfma = {"bound": "mfma", "achieved": round(tfs, 2), "peak": MFMA_F32_PEAK_TFS, "unit": "TFLOP/s",
-            "frac": round(tfs / MFMA_F32_PEAK_TFS, 4), "flops": flops}
+    mfma = {"bound": "mfma", "achieved": round(tfs, 2), "peak": peak, "unit": "TFLOP/s",
+            "frac": round(tfs / peak, 4), "flops": flops}
     # the resource nearer to saturation is the roofline; the other is reported beside it
     roof, other = (mfma, hbm) if mfma["frac"] > hbm["frac"] else (hbm, mfma)
     res = {"metric": "chunked-prefill attention query tokens/sec", "value": round(n_tok / t, 1), "unit": "tokens/s",
            "n_gpus": 1, "steps": steps, "warmup": args.warmup, "ms_per_step": round(t * 1e3, 4),
-           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32-mfma", "data": "synthetic",
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+           "dtype": "f16x2-mfma+f32" if wide else "f32-mfma", "data": "synthetic",
            "config": {"workload": f"{w.name}: {n} sequences, chunks of the last {args.prefill_chunk} cached tokens "
                                   f"({n_tok} query tokens), {Hq}/{H} heads, d {d}, context {w.ctx_min}..{w.ctx}"
                                   + (f", sliding window {win}" if win else ""),
                       "global_batch": n, "seq_len": max_len, "parallelism": "single GPU"},
+           "row_block_rows": 128 if wide else 64,
            "roofline": dict(roof, traffic=None,
                             row_blocks_per_chunk=round(passes / max(1, sum(1 for s in range(n) if int(clen[s]) > 0)), 3)),
            "roofline_other": other}

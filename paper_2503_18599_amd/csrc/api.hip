@@ -387,8 +387,14 @@ size_t oaken_prefill_attention_workspace_bytes(int32_t n_tokens, int32_t n_q_hea
     if (n_tokens <= 0 || n_q_heads <= 0 || n_kv_heads <= 0 || n_q_heads % n_kv_heads != 0 ||
         n_q_heads / n_kv_heads > 8 || !supported_dim(head_dim) || max_seq_len <= 0 || sliding_window < 0)
         return 0;
-    const oaken::PrefillPlan p = oaken::plan_prefill(n_tokens, n_q_heads, n_kv_heads, max_seq_len, sliding_window);
-    return prefill_ws(n_tokens, n_q_heads, head_dim, p).total;
+    // (the call picks the block width from the chunk lengths: room for either plan)
+    const oaken::PrefillPlan p0 = oaken::plan_prefill(n_tokens, n_q_heads, n_kv_heads, max_seq_len, sliding_window, false);
+    size_t total = prefill_ws(n_tokens, n_q_heads, head_dim, p0).total;
+    if (head_dim == 128) {
+        const oaken::PrefillPlan p1 = oaken::plan_prefill(n_tokens, n_q_heads, n_kv_heads, max_seq_len, sliding_window, true);
+        total = std::max(total, prefill_ws(n_tokens, n_q_heads, head_dim, p1).total);
+    }
+    return total;
 }
 
 int oaken_prefill_attention(const oaken_cache* cache, const void* q, int32_t n_q_heads,
@@ -410,11 +416,14 @@ int oaken_prefill_attention(const oaken_cache* cache, const void* q, int32_t n_q
         return fail(OAKEN_ERR_INVALID_ARG, "block table too narrow for max_seq_len");
     if (!std::isfinite(softmax_scale)) return fail(OAKEN_ERR_INVALID_ARG, "softmax_scale not finite");
     if (sliding_window < 0) return fail(OAKEN_ERR_INVALID_ARG, "sliding_window must be >= 0");
+    const bool wide = oaken::prefill_wide(n_tokens, n_seqs, n_q_heads, cache->n_kv_heads, cache->head_dim);
     const oaken::PrefillPlan p = oaken::plan_prefill(n_tokens, n_q_heads, cache->n_kv_heads, max_seq_len,
-                                                     sliding_window);
+                                                     sliding_window, wide);
     const PrefillWs w = prefill_ws(n_tokens, n_q_heads, cache->head_dim, p);
-    if (!workspace || workspace_bytes < w.total)
-        return fail(OAKEN_ERR_WORKSPACE, "prefill attention workspace %zu < %zu bytes", workspace_bytes, w.total);
+    const size_t need = oaken_prefill_attention_workspace_bytes(n_tokens, n_q_heads, cache->n_kv_heads,
+                                                                cache->head_dim, max_seq_len, sliding_window);
+    if (!workspace || workspace_bytes < need)
+        return fail(OAKEN_ERR_WORKSPACE, "prefill attention workspace %zu < %zu bytes", workspace_bytes, need);
     if (reinterpret_cast<uintptr_t>(workspace) % 16 != 0)
         return fail(OAKEN_ERR_INVALID_ARG, "prefill attention workspace not 16-byte aligned");
     uint8_t* ws = static_cast<uint8_t*>(workspace);
@@ -447,6 +456,7 @@ int oaken_prefill_attention(const oaken_cache* cache, const void* q, int32_t n_q
     a.scale = softmax_scale;
     a.spool = static_cast<const uint8_t*>(cache->sparse_pool);
     a.spages = cache->sparse_pages;
+    a.wide = p.wide ? 1 : 0;
     const hipStream_t s = static_cast<hipStream_t>(stream);
     int rc = hip_status(oaken::launch_prefill(a, cache->head_dim, reinterpret_cast<int2*>(ws + w.part),
                                               reinterpret_cast<int32_t*>(ws + w.part + w.blocks), s),

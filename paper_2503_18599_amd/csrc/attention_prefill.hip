@@ -22,6 +22,13 @@
 // the wave's quarter of the scores and token 4 g + s of the value product.  Both products
 // are formed transposed (keys and values as the A operand, queries and probabilities as
 // B), so a query row lives on the four lanes q + 16 g of column q.
+//
+// With more rows per KV head than one block of 64 holds (several query heads times a long
+// chunk), prefill_wide_kernel takes up to 256 rows: each wave owns 64 rows over all the
+// channels, and the tiles are contracted on the fp16 matrix cores with every real operand
+// split into a high and a low fp16 part (x = hi + lo to about 2^-22 relative; the query is
+// fp16 already): S^T = K_hi Q^T + K_lo Q^T and O^T += V_hi P_hi + V_hi P_lo + V_lo P_hi,
+// accumulated in fp32.  A page is then read and dequantized once for all the rows.
 #include "oaken_internal.h"
 
 #include <hip/hip_fp16.h>
@@ -74,16 +81,104 @@ struct PfLayout {
 constexpr int kWaves = kPfThreads / 64;
 constexpr int kMaxRowTiles = kRowsPerBlock / 16;
 
+// What every prefill kernel stages per page: the two records' bytes, the per-slot
+// dequantization constants, the COO bytes used and each COO byte's (slot, chunk) bucket.
 template <int D, bool PG>
-struct PfSmem {
-    float kt[kPage][D + 4];                          // keys, token-major
-    float vt[D][kPage + 4];                          // values, channel-major
-    f4 sp[kWaves][kMaxRowTiles][64];                 // per wave: partial scores over its channels
+struct PfStage {
     float tokc[2][kPage][8];                         // per record (K, V) and slot: Min, Delta of
                                                      // inner, middle, outer
     int used[2];                                     // COO bytes of each record
     __align__(16) uint8_t rec[2][PfLayout<D, PG>::STAGE];
     uint8_t owner[2][PfLayout<D, PG>::CAP];          // per COO byte: its (slot, chunk) bucket
+};
+
+// The dequantized page as fp32 tiles: keys token-major, values channel-major.
+template <int D>
+struct TilesF32 {
+    __align__(16) float kt[kPage][D + 4];
+    __align__(16) float vt[D][kPage + 4];
+    __device__ void put_k8(int t, int j0, const float (&x)[8]) {
+        *reinterpret_cast<float4*>(&kt[t][j0]) = make_float4(x[0], x[1], x[2], x[3]);
+        *reinterpret_cast<float4*>(&kt[t][j0 + 4]) = make_float4(x[4], x[5], x[6], x[7]);
+    }
+    __device__ void put_v8(int j, int t0, const float (&x)[8]) {
+        *reinterpret_cast<float4*>(&vt[j][t0]) = make_float4(x[0], x[1], x[2], x[3]);
+        *reinterpret_cast<float4*>(&vt[j][t0 + 4]) = make_float4(x[4], x[5], x[6], x[7]);
+    }
+    __device__ void put_k(int t, int j, float x) { kt[t][j] = x; }
+    __device__ void put_v(int j, int t, float x) { vt[j][t] = x; }
+};
+
+typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+
+// x = hi + lo with both parts fp16: hi the nearest fp16, lo the nearest fp16 to the exact
+// rest (about 2^-22 |x| off in all).
+struct Split16 {
+    _Float16 hi, lo;
+};
+__device__ __forceinline__ Split16 split16(float x) {
+    const _Float16 hi = (_Float16)x;
+    return Split16{hi, (_Float16)(x - (float)hi)};
+}
+
+// The dequantized page as fp16 high and low parts: key rows of 272 bytes (16-byte aligned
+// operand reads, rows spread over the banks), value channel rows of 40 bytes.
+template <int D>
+struct TilesF16 {
+    static constexpr int KS = D + 8, VS = kPage + 4;
+    __align__(16) _Float16 kh[kPage][KS];
+    __align__(16) _Float16 kl[kPage][KS];
+    __align__(16) _Float16 vh[D][VS];
+    __align__(16) _Float16 vl[D][VS];
+    __device__ void put_k8(int t, int j0, const float (&x)[8]) {
+        h8 hi, lo;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const Split16 z = split16(x[e]);
+            hi[e] = z.hi;
+            lo[e] = z.lo;
+        }
+        *reinterpret_cast<h8*>(&kh[t][j0]) = hi;
+        *reinterpret_cast<h8*>(&kl[t][j0]) = lo;
+    }
+    __device__ void put_v8(int j, int t0, const float (&x)[8]) {
+        h4 h0, h1, l0, l1;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const Split16 z0 = split16(x[e]), z1 = split16(x[e + 4]);
+            h0[e] = z0.hi;
+            l0[e] = z0.lo;
+            h1[e] = z1.hi;
+            l1[e] = z1.lo;
+        }
+        *reinterpret_cast<h4*>(&vh[j][t0]) = h0;
+        *reinterpret_cast<h4*>(&vh[j][t0 + 4]) = h1;
+        *reinterpret_cast<h4*>(&vl[j][t0]) = l0;
+        *reinterpret_cast<h4*>(&vl[j][t0 + 4]) = l1;
+    }
+    __device__ void put_k(int t, int j, float x) {
+        const Split16 z = split16(x);
+        kh[t][j] = z.hi;
+        kl[t][j] = z.lo;
+    }
+    __device__ void put_v(int j, int t, float x) {
+        const Split16 z = split16(x);
+        vh[j][t] = z.hi;
+        vl[j][t] = z.lo;
+    }
+};
+
+template <int D, bool PG>
+struct PfSmem {
+    PfStage<D, PG> st;
+    TilesF32<D> tl;
+    f4 sp[kWaves][kMaxRowTiles][64];                 // per wave: partial scores over its channels
+};
+template <int D, bool PG>
+struct PfWideSmem {
+    PfStage<D, PG> st;
+    TilesF16<D> tl;
 };
 
 // The record bytes a thread prefetches for the next page: chunk c of record w holds bytes
@@ -96,12 +191,144 @@ struct PfPrefetch {
     static constexpr int CH = PfLayout<D, PG>::PRE / 16 + WIN / 16;   // chunks per record
 };
 
-template <int D, bool PG>
-__global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(3))) void prefill_kernel(PrefillArgs a) {
+// Phases (2)-(4) of a page, every thread of the workgroup taking part; the page's records
+// are already staged in S.rec (phase 1) and block b is valid.  Leaves the dequantized page
+// in the tiles, after a barrier.
+template <int D, bool PG, class Tiles>
+__device__ __forceinline__ void pf_dequant_page(PfStage<D, PG>& S, Tiles& T, const PrefillArgs& a, int b, int h,
+                                                const float (&tk)[4], const float (&tv)[4], int tid) {
     using PL = PfLayout<D, PG>;
     using PF = PfPrefetch<D, PG>;
     constexpr Layout LY = PL::LY;
     constexpr int NC = PL::NC;
+    const int lane = tid & 63, wave = tid >> 6;
+    auto record = [&](int w) { return a.pool + (((int64_t)b * a.H + h) * 2 + w) * a.stride; };
+
+    // (2) wave 0: each record's (slot, chunk) buckets, their stream offsets (a DPP prefix
+    //     sum: K buckets on lanes 0.., V buckets on lanes 32..) and the bucket owning each
+    //     stream byte; wave 1: per-slot dequantization constants
+    if (wave == 0) {
+        const int w = lane >> 5, bk = lane & 31;
+        const int cnt = bk < kPage * NC ? (int)S.rec[w][LY.counts + bk] : 0;
+        int x = cnt;
+        x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false);   // row_shr:1
+        x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false);   // row_shr:2
+        x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false);   // row_shr:4
+        x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false);   // row_shr:8
+        x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);   // row_bcast:15 into rows 1, 3
+        const int st = x - cnt;
+        if (bk == 31) S.used[w] = min(x, PL::CAP);
+        for (int k = 0; k < cnt && st + k < PL::CAP; ++k) S.owner[w][st + k] = (uint8_t)bk;
+    } else if (wave == 1 && lane < 2 * kPage) {
+        const int w = lane / kPage, t = lane % kPage;
+        const uint16_t* mt = reinterpret_cast<const uint16_t*>(S.rec[w] + LY.meta + 12 * t);
+#pragma unroll
+        for (int k = 0; k < 6; ++k) S.tokc[w][t][k] = h2f(mt[k]);
+    }
+    __syncthreads();
+
+    // (3) stream bytes past the prefetched window (and, with on-demand sparse pages, the
+    //     whole stream, through the page table)
+    if (PG || S.used[0] > PF::WIN || S.used[1] > PF::WIN) {
+        const int c0 = PF::WIN / 16;
+        const int nk = max(0, (S.used[0] + 15) / 16 - c0), nv = max(0, (S.used[1] + 15) / 16 - c0);
+        for (int c = tid; c < nk + nv; c += kPfThreads) {
+            const int w = c >= nk, cc = c0 + (c - w * nk);
+            const uint8_t* src;
+            if constexpr (PG) {
+                const int32_t e = reinterpret_cast<const int32_t*>(S.rec[w] + LY.sparse)[(16 * cc) / kSparsePage] - 1;
+                src = a.spool + (int64_t)((e >= 0 && e < a.spages) ? e : 0) * kSparsePage + (16 * cc) % kSparsePage;
+            } else {
+                src = record(w) + LY.sparse + 16 * cc;
+            }
+            *reinterpret_cast<uint4*>(&S.rec[w][PL::PRE + 16 * cc]) = *reinterpret_cast<const uint4*>(src);
+        }
+    }
+    // middle reading of every nibble into the tiles
+    {
+        // keys: thread = (slot, 8 channels); dense byte t * d/2 + j/2, low nibble = even j
+        constexpr int GPT = D / 8;
+        if (tid < kPage * GPT) {
+            const int t = tid / GPT, cg = tid % GPT;
+            const uint32_t dw = *reinterpret_cast<const uint32_t*>(&S.rec[0][LY.dense + t * (D / 2) + 4 * cg]);
+            const float mn = S.tokc[0][t][2], dl = S.tokc[0][t][3];
+            float x[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const uint32_t u = (dw >> (4 * e)) & 15u;
+                const bool hi = u >= 8;
+                const float mag = mn + (float)(hi ? u - 8 : 7 - u) * dl;
+                x[e] = hi ? tk[2] + mag : tk[1] - mag;
+            }
+            T.put_k8(t, 8 * cg, x);
+        }
+        // values: thread = (channel j, 8 slots); dense byte j * 8 + t/2, low nibble = even t
+        if (tid < 2 * D) {
+            const int j = tid >> 1, t0 = 8 * (tid & 1);
+            const uint32_t dw = *reinterpret_cast<const uint32_t*>(&S.rec[1][LY.dense + j * (kPage / 2) + (t0 >> 1)]);
+            float x[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const uint32_t u = (dw >> (4 * e)) & 15u;
+                const bool hi = u >= 8;
+                const float mag = S.tokc[1][t0 + e][2] + (float)(hi ? u - 8 : 7 - u) * S.tokc[1][t0 + e][3];
+                x[e] = hi ? tv[2] + mag : tv[1] - mag;
+            }
+            T.put_v8(j, t0, x);
+        }
+    }
+    __syncthreads();
+
+    // (4) COO entries replace their elements' middle readings by their true values
+    //     (thread = entry of either record's stream)
+    {
+        const int uk = S.used[0], utot = uk + S.used[1];
+        for (int e = tid; e < utot; e += kPfThreads) {
+            const int w = e >= uk, ee = e - w * uk;
+            const uint8_t* r = S.rec[w];
+            const int bk = S.owner[w][ee], t = bk / NC, c = bk % NC;
+            const uint32_t en = r[PL::PRE + ee];
+            const int j = 64 * c + (int)(en & 63u);
+            const uint32_t byte = w ? r[LY.dense + j * (kPage / 2) + (t >> 1)] : r[LY.dense + t * (D / 2) + (j >> 1)];
+            const uint32_t n = (byte >> (4 * (w ? (t & 1) : (j & 1)))) & 15u;
+            const bool side = (en >> 7) != 0, outer = ((en >> 6) & 1u) != 0;
+            const float* thw = w ? tv : tk;
+            const float cf = (float)(side ? n : 15u - n);
+            const float mag = outer ? S.tokc[w][t][4] + cf * S.tokc[w][t][5] : S.tokc[w][t][0] + cf * S.tokc[w][t][1];
+            const float x = outer ? (side ? thw[3] + mag : thw[0] - mag) : (side ? mag : -mag);
+            if (w) T.put_v(j, t, x);
+            else T.put_k(t, j, x);
+        }
+    }
+    __syncthreads();
+}
+
+// The row block's pages [pg_first, pg_end) and its rows' positions (shared by both kernels).
+struct PfBlock {
+    int s, i0, tok0, C, start, G, i_end, n_rows, pg_first, pg_end;
+};
+__device__ __forceinline__ PfBlock pf_block(const PrefillArgs& a, int split) {
+    PfBlock B;
+    const int2 blk = a.row_blocks[blockIdx.x];
+    B.s = blk.x;
+    B.i0 = blk.y;
+    B.tok0 = a.cu_tokens[B.s];
+    B.C = a.cu_tokens[B.s + 1] - B.tok0;
+    B.start = a.start_pos[B.s];
+    B.G = a.Hq / a.H;
+    B.i_end = min(B.C, B.i0 + a.tokens_per_block);
+    B.n_rows = max(0, (B.i_end - B.i0) * B.G);
+    const int p_last = B.start + B.i_end - 1;
+    const int lo_first = a.window > 0 ? max(0, B.start + B.i0 + 1 - a.window) : 0;
+    B.pg_first = lo_first / kPage + split * a.pages_per_split;
+    B.pg_end = min(p_last / kPage + 1, lo_first / kPage + (split + 1) * a.pages_per_split);
+    return B;
+}
+
+template <int D, bool PG>
+__global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(3))) void prefill_kernel(PrefillArgs a) {
+    using PL = PfLayout<D, PG>;
+    using PF = PfPrefetch<D, PG>;
     constexpr int CPW = D / kWaves;    // channels of each wave (scores and outputs)
     constexpr int KSW = CPW / 4;       // 4-wide contraction steps of a wave's scores
     constexpr int NCT = CPW / 16;      // 16-wide output tiles of a wave
@@ -111,19 +338,10 @@ __global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(3)))
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 4;
     if ((int)blockIdx.x >= *a.n_row_blocks) return;   // (uniform)
     const int h = blockIdx.y, split = blockIdx.z;
-    const int2 blk = a.row_blocks[blockIdx.x];
-    const int s = blk.x, i0 = blk.y;
-    const int tok0 = a.cu_tokens[s];
-    const int C = a.cu_tokens[s + 1] - tok0;
-    const int start = a.start_pos[s];
-    const int G = a.Hq / a.H;
-    const int i_end = min(C, i0 + a.tokens_per_block);
-    const int n_rows = max(0, (i_end - i0) * G);
+    const PfBlock Bk = pf_block(a, split);
+    const int G = Bk.G, n_rows = Bk.n_rows, tok0 = Bk.tok0, i0 = Bk.i0, start = Bk.start;
     const int R = (n_rows + 15) / 16;                 // 16-row tiles
-    const int p_last = start + i_end - 1;
-    const int lo_first = a.window > 0 ? max(0, start + i0 + 1 - a.window) : 0;
-    const int pg_first = lo_first / kPage + split * a.pages_per_split;
-    const int pg_end = min(p_last / kPage + 1, lo_first / kPage + (split + 1) * a.pages_per_split);
+    const int pg_first = Bk.pg_first, pg_end = Bk.pg_end;
     const float* th = a.thr + h * 8;
     const float tk[4] = {th[0], th[1], th[2], th[3]}, tv[4] = {th[4], th[5], th[6], th[7]};
 
@@ -163,7 +381,7 @@ __global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(3)))
         for (int n = 0; n < NCT; ++n) o[rt][n] = f4{0.0f, 0.0f, 0.0f, 0.0f};
     }
 
-    const int32_t* btab = a.block_table + (int64_t)s * a.max_blocks;
+    const int32_t* btab = a.block_table + (int64_t)Bk.s * a.max_blocks;
     auto record = [&](int b, int w) { return a.pool + (((int64_t)b * a.H + h) * 2 + w) * a.stride; };
     auto valid_block = [&](int b) { return b >= 0 && b < a.num_blocks; };
     const int pw_ = tid / PF::CH, pc_ = tid % PF::CH;   // this thread's prefetch chunk
@@ -178,115 +396,16 @@ __global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(3)))
     for (int pg = pg_first; pg < pg_end; ++pg) {
         const int b = btab[pg];
         // (1) stage this page's prefetched bytes, request the next page's
-        if (tid < 2 * PF::CH) *reinterpret_cast<uint4*>(&S.rec[pw_][16 * pc_]) = cur;
+        if (tid < 2 * PF::CH) *reinterpret_cast<uint4*>(&S.st.rec[pw_][16 * pc_]) = cur;
         cur = prefetch(pg + 1);
         __syncthreads();
         if (!valid_block(b)) continue;   // (uniform; a precondition violation reads nothing)
-
-        // (2) wave 0: each record's (slot, chunk) buckets, their stream offsets (a DPP prefix
-        //     sum: K buckets on lanes 0.., V buckets on lanes 32..) and the bucket owning each
-        //     stream byte; wave 1: per-slot dequantization constants
-        if (wave == 0) {
-            const int w = lane >> 5, bk = lane & 31;
-            const int cnt = bk < kPage * NC ? (int)S.rec[w][LY.counts + bk] : 0;
-            int x = cnt;
-            x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false);   // row_shr:1
-            x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false);   // row_shr:2
-            x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false);   // row_shr:4
-            x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false);   // row_shr:8
-            x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);   // row_bcast:15 into rows 1, 3
-            const int st = x - cnt;
-            if (bk == 31) S.used[w] = min(x, PL::CAP);
-            for (int k = 0; k < cnt && st + k < PL::CAP; ++k) S.owner[w][st + k] = (uint8_t)bk;
-        } else if (wave == 1 && lane < 2 * kPage) {
-            const int w = lane / kPage, t = lane % kPage;
-            const uint16_t* mt = reinterpret_cast<const uint16_t*>(S.rec[w] + LY.meta + 12 * t);
-#pragma unroll
-            for (int k = 0; k < 6; ++k) S.tokc[w][t][k] = h2f(mt[k]);
-        }
-        __syncthreads();
-
-        // (3) stream bytes past the prefetched window (and, with on-demand sparse pages, the
-        //     whole stream, through the page table)
-        if (PG || S.used[0] > PF::WIN || S.used[1] > PF::WIN) {
-            const int c0 = PF::WIN / 16;
-            const int nk = max(0, (S.used[0] + 15) / 16 - c0), nv = max(0, (S.used[1] + 15) / 16 - c0);
-            for (int c = tid; c < nk + nv; c += kPfThreads) {
-                const int w = c >= nk, cc = c0 + (c - w * nk);
-                const uint8_t* src;
-                if constexpr (PG) {
-                    const int32_t e = reinterpret_cast<const int32_t*>(S.rec[w] + LY.sparse)[(16 * cc) / kSparsePage] - 1;
-                    src = a.spool + (int64_t)((e >= 0 && e < a.spages) ? e : 0) * kSparsePage + (16 * cc) % kSparsePage;
-                } else {
-                    src = record(b, w) + LY.sparse + 16 * cc;
-                }
-                *reinterpret_cast<uint4*>(&S.rec[w][PL::PRE + 16 * cc]) = *reinterpret_cast<const uint4*>(src);
-            }
-        }
-        // middle reading of every nibble into the tiles
-        {
-            // keys: thread = (slot, 8 channels); dense byte t * d/2 + j/2, low nibble = even j
-            constexpr int GPT = D / 8;
-            if (tid < kPage * GPT) {
-                const int t = tid / GPT, cg = tid % GPT;
-                const uint32_t dw = *reinterpret_cast<const uint32_t*>(&S.rec[0][LY.dense + t * (D / 2) + 4 * cg]);
-                const float mn = S.tokc[0][t][2], dl = S.tokc[0][t][3];
-                float x[8];
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const uint32_t u = (dw >> (4 * e)) & 15u;
-                    const bool hi = u >= 8;
-                    const float mag = mn + (float)(hi ? u - 8 : 7 - u) * dl;
-                    x[e] = hi ? tk[2] + mag : tk[1] - mag;
-                }
-                *reinterpret_cast<float4*>(&S.kt[t][8 * cg]) = make_float4(x[0], x[1], x[2], x[3]);
-                *reinterpret_cast<float4*>(&S.kt[t][8 * cg + 4]) = make_float4(x[4], x[5], x[6], x[7]);
-            }
-            // values: thread = (channel j, 8 slots); dense byte j * 8 + t/2, low nibble = even t
-            if (tid < 2 * D) {
-                const int j = tid >> 1, t0 = 8 * (tid & 1);
-                const uint32_t dw = *reinterpret_cast<const uint32_t*>(&S.rec[1][LY.dense + j * (kPage / 2) + (t0 >> 1)]);
-                float x[8];
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const uint32_t u = (dw >> (4 * e)) & 15u;
-                    const bool hi = u >= 8;
-                    const float mag = S.tokc[1][t0 + e][2] + (float)(hi ? u - 8 : 7 - u) * S.tokc[1][t0 + e][3];
-                    x[e] = hi ? tv[2] + mag : tv[1] - mag;
-                }
-                *reinterpret_cast<float4*>(&S.vt[j][t0]) = make_float4(x[0], x[1], x[2], x[3]);
-                *reinterpret_cast<float4*>(&S.vt[j][t0 + 4]) = make_float4(x[4], x[5], x[6], x[7]);
-            }
-        }
-        __syncthreads();
-
-        // (4) COO entries replace their elements' middle readings by their true values
-        //     (thread = entry of either record's stream)
-        {
-            const int uk = S.used[0], utot = uk + S.used[1];
-            for (int e = tid; e < utot; e += kPfThreads) {
-                const int w = e >= uk, ee = e - w * uk;
-                const uint8_t* r = S.rec[w];
-                const int bk = S.owner[w][ee], t = bk / NC, c = bk % NC;
-                const uint32_t en = r[PL::PRE + ee];
-                const int j = 64 * c + (int)(en & 63u);
-                const uint32_t byte = w ? r[LY.dense + j * (kPage / 2) + (t >> 1)] : r[LY.dense + t * (D / 2) + (j >> 1)];
-                const uint32_t n = (byte >> (4 * (w ? (t & 1) : (j & 1)))) & 15u;
-                const bool side = (en >> 7) != 0, outer = ((en >> 6) & 1u) != 0;
-                const float* thw = w ? tv : tk;
-                const float cf = (float)(side ? n : 15u - n);
-                const float mag = outer ? S.tokc[w][t][4] + cf * S.tokc[w][t][5] : S.tokc[w][t][0] + cf * S.tokc[w][t][1];
-                const float x = outer ? (side ? thw[3] + mag : thw[0] - mag) : (side ? mag : -mag);
-                if (w) S.vt[j][t] = x;
-                else S.kt[t][j] = x;
-            }
-        }
-        __syncthreads();
+        pf_dequant_page<D, PG>(S.st, S.tl, a, b, h, tk, tv, tid);
 
         // (5) partial scores of every row tile over this wave's channels: lane (g, query
         //     row q) gets S^T[4 g + r][q] over channels CPW w .. + CPW
         {
-            const float* krow = &S.kt[lane & 15][CPW * wave + KSW * g];
+            const float* krow = &S.tl.kt[lane & 15][CPW * wave + KSW * g];
             float ka[KSW];
 #pragma unroll
             for (int k = 0; k < KSW; k += 4) {
@@ -339,7 +458,7 @@ __global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(3)))
 #pragma unroll
             for (int n = 0; n < NCT; ++n) {
                 o[rt][n] *= alpha;
-                const float4 va = *reinterpret_cast<const float4*>(&S.vt[CPW * wave + 16 * n + (lane & 15)][4 * g]);
+                const float4 va = *reinterpret_cast<const float4*>(&S.tl.vt[CPW * wave + 16 * n + (lane & 15)][4 * g]);
                 o[rt][n] = mfma4(va.x, p[0], o[rt][n]);
                 o[rt][n] = mfma4(va.y, p[1], o[rt][n]);
                 o[rt][n] = mfma4(va.z, p[2], o[rt][n]);
@@ -367,6 +486,183 @@ __global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(3)))
             for (int n = 0; n < NCT; ++n)
                 for (int r = 0; r < 4; ++r) pp[CPW * wave + 16 * n + 4 * g + r] = o[rt][n][r];
             if (wave == 0 && g == 0) {
+                pp[D] = m[rt];
+                pp[D + 1] = l[rt];
+            }
+        }
+    }
+}
+
+// Up to kWideRows rows per block: wave w owns rows 32 w .. 32 w + 31 (two row tiles) over all
+// D channels.  Per page and row tile: S^T = K Q^T on v_mfma_f32_16x16x32_f16 (A = 8 fp16 of
+// a key row, K_hi then K_lo; B = the row's query, unscaled fp16), the online softmax as in
+// prefill_kernel (scale applied to the fp32 scores), then O^T += V^T P^T on
+// v_mfma_f32_16x16x16f16 with P split into hi and lo in registers.  The key and value
+// operands read from LDS serve all four row tiles of the wave.
+constexpr int kWideRows = 128;
+constexpr int kWideTiles = kWideRows / kWaves / 16;   // row tiles per wave
+
+template <bool PG>
+__global__ __launch_bounds__(kPfThreads) void prefill_wide_kernel(PrefillArgs a) {
+    constexpr int D = 128;
+    using PL = PfLayout<D, PG>;
+    using PF = PfPrefetch<D, PG>;
+    constexpr int NCT = D / 16;        // output channel tiles
+    constexpr int KST = D / 32;        // 32-wide contraction steps of the scores
+    static_assert(PL::PRE % 16 == 0 && 2 * PF::CH <= kPfThreads, "one prefetch chunk per thread");
+
+    __shared__ PfWideSmem<D, PG> S;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 4, q16 = lane & 15;
+    if ((int)blockIdx.x >= *a.n_row_blocks) return;   // (uniform)
+    const int h = blockIdx.y, split = blockIdx.z;
+    const PfBlock Bk = pf_block(a, split);
+    const int G = Bk.G, tok0 = Bk.tok0, i0 = Bk.i0, start = Bk.start;
+    const int wrow0 = kWideTiles * 16 * wave;                          // the wave's first row
+    const int R = max(0, min(kWideTiles, (Bk.n_rows - wrow0 + 15) / 16));   // its row tiles
+    const int pg_first = Bk.pg_first, pg_end = Bk.pg_end;
+    const float* th = a.thr + h * 8;
+    const float tk[4] = {th[0], th[1], th[2], th[3]}, tv[4] = {th[4], th[5], th[6], th[7]};
+
+    // B operand of the scores: row tile rt, query row q16, channels 32 k + 8 g .. + 7
+    h8 bq[kWideTiles][KST];
+    int rpos[kWideTiles], rlo[kWideTiles];
+    bool rok[kWideTiles];
+#pragma unroll
+    for (int rt = 0; rt < kWideTiles; ++rt) {
+        const int rc = wrow0 + 16 * rt + q16;
+        rok[rt] = rc < Bk.n_rows;
+        const int i = i0 + (rok[rt] ? rc / G : 0), hd = rok[rt] ? rc % G : 0;
+        const uint16_t* qp = a.q + ((int64_t)(tok0 + i) * a.Hq + h * G + hd) * D + 8 * g;
+#pragma unroll
+        for (int k = 0; k < KST; ++k) {
+            const uint4 w = rok[rt] ? *reinterpret_cast<const uint4*>(qp + 32 * k) : make_uint4(0, 0, 0, 0);
+            bq[rt][k] = __builtin_bit_cast(h8, w);
+        }
+        rpos[rt] = start + i;
+        rlo[rt] = a.window > 0 ? max(0, rpos[rt] + 1 - a.window) : 0;
+    }
+    float m[kWideTiles], l[kWideTiles];
+    f4 o[kWideTiles][NCT];   // O^T: channels 16 n + 4 g + r of the lane's query row
+#pragma unroll
+    for (int rt = 0; rt < kWideTiles; ++rt) {
+        m[rt] = -INFINITY;
+        l[rt] = 0.0f;
+#pragma unroll
+        for (int n = 0; n < NCT; ++n) o[rt][n] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+    }
+
+    const int32_t* btab = a.block_table + (int64_t)Bk.s * a.max_blocks;
+    auto record = [&](int b, int w) { return a.pool + (((int64_t)b * a.H + h) * 2 + w) * a.stride; };
+    auto valid_block = [&](int b) { return b >= 0 && b < a.num_blocks; };
+    const int pw_ = tid / PF::CH, pc_ = tid % PF::CH;   // this thread's prefetch chunk
+    auto prefetch = [&](int pg) -> uint4 {
+        if (pg >= pg_end || tid >= 2 * PF::CH) return make_uint4(0, 0, 0, 0);
+        const int b = btab[pg];
+        if (!valid_block(b)) return make_uint4(0, 0, 0, 0);
+        return *reinterpret_cast<const uint4*>(record(b, pw_) + 16 * pc_);
+    };
+
+    // (two pages in flight: with few workgroups per CU one page ahead does not cover the
+    // memory latency)
+    uint4 cur = prefetch(pg_first), nxt = prefetch(pg_first + 1);
+    for (int pg = pg_first; pg < pg_end; ++pg) {
+        const int b = btab[pg];
+        if (tid < 2 * PF::CH) *reinterpret_cast<uint4*>(&S.st.rec[pw_][16 * pc_]) = cur;
+        cur = nxt;
+        nxt = prefetch(pg + 2);
+        __syncthreads();
+        if (!valid_block(b)) continue;   // (uniform; a precondition violation reads nothing)
+        pf_dequant_page<D, PG>(S.st, S.tl, a, b, h, tk, tv, tid);
+        if (R == 0) continue;   // (uniform per wave; the next barrier is at the loop top)
+
+        // scores of the wave's row tiles: lane (g, q16) gets S^T[4 g + r][q16]
+        f4 sc[kWideTiles];
+#pragma unroll
+        for (int rt = 0; rt < kWideTiles; ++rt) sc[rt] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int k = 0; k < KST; ++k) {
+            const h8 ah = *reinterpret_cast<const h8*>(&S.tl.kh[q16][32 * k + 8 * g]);
+            const h8 al = *reinterpret_cast<const h8*>(&S.tl.kl[q16][32 * k + 8 * g]);
+#pragma unroll
+            for (int rt = 0; rt < kWideTiles; ++rt) {
+                if (rt < R) {
+                    sc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, bq[rt][k], sc[rt], 0, 0, 0);
+                    sc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(al, bq[rt][k], sc[rt], 0, 0, 0);
+                }
+            }
+        }
+        // online softmax per row tile, probabilities split for the value product
+        h4 ph[kWideTiles], pl[kWideTiles];
+#pragma unroll
+        for (int rt = 0; rt < kWideTiles; ++rt) {
+            if (rt >= R) break;
+            float v[4];
+            float mx = -INFINITY;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int kp = pg * kPage + 4 * g + r;   // key position
+                const bool vis = rok[rt] && kp <= rpos[rt] && kp >= rlo[rt];
+                v[r] = vis ? a.scale * sc[rt][r] : -INFINITY;
+                mx = fmaxf(mx, v[r]);
+            }
+            mx = max4(mx);
+            const float mn = fmaxf(m[rt], mx);
+            const float alpha = (mn == -INFINITY) ? 1.0f : __expf(m[rt] - mn);
+            float ps = 0.0f;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const float p = (v[r] == -INFINITY) ? 0.0f : __expf(v[r] - mn);
+                ps += p;
+                const Split16 z = split16(p);
+                ph[rt][r] = z.hi;
+                pl[rt][r] = z.lo;
+            }
+            ps = sum4(ps);
+            l[rt] = l[rt] * alpha + ps;
+            m[rt] = mn;
+            // (the accumulators are rescaled only when some row's maximum moved)
+            if (__builtin_amdgcn_ballot_w64(alpha != 1.0f)) {
+#pragma unroll
+                for (int n = 0; n < NCT; ++n) o[rt][n] *= alpha;
+            }
+        }
+        // O^T += V^T P^T: A = channels 16 n + q16 x keys 4 g .. + 3 (hi, lo); B = the lane's
+        // probabilities (hi, lo); the hi x hi, hi x lo and lo x hi products
+#pragma unroll
+        for (int n = 0; n < NCT; ++n) {
+            const h4 vh = *reinterpret_cast<const h4*>(&S.tl.vh[16 * n + q16][4 * g]);
+            const h4 vl = *reinterpret_cast<const h4*>(&S.tl.vl[16 * n + q16][4 * g]);
+#pragma unroll
+            for (int rt = 0; rt < kWideTiles; ++rt) {
+                if (rt < R) {
+                    o[rt][n] = __builtin_amdgcn_mfma_f32_16x16x16f16(vh, ph[rt], o[rt][n], 0, 0, 0);
+                    o[rt][n] = __builtin_amdgcn_mfma_f32_16x16x16f16(vh, pl[rt], o[rt][n], 0, 0, 0);
+                    o[rt][n] = __builtin_amdgcn_mfma_f32_16x16x16f16(vl, ph[rt], o[rt][n], 0, 0, 0);
+                }
+            }
+        }
+        // (the next page's staging waits at its first barrier for every wave)
+    }
+
+    // ---- outputs, or this range's partials ------------------------------------------------
+#pragma unroll
+    for (int rt = 0; rt < kWideTiles; ++rt) {
+        if (rt >= R || !rok[rt]) continue;
+        const int rc = wrow0 + 16 * rt + q16;
+        const int64_t row = (int64_t)(tok0 + i0 + rc / G) * a.Hq + h * G + rc % G;
+        if (a.n_splits == 1) {
+            const float inv = l[rt] > 0.0f ? 1.0f / l[rt] : 0.0f;
+#pragma unroll
+            for (int n = 0; n < NCT; ++n)
+                *reinterpret_cast<float4*>(&a.out[row * D + 16 * n + 4 * g]) =
+                    make_float4(o[rt][n][0] * inv, o[rt][n][1] * inv, o[rt][n][2] * inv, o[rt][n][3] * inv);
+        } else {
+            float* pp = a.partial + (row * a.n_splits + split) * (D + 2);
+#pragma unroll
+            for (int n = 0; n < NCT; ++n)
+                *reinterpret_cast<float4*>(&pp[16 * n + 4 * g]) =
+                    make_float4(o[rt][n][0], o[rt][n][1], o[rt][n][2], o[rt][n][3]);
+            if (g == 0) {
                 pp[D] = m[rt];
                 pp[D + 1] = l[rt];
             }
@@ -405,10 +701,11 @@ __global__ __launch_bounds__(1024) void prefill_blocks_kernel(const int32_t* cu_
 }  // namespace
 
 PrefillPlan plan_prefill(int32_t n_tokens, int32_t n_q_heads, int32_t n_kv_heads, int32_t max_seq_len,
-                         int32_t window) {
+                         int32_t window, bool wide) {
     PrefillPlan p{};
     const int G = n_q_heads / n_kv_heads;
-    p.tokens_per_block = kRowsPerBlock / G;
+    p.wide = wide;
+    p.tokens_per_block = (wide ? kWideRows : kRowsPerBlock) / G;
     // keys a block can see: its own tokens and everything before them (or a window of W
     // before its first token)
     const int64_t span = window > 0 ? std::min<int64_t>(max_seq_len, (int64_t)window + p.tokens_per_block + kPage)
@@ -428,6 +725,14 @@ hipError_t launch_prefill(const PrefillArgs& a, int d, int2* row_blocks, int32_t
     if (e != hipSuccess) return e;
     const dim3 grid(a.max_row_blocks, a.H, a.n_splits);
     const bool pg = a.spool != nullptr;
+    if (a.wide) {
+        if (d != 128) return hipErrorInvalidValue;
+        if (pg)
+            hipLaunchKernelGGL(prefill_wide_kernel<true>, grid, dim3(kPfThreads), 0, st, a);
+        else
+            hipLaunchKernelGGL(prefill_wide_kernel<false>, grid, dim3(kPfThreads), 0, st, a);
+        return hipGetLastError();
+    }
     if (d == 128 && !pg)
         hipLaunchKernelGGL((prefill_kernel<128, false>), grid, dim3(kPfThreads), 0, st, a);
     else if (d == 128)

@@ -122,12 +122,21 @@ struct PrefillArgs {
     float scale;
     const uint8_t* spool;         // on-demand sparse pages (nullptr: fixed records)
     int32_t spages;
+    int32_t wide;                 // blocks of up to 256 rows on the fp16 matrix cores (head_dim 128)
 };
 struct PrefillPlan {
     int32_t tokens_per_block, pages_per_split, n_splits;
+    bool wide;
 };
+// Row blocks of 64 rows, or of 256 (wide: head_dim 128, for chunks with more rows per KV
+// head than 64).
 PrefillPlan plan_prefill(int32_t n_tokens, int32_t n_q_heads, int32_t n_kv_heads, int32_t max_seq_len,
-                         int32_t window);
+                         int32_t window, bool wide);
+// Whether chunks of about n_tokens / n_seqs tokens take the wide blocks.
+inline bool prefill_wide(int32_t n_tokens, int32_t n_seqs, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim) {
+    const int64_t per_chunk = ((int64_t)n_tokens + n_seqs - 1) / std::max<int32_t>(1, n_seqs);
+    return head_dim == 128 && per_chunk * (n_q_heads / n_kv_heads) > 64;
+}
 hipError_t launch_prefill(const PrefillArgs& a, int d, int2* row_blocks, int32_t* n_row_blocks, hipStream_t st);
 // Log-sum-exp merge of split partials for a.n_seqs * a.Hq rows (attention.hip).
 hipError_t launch_combine(const AttnArgs& a, int d, hipStream_t st);
