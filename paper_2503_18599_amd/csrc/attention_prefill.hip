@@ -14,8 +14,8 @@
 // The four waves split the channels: each forms every row's partial scores over a quarter
 // of the key channels (the partials meet in LDS) and, after the softmax (which every wave
 // computes), the outputs of a quarter of the value channels, so the matrix-core work is
-// shared evenly whatever the number of rows.  The next page's record bytes are requested
-// while the current page is processed.  MFMA operand layout (16x16x4, fp32): lane l holds
+// shared evenly whatever the number of rows.  Record bytes are requested two pages ahead
+// of the page being processed.  MFMA operand layout (16x16x4, fp32): lane l holds
 // A[l & 15][k] and B[k][l & 15] with k = l >> 4 of each 4-wide step; the result holds rows
 // 4 (l >> 4) .. + 3 of column l & 15.  Contraction indices are assigned so that a lane's
 // operands are contiguous in LDS: step s of lane group g takes channel (d / 16) g + s of
@@ -392,12 +392,13 @@ __global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(3)))
         return *reinterpret_cast<const uint4*>(record(b, pw_) + 16 * pc_);
     };
 
-    uint4 cur = prefetch(pg_first);
+    uint4 cur = prefetch(pg_first), nxt = prefetch(pg_first + 1);
     for (int pg = pg_first; pg < pg_end; ++pg) {
         const int b = btab[pg];
-        // (1) stage this page's prefetched bytes, request the next page's
+        // (1) stage this page's prefetched bytes, request the bytes two pages ahead
         if (tid < 2 * PF::CH) *reinterpret_cast<uint4*>(&S.st.rec[pw_][16 * pc_]) = cur;
-        cur = prefetch(pg + 1);
+        cur = nxt;
+        nxt = prefetch(pg + 2);
         __syncthreads();
         if (!valid_block(b)) continue;   // (uniform; a precondition violation reads nothing)
         pf_dequant_page<D, PG>(S.st, S.tl, a, b, h, tk, tv, tid);
@@ -453,11 +454,15 @@ __global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(3)))
             ps = sum4(ps);
             l[rt] = l[rt] * alpha + ps;
             m[rt] = mn;
+            // (the accumulators are rescaled only when some row's maximum moved)
+            if (__builtin_amdgcn_ballot_w64(alpha != 1.0f)) {
+#pragma unroll
+                for (int n = 0; n < NCT; ++n) o[rt][n] *= alpha;
+            }
             // O^T += V^T P^T: A = the value tile's channels (row) x tokens 4 g + s, B = this
             // lane's probabilities
 #pragma unroll
             for (int n = 0; n < NCT; ++n) {
-                o[rt][n] *= alpha;
                 const float4 va = *reinterpret_cast<const float4*>(&S.tl.vt[CPW * wave + 16 * n + (lane & 15)][4 * g]);
                 o[rt][n] = mfma4(va.x, p[0], o[rt][n]);
                 o[rt][n] = mfma4(va.y, p[1], o[rt][n]);
