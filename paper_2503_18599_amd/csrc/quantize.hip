@@ -69,16 +69,35 @@ __device__ inline int sum8(int v) {
     return v;
 }
 
-// Inclusive prefix sum over the wave (DPP row scan, then the rows' totals).
-__device__ inline int wave_incl_scan(int x, int lane) {
+// Inclusive prefix sum over the wave: DPP row scan, then the rows' totals carried by row
+// broadcasts (lane 15 of rows 0 and 2 into rows 1 and 3, then lane 31 into rows 2 and 3).
+__device__ inline int wave_incl_scan(int x) {
     x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false);   // row_shr:1
     x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false);   // row_shr:2
     x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false);   // row_shr:4
     x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false);   // row_shr:8
-    const int r0 = __builtin_amdgcn_readlane(x, 15), r1 = __builtin_amdgcn_readlane(x, 31);
-    const int r2 = __builtin_amdgcn_readlane(x, 47);
-    const int row = lane >> 4;
-    return x + (row == 0 ? 0 : row == 1 ? r0 : row == 2 ? r0 + r1 : r0 + r1 + r2);
+    x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);   // row_bcast:15
+    x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);   // row_bcast:31
+    return x;
+}
+
+// LDS addresses as plain 32-bit integers (an address that a select picks whole).
+typedef __attribute__((address_space(3))) uint8_t lds_byte;
+__device__ inline uint32_t off_lds(const void* p) { return (uint32_t)(uintptr_t)(const lds_byte*)p; }
+__device__ inline lds_byte& lds_u8(uint32_t a) { return *(lds_byte*)(uintptr_t)a; }
+
+// x + 1 in the lanes of the lane mask c, else x: one add with c as the carry in.
+__device__ inline int add_if(int x, uint64_t c) {
+    int r;
+    uint64_t carry;
+    asm("v_addc_co_u32_e64 %0, %1, %2, 0, %3" : "=v"(r), "=s"(carry) : "v"(x), "s"(c));
+    return r;
+}
+// c ? a : b per lane of the lane mask c.
+__device__ inline uint32_t pick(uint64_t c, uint32_t a, uint32_t b) {
+    uint32_t r;
+    asm("v_cndmask_b32_e64 %0, %1, %2, %3" : "=v"(r) : "v"(b), "v"(a), "s"(c));
+    return r;
 }
 
 // The lanes of one wave hand LDS data to each other: LDS operations of a wave execute in
@@ -94,39 +113,43 @@ __device__ inline void wave_sync() {
 struct LaneCodes {
     uint32_t nib[8];   // the dense nibble (low 4 bits of the code)
     uint32_t cb[8];    // the COO byte of an inner or outer value
-    bool middle[8];
+    uint64_t out[8];   // lane mask of the lanes whose element e is inner or outer
     int n_out;         // inner and outer values among the eight
     float meta;        // lanes m < 6: field m of the vector's metadata (Min_g, Delta_g)
 };
 
+// The thresholds must satisfy lo_o <= lo_i <= hi_i <= hi_o and x must be finite.  Per
+// element, with t_o = med3(x, lo_o, hi_o) and t_i = med3(x, lo_i, hi_i) (x clamped to the
+// outer and inner intervals): x - t_o is non-zero exactly for outer values, where it is
+// the Eq. 4 shifted value, and x - t_i is zero exactly for inner values and the shifted
+// value of a middle one (differences of distinct floats never round to zero).  The
+// signed value v (x + 0 for inner ones, which turns -0 into +0) then carries the side in
+// its sign bit (side = v >= 0) and the group's magnitude a = |v|.
 template <int LPV>
 __device__ inline LaneCodes quantize_lane(const uint32_t (&w4)[4], float lo_o, float lo_i, float hi_i, float hi_o,
                                           int m, int lane) {
     LaneCodes R;
-    // group, side and shifted magnitude per element; group minima and maxima over the
-    // magnitudes' bit patterns (non-negative floats order as integers): an element of
-    // another group reads as 0xffffffff, the largest unsigned and the smallest signed
-    // key, so one key serves the unsigned minimum and the signed maximum
-    float mag[8];
-    bool outer[8], side[8];
+    // group minima and maxima over the magnitudes' bit patterns (non-negative floats order
+    // as integers): an element of another group reads as 0xffffffff, the largest unsigned
+    // and the smallest signed key, so one key serves the unsigned minimum and the signed
+    // maximum
+    float v[8];
+    bool outer[8], inner[8];
     uint32_t kmin[3] = {~0u, ~0u, ~0u};
     int kmax[3] = {-1, -1, -1};
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
         const float xf = half_bits_to_float((e & 1) ? (w4[e >> 1] >> 16) : (w4[e >> 1] & 0xffffu));
-        const bool c_ho = xf > hi_o, c_lo = xf < lo_o, c_hi = xf > hi_i, c_li = xf < lo_i;
-        const bool o = c_ho || c_lo;                 // Eq. 1, outer
-        const bool not_inner = c_hi || c_li;         // outer or middle
-        const float shift = c_lo ? lo_o : (c_ho ? hi_o : (c_hi ? hi_i : lo_i));
-        const float dv = not_inner ? xf - shift : xf;   // Eq. 4 (inner not shifted)
-        mag[e] = fabsf(dv);
-        // the side is the sign of the shifted value: non-zero for outer and middle
-        // values, and x >= 0 (-0 included) for inner ones
-        side[e] = !(dv < 0.0f);
+        const float d_o = xf - __builtin_amdgcn_fmed3f(xf, lo_o, hi_o);
+        const float d_i = xf - __builtin_amdgcn_fmed3f(xf, lo_i, hi_i);
+        const bool o = d_o != 0.0f;                  // Eq. 1, outer
+        const bool in = d_i == 0.0f;                 // inner (not shifted)
+        v[e] = in ? xf + 0.0f : (o ? d_o : d_i);     // Eq. 4
         outer[e] = o;
-        R.middle[e] = not_inner && !o;
-        const uint32_t mb = __float_as_uint(mag[e]);
-        const uint32_t ki = not_inner ? ~0u : mb, km = R.middle[e] ? mb : ~0u, ko = o ? mb : ~0u;
+        inner[e] = in;
+        R.out[e] = __builtin_amdgcn_ballot_w64(d_o != 0.0f) | __builtin_amdgcn_ballot_w64(d_i == 0.0f);
+        const uint32_t mb = __float_as_uint(v[e]) & 0x7fffffffu;
+        const uint32_t ki = in ? mb : ~0u, km = (o || in) ? ~0u : mb, ko = o ? mb : ~0u;
         kmin[0] = min(kmin[0], ki); kmax[0] = max(kmax[0], (int)ki);
         kmin[1] = min(kmin[1], km); kmax[1] = max(kmax[1], (int)km);
         kmin[2] = min(kmin[2], ko); kmax[2] = max(kmax[2], (int)ko);
@@ -154,19 +177,24 @@ __device__ inline LaneCodes quantize_lane(const uint32_t (&w4)[4], float lo_o, f
     for (int g = 0; g < 3; ++g) sig[g] = __shfl(quo, vbase + 2 * g, 64);
     R.meta = is_delta ? quo : gmin[g6];
 
-    // Eq. 3 and the offset-binary code u = side ? 2^b + c : 2^b - 1 - c, whose low four
-    // bits are c ^ L ^ (side ? 15 : 0).  No clamp is needed: 0 <= a - Min <= R rounds
-    // to at most R, and R * fl(L / R) rounds to less than L + 1/2.
+    // Eq. 3.  0 <= (a - Min) * sigma < L + 1/2 (a - Min <= R rounds to at most R, and
+    // R * fl(L / R) to less than L + 1/2), so adding 2^23 rounds it half-to-even to an
+    // integer c in the low bits and no clamp is needed.  The offset-binary code
+    // u = side ? 2^b + c : 2^b - 1 - c has the low four bits c ^ (middle ? 8 : 0) when the
+    // side is set and their complement otherwise; sg (v's sign spread over the word) is
+    // the complement of the side.
+    const uint32_t m8 = (uint32_t)(8 * m) & 63u;
     R.n_out = 0;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-        const float gm = outer[e] ? gmin[2] : (R.middle[e] ? gmin[1] : gmin[0]);
-        const float gs = outer[e] ? sig[2] : (R.middle[e] ? sig[1] : sig[0]);
-        const uint32_t ci = (uint32_t)rintf((mag[e] - gm) * gs);
-        R.nib[e] = ci ^ (R.middle[e] ? 7u : 15u) ^ (side[e] ? 15u : 0u);
-        const uint32_t c0 = outer[e] ? (0x40u | (uint32_t)((8 * m + e) & 63)) : (uint32_t)((8 * m + e) & 63);
-        R.cb[e] = side[e] ? (c0 | 0x80u) : c0;
-        R.n_out += R.middle[e] ? 0 : 1;
+        const bool o = outer[e], in = inner[e];
+        const float gm = o ? gmin[2] : (in ? gmin[0] : gmin[1]);
+        const float gs = o ? sig[2] : (in ? sig[0] : sig[1]);
+        const float r = (fabsf(v[e]) - gm) * gs + 0x1p23f;
+        const uint32_t sg = (uint32_t)(__float_as_int(v[e]) >> 31);
+        R.nib[e] = (__float_as_uint(r) ^ ((o || in) ? 0u : 8u) ^ sg) & 15u;
+        R.cb[e] = (((o ? 0xc0u : 0x80u) | m8) + (uint32_t)e) ^ (sg & 0x80u);
+        R.n_out = add_if(R.n_out, R.out[e]);
     }
     return R;
 }
@@ -176,7 +204,7 @@ __device__ inline LaneCodes quantize_lane(const uint32_t (&w4)[4], float lo_o, f
 // record's sparse page ids (on-demand pages).
 template <int D>
 struct WaveBuf {
-    __align__(16) uint8_t coo[kPage * D];
+    __align__(16) uint8_t coo[kPage * D + 256];   // (+ one spare byte per lane, 4 apart)
     __align__(16) uint8_t vn[kPage][D];
     __align__(16) uint16_t meta[kPage][6];
     uint8_t cnt[kPage][D / 64];
@@ -231,7 +259,7 @@ __global__ __launch_bounds__(64 * kWavesPerGroup) void quantize_kernel(QuantArgs
     int pre = 0;
     if (slot0 > 0) {
         const int c = lane < slot0 * NC ? (int)rec[LY.counts + lane] : 0;
-        pre = __builtin_amdgcn_readlane(wave_incl_scan(c, lane), 63);
+        pre = __builtin_amdgcn_readlane(wave_incl_scan(c), 63);
         pre = min(pre, CAP);
     }
     const int tab_pre = (PG && lane < NT) ? reinterpret_cast<const int32_t*>(rec + LY.sparse)[lane] : 0;
@@ -277,16 +305,19 @@ __global__ __launch_bounds__(64 * kWavesPerGroup) void quantize_kernel(QuantArgs
         if (valid && m < 6) W.meta[t][m] = float_to_half_bits(Q.meta);
 
         // COO entries: positions from a wave-wide prefix sum of the lanes' counts
-        const int incl = wave_incl_scan(cnt, lane);
+        const int incl = wave_incl_scan(cnt);
         const int c8 = sum8(cnt);   // entries of the lane's 64-value chunk
         if (valid && (m & 7) == 0) W.cnt[t][m >> 3] = (uint8_t)c8;
-        int pos = off - pre + incl - cnt;
+        // every element stores its byte: entries at their stream positions (below CAP:
+        // a segment has at most CAP entries), the others in the lane's own spare byte
+        const uint64_t vmask = __builtin_amdgcn_ballot_w64(valid);
+        const uint32_t spare = off_lds(&W.coo[CAP + 4 * lane]);
+        int at = (int)off_lds(&W.coo[0]) + off - pre + incl - cnt;
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-            if (valid && !Q.middle[e]) {
-                if (pos < CAP) W.coo[pos] = (uint8_t)Q.cb[e];
-                ++pos;
-            }
+            const uint64_t put = vmask & Q.out[e];
+            lds_u8(pick(put, (uint32_t)at, spare)) = (uint8_t)Q.cb[e];
+            at = add_if(at, put);
         }
         off += __builtin_amdgcn_readlane(incl, 63);
     }
@@ -505,7 +536,7 @@ __global__ __launch_bounds__(256) void quantize_token_kernel(QuantArgs a) {
     int p = pre + incl - cnt;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-        if (!Q.middle[e]) {
+        if ((Q.out[e] >> lane) & 1) {
             if (p < CAP) rec[LY.sparse + p] = (uint8_t)Q.cb[e];
             ++p;
         }
