@@ -25,8 +25,8 @@
  *     violating them is undefined behaviour.
  *   - No C++ exception crosses this interface.
  *
- * Quantizer rule (bit-exact contract).  For a vector x[0..d) of fp16 values and
- * fp32 thresholds lo_o <= lo_i <= hi_i <= hi_o, in IEEE fp32 with one rounding
+ * Quantizer rule (bit-exact contract).  For a vector x[0..d) of finite fp16 values
+ * and fp32 thresholds lo_o <= lo_i <= hi_i <= hi_o, in IEEE fp32 with one rounding
  * per operation (no fused multiply-add):
  *   group  OUTER if x < lo_o or x > hi_o; else MIDDLE if x < lo_i or x > hi_i;
  *          else INNER                                                  (Eq. 1)
