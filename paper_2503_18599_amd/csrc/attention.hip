@@ -281,7 +281,7 @@ SplitPlan plan_splits(int32_t n_seqs, int32_t n_q_heads, int32_t n_kv_heads, int
     int pps = (max_pages + want - 1) / want;
     pps = max(pps, 8);
     if (mfma)
-        pps = min(pps, mfma_score_cap() / kPage);
+        pps = min(pps, mfma_score_cap(mfma_wave_heads(G)) / kPage);
     else
         pps = min(pps, kScoreCap / (kPage * G));
     pps = max(pps, 1);

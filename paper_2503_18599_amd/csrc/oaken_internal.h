@@ -198,7 +198,7 @@ hipError_t launch_variant_dequantize(const VariantArgs& a, int d, hipStream_t st
 // per workgroup).
 bool mfma_attention_supported(int d, int G);
 int mfma_wave_heads(int G);      // query heads per workgroup for G heads per KV head
-int mfma_score_cap();   // tokens per query head in one workgroup's page range
+int mfma_score_cap(int wave_heads);   // tokens per query head in one workgroup's page range
 hipError_t launch_attention_mfma(const AttnArgs& a, hipStream_t st);
 hipError_t launch_attention_mfma_paged(const AttnArgs& a, hipStream_t st);   // on-demand sparse pages
 
