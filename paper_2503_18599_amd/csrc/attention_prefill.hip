@@ -346,6 +346,12 @@ __global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(3)))
     const float tk[4] = {th[0], th[1], th[2], th[3]}, tv[4] = {th[4], th[5], th[6], th[7]};
 
     // ---- rows ------------------------------------------------------------------------
+    // Scores are kept in base-2 units (scaled by log2 e, so that the softmax exponentials
+    // are single exp2 instructions); the partials' maxima go out in natural units.
+    const float sl2 = a.scale * 1.44269504088896341f;
+    // pages whose every key every row of the block sees need no mask
+    const int vis_hi = start + i0;
+    const int vis_lo = a.window > 0 ? max(0, start + Bk.i_end - a.window) : 0;
     // Transposed products: scores S^T = K Q^T and outputs O^T = V^T P^T, so that the lanes
     // holding a query row's scores (column lane & 15 of the result) also hold its
     // probabilities as the B operand of the value product and its outputs, and the softmax
@@ -359,7 +365,7 @@ __global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(3)))
         const int i = i0 + (ok ? ra / G : 0), hd = ok ? ra % G : 0;
         const uint16_t* qp = a.q + ((int64_t)(tok0 + i) * a.Hq + h * G + hd) * D + CPW * wave + KSW * g;
 #pragma unroll
-        for (int k = 0; k < KSW; ++k) bq[rt][k] = ok ? a.scale * h2f(qp[k]) : 0.0f;
+        for (int k = 0; k < KSW; ++k) bq[rt][k] = ok ? sl2 * h2f(qp[k]) : 0.0f;
     }
     // this lane's query row in each tile, its position and window start
     int rpos[kMaxRowTiles], rlo[kMaxRowTiles];
@@ -402,6 +408,7 @@ __global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(3)))
         __syncthreads();
         if (!valid_block(b)) continue;   // (uniform; a precondition violation reads nothing)
         pf_dequant_page<D, PG>(S.st, S.tl, a, b, h, tk, tv, tid);
+        const bool full = pg * kPage + kPage - 1 <= vis_hi && pg * kPage >= vis_lo;
 
         // (5) partial scores of every row tile over this wave's channels: lane (g, query
         //     row q) gets S^T[4 g + r][q] over channels CPW w .. + CPW
@@ -434,21 +441,26 @@ __global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(3)))
 #pragma unroll
             for (int w = 1; w < kWaves; ++w) sc += S.sp[w][rt][lane];
             float v[4];
-            float mx = -INFINITY;
+            if (full) {
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int kp = pg * kPage + 4 * g + r;   // key position
-                const bool vis = rok[rt] && kp <= rpos[rt] && kp >= rlo[rt];
-                v[r] = vis ? sc[r] : -INFINITY;
-                mx = fmaxf(mx, v[r]);
+                for (int r = 0; r < 4; ++r) v[r] = sc[r];
+            } else {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int kp = pg * kPage + 4 * g + r;   // key position
+                    const bool vis = rok[rt] && kp <= rpos[rt] && kp >= rlo[rt];
+                    v[r] = vis ? sc[r] : -INFINITY;
+                }
             }
-            mx = max4(mx);
+            const float mx = max4(fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])));
             const float mn = fmaxf(m[rt], mx);
-            const float alpha = (mn == -INFINITY) ? 1.0f : __expf(m[rt] - mn);
+            // (a row with no visible key yet keeps l = 0 and o = 0 whatever alpha is)
+            const float ms = (mn == -INFINITY) ? 0.0f : mn;
+            const float alpha = __builtin_amdgcn_exp2f(m[rt] - ms);
             float p[4], ps = 0.0f;
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                p[r] = (v[r] == -INFINITY) ? 0.0f : __expf(v[r] - mn);
+                p[r] = __builtin_amdgcn_exp2f(v[r] - ms);
                 ps += p[r];
             }
             ps = sum4(ps);
@@ -491,7 +503,7 @@ __global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(3)))
             for (int n = 0; n < NCT; ++n)
                 for (int r = 0; r < 4; ++r) pp[CPW * wave + 16 * n + 4 * g + r] = o[rt][n][r];
             if (wave == 0 && g == 0) {
-                pp[D] = m[rt];
+                pp[D] = m[rt] * 0.693147180559945309f;
                 pp[D + 1] = l[rt];
             }
         }
@@ -546,6 +558,10 @@ __global__ __launch_bounds__(kPfThreads) void prefill_wide_kernel(PrefillArgs a)
         rpos[rt] = start + i;
         rlo[rt] = a.window > 0 ? max(0, rpos[rt] + 1 - a.window) : 0;
     }
+    // scores in base-2 units (see prefill_kernel); pages every row sees need no mask
+    const float sl2 = a.scale * 1.44269504088896341f;
+    const int vis_hi = start + i0;
+    const int vis_lo = a.window > 0 ? max(0, start + Bk.i_end - a.window) : 0;
     float m[kWideTiles], l[kWideTiles];
     f4 o[kWideTiles][NCT];   // O^T: channels 16 n + 4 g + r of the lane's query row
 #pragma unroll
@@ -579,6 +595,7 @@ __global__ __launch_bounds__(kPfThreads) void prefill_wide_kernel(PrefillArgs a)
         if (!valid_block(b)) continue;   // (uniform; a precondition violation reads nothing)
         pf_dequant_page<D, PG>(S.st, S.tl, a, b, h, tk, tv, tid);
         if (R == 0) continue;   // (uniform per wave; the next barrier is at the loop top)
+        const bool full = pg * kPage + kPage - 1 <= vis_hi && pg * kPage >= vis_lo;
 
         // scores of the wave's row tiles: lane (g, q16) gets S^T[4 g + r][q16]
         f4 sc[kWideTiles];
@@ -602,21 +619,26 @@ __global__ __launch_bounds__(kPfThreads) void prefill_wide_kernel(PrefillArgs a)
         for (int rt = 0; rt < kWideTiles; ++rt) {
             if (rt >= R) break;
             float v[4];
-            float mx = -INFINITY;
+            if (full) {
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int kp = pg * kPage + 4 * g + r;   // key position
-                const bool vis = rok[rt] && kp <= rpos[rt] && kp >= rlo[rt];
-                v[r] = vis ? a.scale * sc[rt][r] : -INFINITY;
-                mx = fmaxf(mx, v[r]);
+                for (int r = 0; r < 4; ++r) v[r] = sl2 * sc[rt][r];
+            } else {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int kp = pg * kPage + 4 * g + r;   // key position
+                    const bool vis = rok[rt] && kp <= rpos[rt] && kp >= rlo[rt];
+                    v[r] = vis ? sl2 * sc[rt][r] : -INFINITY;
+                }
             }
-            mx = max4(mx);
+            const float mx = max4(fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])));
             const float mn = fmaxf(m[rt], mx);
-            const float alpha = (mn == -INFINITY) ? 1.0f : __expf(m[rt] - mn);
+            // (a row with no visible key yet keeps l = 0 and o = 0 whatever alpha is)
+            const float ms = (mn == -INFINITY) ? 0.0f : mn;
+            const float alpha = __builtin_amdgcn_exp2f(m[rt] - ms);
             float ps = 0.0f;
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                const float p = (v[r] == -INFINITY) ? 0.0f : __expf(v[r] - mn);
+                const float p = __builtin_amdgcn_exp2f(v[r] - ms);
                 ps += p;
                 const Split16 z = split16(p);
                 ph[rt][r] = z.hi;
@@ -668,7 +690,7 @@ __global__ __launch_bounds__(kPfThreads) void prefill_wide_kernel(PrefillArgs a)
                 *reinterpret_cast<float4*>(&pp[16 * n + 4 * g]) =
                     make_float4(o[rt][n][0], o[rt][n][1], o[rt][n][2], o[rt][n][3]);
             if (g == 0) {
-                pp[D] = m[rt];
+                pp[D] = m[rt] * 0.693147180559945309f;
                 pp[D + 1] = l[rt];
             }
         }
