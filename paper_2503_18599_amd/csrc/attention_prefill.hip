@@ -88,6 +88,8 @@ struct PfStage {
     float tokc[2][kPage][8];                         // per record (K, V) and slot: Min, Delta of
                                                      // inner, middle, outer
     int used[2];                                     // COO bytes of each record
+    uint32_t mid[2][kPage][16];                      // per record, slot and nibble: the middle
+                                                     // reading in the tiles' word format
     __align__(16) uint8_t rec[2][PfLayout<D, PG>::STAGE];
     uint8_t owner[2][PfLayout<D, PG>::CAP];          // per COO byte: its (slot, chunk) bucket
 };
@@ -97,16 +99,18 @@ template <int D>
 struct TilesF32 {
     __align__(16) float kt[kPage][D + 4];
     __align__(16) float vt[D][kPage + 4];
-    __device__ void put_k8(int t, int j0, const float (&x)[8]) {
-        *reinterpret_cast<float4*>(&kt[t][j0]) = make_float4(x[0], x[1], x[2], x[3]);
-        *reinterpret_cast<float4*>(&kt[t][j0 + 4]) = make_float4(x[4], x[5], x[6], x[7]);
-    }
-    __device__ void put_v8(int j, int t0, const float (&x)[8]) {
-        *reinterpret_cast<float4*>(&vt[j][t0]) = make_float4(x[0], x[1], x[2], x[3]);
-        *reinterpret_cast<float4*>(&vt[j][t0 + 4]) = make_float4(x[4], x[5], x[6], x[7]);
-    }
     __device__ void put_k(int t, int j, float x) { kt[t][j] = x; }
     __device__ void put_v(int j, int t, float x) { vt[j][t] = x; }
+    // a tile element as one 32-bit word: the fp32 bits
+    static __device__ uint32_t word(float x) { return __float_as_uint(x); }
+    __device__ void put_k8w(int t, int j0, const uint32_t (&w)[8]) {
+        *reinterpret_cast<uint4*>(&kt[t][j0]) = make_uint4(w[0], w[1], w[2], w[3]);
+        *reinterpret_cast<uint4*>(&kt[t][j0 + 4]) = make_uint4(w[4], w[5], w[6], w[7]);
+    }
+    __device__ void put_v8w(int j, int t0, const uint32_t (&w)[8]) {
+        *reinterpret_cast<uint4*>(&vt[j][t0]) = make_uint4(w[0], w[1], w[2], w[3]);
+        *reinterpret_cast<uint4*>(&vt[j][t0 + 4]) = make_uint4(w[4], w[5], w[6], w[7]);
+    }
 };
 
 typedef _Float16 h4 __attribute__((ext_vector_type(4)));
@@ -131,32 +135,6 @@ struct TilesF16 {
     __align__(16) _Float16 kl[kPage][KS];
     __align__(16) _Float16 vh[D][VS];
     __align__(16) _Float16 vl[D][VS];
-    __device__ void put_k8(int t, int j0, const float (&x)[8]) {
-        h8 hi, lo;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const Split16 z = split16(x[e]);
-            hi[e] = z.hi;
-            lo[e] = z.lo;
-        }
-        *reinterpret_cast<h8*>(&kh[t][j0]) = hi;
-        *reinterpret_cast<h8*>(&kl[t][j0]) = lo;
-    }
-    __device__ void put_v8(int j, int t0, const float (&x)[8]) {
-        h4 h0, h1, l0, l1;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const Split16 z0 = split16(x[e]), z1 = split16(x[e + 4]);
-            h0[e] = z0.hi;
-            l0[e] = z0.lo;
-            h1[e] = z1.hi;
-            l1[e] = z1.lo;
-        }
-        *reinterpret_cast<h4*>(&vh[j][t0]) = h0;
-        *reinterpret_cast<h4*>(&vh[j][t0 + 4]) = h1;
-        *reinterpret_cast<h4*>(&vl[j][t0]) = l0;
-        *reinterpret_cast<h4*>(&vl[j][t0 + 4]) = l1;
-    }
     __device__ void put_k(int t, int j, float x) {
         const Split16 z = split16(x);
         kh[t][j] = z.hi;
@@ -166,6 +144,32 @@ struct TilesF16 {
         const Split16 z = split16(x);
         vh[j][t] = z.hi;
         vl[j][t] = z.lo;
+    }
+    // a tile element as one 32-bit word: the high part in the low half, the low part above
+    static __device__ uint32_t word(float x) {
+        const Split16 z = split16(x);
+        return (uint32_t)__builtin_bit_cast(uint16_t, z.hi) | ((uint32_t)__builtin_bit_cast(uint16_t, z.lo) << 16);
+    }
+    // eight words: their low halves to the high tile, their high halves to the low one
+    static __device__ void halves8(const uint32_t (&w)[8], uint4& hi, uint4& lo) {
+        hi = make_uint4(__builtin_amdgcn_perm(w[1], w[0], 0x05040100u), __builtin_amdgcn_perm(w[3], w[2], 0x05040100u),
+                        __builtin_amdgcn_perm(w[5], w[4], 0x05040100u), __builtin_amdgcn_perm(w[7], w[6], 0x05040100u));
+        lo = make_uint4(__builtin_amdgcn_perm(w[1], w[0], 0x07060302u), __builtin_amdgcn_perm(w[3], w[2], 0x07060302u),
+                        __builtin_amdgcn_perm(w[5], w[4], 0x07060302u), __builtin_amdgcn_perm(w[7], w[6], 0x07060302u));
+    }
+    __device__ void put_k8w(int t, int j0, const uint32_t (&w)[8]) {
+        uint4 hi, lo;
+        halves8(w, hi, lo);
+        *reinterpret_cast<uint4*>(&kh[t][j0]) = hi;
+        *reinterpret_cast<uint4*>(&kl[t][j0]) = lo;
+    }
+    __device__ void put_v8w(int j, int t0, const uint32_t (&w)[8]) {
+        uint4 hi, lo;
+        halves8(w, hi, lo);
+        *reinterpret_cast<uint2*>(&vh[j][t0]) = make_uint2(hi.x, hi.y);
+        *reinterpret_cast<uint2*>(&vh[j][t0 + 4]) = make_uint2(hi.z, hi.w);
+        *reinterpret_cast<uint2*>(&vl[j][t0]) = make_uint2(lo.x, lo.y);
+        *reinterpret_cast<uint2*>(&vl[j][t0 + 4]) = make_uint2(lo.z, lo.w);
     }
 };
 
@@ -225,6 +229,18 @@ __device__ __forceinline__ void pf_dequant_page(PfStage<D, PG>& S, Tiles& T, con
 #pragma unroll
         for (int k = 0; k < 6; ++k) S.tokc[w][t][k] = h2f(mt[k]);
     }
+    // the middle reading of each (record, slot, nibble): offset-binary code u, side u >= 8
+    // (Eq. 3 inverted, then the Eq. 4 shift undone), in the tiles' word format
+#pragma unroll
+    for (int i = 0; i < 2 * kPage * 16 / kPfThreads; ++i) {
+        const int e = tid + i * kPfThreads, w = e / (kPage * 16), t = (e / 16) % kPage, u = e % 16;
+        const uint16_t* mt = reinterpret_cast<const uint16_t*>(S.rec[w] + LY.meta + 12 * t);
+        const float mn = h2f(mt[2]), dl = h2f(mt[3]);
+        const float* thw = w ? tv : tk;
+        const bool hi = u >= 8;
+        const float mag = mn + (float)(hi ? u - 8 : 7 - u) * dl;
+        S.mid[w][t][u] = Tiles::word(hi ? thw[2] + mag : thw[1] - mag);
+    }
     __syncthreads();
 
     // (3) stream bytes past the prefetched window (and, with on-demand sparse pages, the
@@ -251,30 +267,19 @@ __device__ __forceinline__ void pf_dequant_page(PfStage<D, PG>& S, Tiles& T, con
         if (tid < kPage * GPT) {
             const int t = tid / GPT, cg = tid % GPT;
             const uint32_t dw = *reinterpret_cast<const uint32_t*>(&S.rec[0][LY.dense + t * (D / 2) + 4 * cg]);
-            const float mn = S.tokc[0][t][2], dl = S.tokc[0][t][3];
-            float x[8];
+            uint32_t x[8];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const uint32_t u = (dw >> (4 * e)) & 15u;
-                const bool hi = u >= 8;
-                const float mag = mn + (float)(hi ? u - 8 : 7 - u) * dl;
-                x[e] = hi ? tk[2] + mag : tk[1] - mag;
-            }
-            T.put_k8(t, 8 * cg, x);
+            for (int e = 0; e < 8; ++e) x[e] = S.mid[0][t][(dw >> (4 * e)) & 15u];
+            T.put_k8w(t, 8 * cg, x);
         }
         // values: thread = (channel j, 8 slots); dense byte j * 8 + t/2, low nibble = even t
         if (tid < 2 * D) {
             const int j = tid >> 1, t0 = 8 * (tid & 1);
             const uint32_t dw = *reinterpret_cast<const uint32_t*>(&S.rec[1][LY.dense + j * (kPage / 2) + (t0 >> 1)]);
-            float x[8];
+            uint32_t x[8];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const uint32_t u = (dw >> (4 * e)) & 15u;
-                const bool hi = u >= 8;
-                const float mag = S.tokc[1][t0 + e][2] + (float)(hi ? u - 8 : 7 - u) * S.tokc[1][t0 + e][3];
-                x[e] = hi ? tv[2] + mag : tv[1] - mag;
-            }
-            T.put_v8(j, t0, x);
+            for (int e = 0; e < 8; ++e) x[e] = S.mid[1][t0 + e][(dw >> (4 * e)) & 15u];
+            T.put_v8w(j, t0, x);
         }
     }
     __syncthreads();
