@@ -167,6 +167,42 @@ def test_quantize_edge_thresholds_token_by_token(B, ref, cid):
     compare_pools(ref, case, cache.pool.cpu().numpy(), want)
 
 
+@pytest.mark.parametrize("mode", ["prefill", "token"])
+@pytest.mark.parametrize("cid", [2, 1])
+def test_quantize_signed_zeros_and_threshold_ties(B, ref, cid, mode):
+    """Values exactly on the thresholds and zeros of both signs, in both quantize kernels
+    (a prefill call, and one token per call): thresholds (-1, -0, +0, 1), where zeros of
+    either sign are inner (side set: x >= 0 holds for -0) and every other value is a middle
+    or outer one, and (-0.5, -0.25, 0.25, 0.5) with a quarter of the inputs planted on
+    +-0, +-0.25, +-0.5 and +-1 (a value on a threshold stays in the narrower group)."""
+    w = synth.scaled(synth.WORKLOADS[cid], n_seqs=3, ctx=37)
+    case = Case(w)
+    thr = np.zeros((case.H, 2, 4), np.float32)
+    thr[0::2] = np.array([-1.0, -0.0, 0.0, 1.0], np.float32)
+    thr[1::2] = np.array([-0.5, -0.25, 0.25, 0.5], np.float32)
+    case.thr = thr
+    g = torch.Generator().manual_seed(11)
+    planted = torch.tensor([-0.0, 0.0, -0.25, 0.25, -0.5, 0.5, -1.0, 1.0], dtype=case.k.dtype)
+    for x in (case.k, case.v):
+        flat = x.view(-1)
+        n = flat.numel() // 4
+        flat[torch.randint(0, flat.numel(), (n,), generator=g)] = planted[torch.randint(0, 8, (n,), generator=g)]
+    want = case.oracle_pool(ref)
+    if mode == "prefill":
+        cache, _ = _gpu_cache(B, case)
+    else:
+        cache, bt = _gpu_cache(B, case, prefill=False)
+        lens = case.lens
+        for step in range(int(lens.max())):
+            act = step < lens
+            cu = torch.zeros(case.n_seqs + 1, dtype=torch.int32)
+            cu[1:] = torch.cumsum(act.to(torch.int32), 0)
+            sel = (case.cu[:-1] + step)[act]
+            B.quantize_kv(cache, case.k[sel].to(DEV), case.v[sel].to(DEV), bt,
+                          torch.full((case.n_seqs,), step, dtype=torch.int32, device=DEV), cu.to(DEV), 1)
+    compare_pools(ref, case, cache.pool.cpu().numpy(), want)
+
+
 @pytest.mark.parametrize("name", list(CASES))
 def test_attention_matches_oracle(B, ref, name):
     case = _case(ref, name)
