@@ -4,12 +4,13 @@
 // A workgroup takes a block of up to 64 query rows: consecutive query tokens of one
 // sequence's chunk times the query heads of one KV head.  It reads every page of the
 // keys those rows can see once, whatever the number of rows: each page record is staged
-// in LDS, dequantized into an fp32 tile (middle values from the dense nibbles, then the
-// COO entries overwrite their elements with their true values: the engine's zero-insert
-// and merge of Sec. 5.2), and the tile is contracted with all rows on the matrix cores in
-// fp32 (v_mfma_f32_16x16x4_f32), with an online softmax across the pages.  Long prefixes
-// are split into page ranges whose partials the decode attention's log-sum-exp combine
-// merges.
+// in LDS, dequantized into an fp32 tile (middle values from the dense nibbles, looked up
+// in a per-page table of each slot's 16 possible readings, then the COO entries overwrite
+// their elements with their true values: the engine's zero-insert and merge of Sec. 5.2),
+// and the tile is contracted with all rows on the matrix cores in fp32
+// (v_mfma_f32_16x16x4_f32), with an online softmax across the pages (scores in base-2
+// units; pages that every row sees skip the masks).  Long prefixes are split into page
+// ranges whose partials the decode attention's log-sum-exp combine merges.
 //
 // The four waves split the channels: each forms every row's partial scores over a quarter
 // of the key channels (the partials meet in LDS) and, after the softmax (which every wave
@@ -23,12 +24,13 @@
 // are formed transposed (keys and values as the A operand, queries and probabilities as
 // B), so a query row lives on the four lanes q + 16 g of column q.
 //
-// With more rows per KV head than one block of 64 holds (several query heads times a long
-// chunk), prefill_wide_kernel takes up to 256 rows: each wave owns 64 rows over all the
-// channels, and the tiles are contracted on the fp16 matrix cores with every real operand
-// split into a high and a low fp16 part (x = hi + lo to about 2^-22 relative; the query is
-// fp16 already): S^T = K_hi Q^T + K_lo Q^T and O^T += V_hi P_hi + V_hi P_lo + V_lo P_hi,
-// accumulated in fp32.  A page is then read and dequantized once for all the rows.
+// With more rows per KV head than one block of 64 holds at head_dim 128 (several query
+// heads times a long chunk), prefill_wide_kernel takes up to 128 rows: each wave owns 32
+// rows over all the channels, and the tiles are contracted on the fp16 matrix cores with
+// every real operand split into a high and a low fp16 part (x = hi + lo to about 2^-22
+// relative; the query is fp16 already): S^T = K_hi Q^T + K_lo Q^T and
+// O^T += V_hi P_hi + V_hi P_lo + V_lo P_hi, accumulated in fp32.  A page is then read and
+// dequantized once for all the rows.
 #include "oaken_internal.h"
 
 #include <hip/hip_fp16.h>
