@@ -184,7 +184,7 @@ struct PfSmem {
 template <int D, bool PG>
 struct PfWideSmem {
     PfStage<D, PG> st;
-    TilesF16<D> tl;
+    TilesF16<D> tl[2];   // the page being contracted and the next page being dequantized
 };
 
 // The record bytes a thread prefetches for the next page: chunk c of record w holds bytes
@@ -197,19 +197,18 @@ struct PfPrefetch {
     static constexpr int CH = PfLayout<D, PG>::PRE / 16 + WIN / 16;   // chunks per record
 };
 
-// Phases (2)-(4) of a page, every thread of the workgroup taking part; the page's records
-// are already staged in S.rec (phase 1) and block b is valid.  Leaves the dequantized page
-// in the tiles, after a barrier.
+// The dequantization of a page in three phases, every thread of the workgroup taking
+// part in each; the page's records are already staged in S.rec (phase 1) and block b is
+// valid.  A barrier must separate the phases (pf_dequant_page places them; the 128-row
+// kernel interleaves its own work with them).
+// (2) buckets, per-slot constants and the middle-reading table
 template <int D, bool PG, class Tiles>
-__device__ __forceinline__ void pf_dequant_page(PfStage<D, PG>& S, Tiles& T, const PrefillArgs& a, int b, int h,
-                                                const float (&tk)[4], const float (&tv)[4], int tid) {
+__device__ __forceinline__ void pf_phase_buckets(PfStage<D, PG>& S, const float (&tk)[4], const float (&tv)[4],
+                                                 int tid) {
     using PL = PfLayout<D, PG>;
-    using PF = PfPrefetch<D, PG>;
     constexpr Layout LY = PL::LY;
     constexpr int NC = PL::NC;
     const int lane = tid & 63, wave = tid >> 6;
-    auto record = [&](int w) { return a.pool + (((int64_t)b * a.H + h) * 2 + w) * a.stride; };
-
     // (2) wave 0: each record's (slot, chunk) buckets, their stream offsets (a DPP prefix
     //     sum: K buckets on lanes 0.., V buckets on lanes 32..) and the bucket owning each
     //     stream byte; wave 1: per-slot dequantization constants
@@ -238,13 +237,22 @@ __device__ __forceinline__ void pf_dequant_page(PfStage<D, PG>& S, Tiles& T, con
         const int e = tid + i * kPfThreads, w = e / (kPage * 16), t = (e / 16) % kPage, u = e % 16;
         const uint16_t* mt = reinterpret_cast<const uint16_t*>(S.rec[w] + LY.meta + 12 * t);
         const float mn = h2f(mt[2]), dl = h2f(mt[3]);
-        const float* thw = w ? tv : tk;
+        // (thresholds selected as values: an array picked by pointer would live in scratch)
+        const float th_lo = w ? tv[1] : tk[1], th_hi = w ? tv[2] : tk[2];
         const bool hi = u >= 8;
         const float mag = mn + (float)(hi ? u - 8 : 7 - u) * dl;
-        S.mid[w][t][u] = Tiles::word(hi ? thw[2] + mag : thw[1] - mag);
+        S.mid[w][t][u] = Tiles::word(hi ? th_hi + mag : th_lo - mag);
     }
-    __syncthreads();
+}
 
+// (3) the stream bytes past the prefetched window, and the middle readings into the tiles
+template <int D, bool PG, class Tiles>
+__device__ __forceinline__ void pf_phase_middle(PfStage<D, PG>& S, Tiles& T, const PrefillArgs& a, int b, int h,
+                                                int tid) {
+    using PL = PfLayout<D, PG>;
+    using PF = PfPrefetch<D, PG>;
+    constexpr Layout LY = PL::LY;
+    auto record = [&](int w) { return a.pool + (((int64_t)b * a.H + h) * 2 + w) * a.stride; };
     // (3) stream bytes past the prefetched window (and, with on-demand sparse pages, the
     //     whole stream, through the page table)
     if (PG || S.used[0] > PF::WIN || S.used[1] > PF::WIN) {
@@ -284,8 +292,15 @@ __device__ __forceinline__ void pf_dequant_page(PfStage<D, PG>& S, Tiles& T, con
             T.put_v8w(j, t0, x);
         }
     }
-    __syncthreads();
+}
 
+// (4) the COO entries' true values into the tiles
+template <int D, bool PG, class Tiles>
+__device__ __forceinline__ void pf_phase_entries(PfStage<D, PG>& S, Tiles& T, const float (&tk)[4],
+                                                 const float (&tv)[4], int tid) {
+    using PL = PfLayout<D, PG>;
+    constexpr Layout LY = PL::LY;
+    constexpr int NC = PL::NC;
     // (4) COO entries replace their elements' middle readings by their true values
     //     (thread = entry of either record's stream)
     {
@@ -299,14 +314,25 @@ __device__ __forceinline__ void pf_dequant_page(PfStage<D, PG>& S, Tiles& T, con
             const uint32_t byte = w ? r[LY.dense + j * (kPage / 2) + (t >> 1)] : r[LY.dense + t * (D / 2) + (j >> 1)];
             const uint32_t n = (byte >> (4 * (w ? (t & 1) : (j & 1)))) & 15u;
             const bool side = (en >> 7) != 0, outer = ((en >> 6) & 1u) != 0;
-            const float* thw = w ? tv : tk;
+            const float th_lo = w ? tv[0] : tk[0], th_hi = w ? tv[3] : tk[3];
             const float cf = (float)(side ? n : 15u - n);
             const float mag = outer ? S.tokc[w][t][4] + cf * S.tokc[w][t][5] : S.tokc[w][t][0] + cf * S.tokc[w][t][1];
-            const float x = outer ? (side ? thw[3] + mag : thw[0] - mag) : (side ? mag : -mag);
+            const float x = outer ? (side ? th_hi + mag : th_lo - mag) : (side ? mag : -mag);
             if (w) T.put_v(j, t, x);
             else T.put_k(t, j, x);
         }
     }
+}
+
+// Phases (2)-(4) with their barriers: leaves the dequantized page in the tiles.
+template <int D, bool PG, class Tiles>
+__device__ __forceinline__ void pf_dequant_page(PfStage<D, PG>& S, Tiles& T, const PrefillArgs& a, int b, int h,
+                                                const float (&tk)[4], const float (&tv)[4], int tid) {
+    pf_phase_buckets<D, PG, Tiles>(S, tk, tv, tid);
+    __syncthreads();
+    pf_phase_middle<D, PG, Tiles>(S, T, a, b, h, tid);
+    __syncthreads();
+    pf_phase_entries<D, PG, Tiles>(S, T, tk, tv, tid);
     __syncthreads();
 }
 
@@ -592,90 +618,126 @@ __global__ __launch_bounds__(kPfThreads) void prefill_wide_kernel(PrefillArgs a)
 
     // (two pages in flight: with few workgroups per CU one page ahead does not cover the
     // memory latency)
+    // Software pipeline over the pages: while the waves contract page pg from one set of
+    // tiles, they stage and dequantize page pg + 1 into the other, each wave taking up its
+    // share of the next page's phases between its own matrix-core and softmax steps, so
+    // that the barriers between the phases find work to overlap.
     uint4 cur = prefetch(pg_first), nxt = prefetch(pg_first + 1);
-    for (int pg = pg_first; pg < pg_end; ++pg) {
-        const int b = btab[pg];
+    bool ok_cur = false;   // (uniform) the page in the current tiles is valid
+    if (pg_first < pg_end) {
+        const int b = btab[pg_first];
         if (tid < 2 * PF::CH) *reinterpret_cast<uint4*>(&S.st.rec[pw_][16 * pc_]) = cur;
         cur = nxt;
-        nxt = prefetch(pg + 2);
+        nxt = prefetch(pg_first + 2);
         __syncthreads();
-        if (!valid_block(b)) continue;   // (uniform; a precondition violation reads nothing)
-        pf_dequant_page<D, PG>(S.st, S.tl, a, b, h, tk, tv, tid);
-        if (R == 0) continue;   // (uniform per wave; the next barrier is at the loop top)
+        ok_cur = valid_block(b);   // (a precondition violation reads nothing)
+        if (ok_cur) pf_dequant_page<D, PG>(S.st, S.tl[0], a, b, h, tk, tv, tid);
+    }
+    for (int pg = pg_first; pg < pg_end; ++pg) {
+        const int par = (pg - pg_first) & 1;
+        TilesF16<D>& Tc = S.tl[par];       // page pg
+        TilesF16<D>& Tn = S.tl[par ^ 1];   // page pg + 1
+        const bool has_next = pg + 1 < pg_end;
+        const int bn = has_next ? btab[pg + 1] : -1;
+        const bool ok_next = has_next && valid_block(bn);
+        // (1) stage the next page (the previous page's phases are past their last barrier)
+        if (has_next && tid < 2 * PF::CH) *reinterpret_cast<uint4*>(&S.st.rec[pw_][16 * pc_]) = cur;
+        cur = nxt;
+        nxt = prefetch(pg + 3);
+        const bool work = ok_cur && R > 0;   // (uniform per wave)
         const bool full = pg * kPage + kPage - 1 <= vis_hi && pg * kPage >= vis_lo;
 
         // scores of the wave's row tiles: lane (g, q16) gets S^T[4 g + r][q16]
         f4 sc[kWideTiles];
 #pragma unroll
         for (int rt = 0; rt < kWideTiles; ++rt) sc[rt] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+        if (work) {
 #pragma unroll
-        for (int k = 0; k < KST; ++k) {
-            const h8 ah = *reinterpret_cast<const h8*>(&S.tl.kh[q16][32 * k + 8 * g]);
-            const h8 al = *reinterpret_cast<const h8*>(&S.tl.kl[q16][32 * k + 8 * g]);
+            for (int k = 0; k < KST; ++k) {
+                const h8 ah = *reinterpret_cast<const h8*>(&Tc.kh[q16][32 * k + 8 * g]);
+                const h8 al = *reinterpret_cast<const h8*>(&Tc.kl[q16][32 * k + 8 * g]);
 #pragma unroll
-            for (int rt = 0; rt < kWideTiles; ++rt) {
-                if (rt < R) {
-                    sc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, bq[rt][k], sc[rt], 0, 0, 0);
-                    sc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(al, bq[rt][k], sc[rt], 0, 0, 0);
+                for (int rt = 0; rt < kWideTiles; ++rt) {
+                    if (rt < R) {
+                        sc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, bq[rt][k], sc[rt], 0, 0, 0);
+                        sc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(al, bq[rt][k], sc[rt], 0, 0, 0);
+                    }
                 }
             }
         }
+        __syncthreads();
+        // (2) the next page's buckets, constants and middle-reading table
+        if (ok_next) pf_phase_buckets<D, PG, TilesF16<D>>(S.st, tk, tv, tid);
+
         // online softmax per row tile, probabilities split for the value product
         h4 ph[kWideTiles], pl[kWideTiles];
-#pragma unroll
-        for (int rt = 0; rt < kWideTiles; ++rt) {
-            if (rt >= R) break;
-            float v[4];
-            if (full) {
-#pragma unroll
-                for (int r = 0; r < 4; ++r) v[r] = sl2 * sc[rt][r];
-            } else {
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int kp = pg * kPage + 4 * g + r;   // key position
-                    const bool vis = rok[rt] && kp <= rpos[rt] && kp >= rlo[rt];
-                    v[r] = vis ? sl2 * sc[rt][r] : -INFINITY;
-                }
-            }
-            const float mx = max4(fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])));
-            const float mn = fmaxf(m[rt], mx);
-            // (a row with no visible key yet keeps l = 0 and o = 0 whatever alpha is)
-            const float ms = (mn == -INFINITY) ? 0.0f : mn;
-            const float alpha = __builtin_amdgcn_exp2f(m[rt] - ms);
-            float ps = 0.0f;
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const float p = __builtin_amdgcn_exp2f(v[r] - ms);
-                ps += p;
-                const Split16 z = split16(p);
-                ph[rt][r] = z.hi;
-                pl[rt][r] = z.lo;
-            }
-            ps = sum4(ps);
-            l[rt] = l[rt] * alpha + ps;
-            m[rt] = mn;
-            // (the accumulators are rescaled only when some row's maximum moved)
-            if (__builtin_amdgcn_ballot_w64(alpha != 1.0f)) {
-#pragma unroll
-                for (int n = 0; n < NCT; ++n) o[rt][n] *= alpha;
-            }
-        }
-        // O^T += V^T P^T: A = channels 16 n + q16 x keys 4 g .. + 3 (hi, lo); B = the lane's
-        // probabilities (hi, lo); the hi x hi, hi x lo and lo x hi products
-#pragma unroll
-        for (int n = 0; n < NCT; ++n) {
-            const h4 vh = *reinterpret_cast<const h4*>(&S.tl.vh[16 * n + q16][4 * g]);
-            const h4 vl = *reinterpret_cast<const h4*>(&S.tl.vl[16 * n + q16][4 * g]);
+        if (work) {
 #pragma unroll
             for (int rt = 0; rt < kWideTiles; ++rt) {
-                if (rt < R) {
-                    o[rt][n] = __builtin_amdgcn_mfma_f32_16x16x16f16(vh, ph[rt], o[rt][n], 0, 0, 0);
-                    o[rt][n] = __builtin_amdgcn_mfma_f32_16x16x16f16(vh, pl[rt], o[rt][n], 0, 0, 0);
-                    o[rt][n] = __builtin_amdgcn_mfma_f32_16x16x16f16(vl, ph[rt], o[rt][n], 0, 0, 0);
+                if (rt >= R) break;
+                float v[4];
+                if (full) {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) v[r] = sl2 * sc[rt][r];
+                } else {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int kp = pg * kPage + 4 * g + r;   // key position
+                        const bool vis = rok[rt] && kp <= rpos[rt] && kp >= rlo[rt];
+                        v[r] = vis ? sl2 * sc[rt][r] : -INFINITY;
+                    }
+                }
+                const float mx = max4(fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])));
+                const float mn = fmaxf(m[rt], mx);
+                // (a row with no visible key yet keeps l = 0 and o = 0 whatever alpha is)
+                const float ms = (mn == -INFINITY) ? 0.0f : mn;
+                const float alpha = __builtin_amdgcn_exp2f(m[rt] - ms);
+                float ps = 0.0f;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const float p = __builtin_amdgcn_exp2f(v[r] - ms);
+                    ps += p;
+                    const Split16 z = split16(p);
+                    ph[rt][r] = z.hi;
+                    pl[rt][r] = z.lo;
+                }
+                ps = sum4(ps);
+                l[rt] = l[rt] * alpha + ps;
+                m[rt] = mn;
+                // (the accumulators are rescaled only when some row's maximum moved)
+                if (__builtin_amdgcn_ballot_w64(alpha != 1.0f)) {
+#pragma unroll
+                    for (int n = 0; n < NCT; ++n) o[rt][n] *= alpha;
                 }
             }
         }
-        // (the next page's staging waits at its first barrier for every wave)
+        __syncthreads();
+        // (3) the next page's middle readings
+        if (ok_next) pf_phase_middle<D, PG, TilesF16<D>>(S.st, Tn, a, bn, h, tid);
+
+        // O^T += V^T P^T: A = channels 16 n + q16 x keys 4 g .. + 3 (hi, lo); B = the lane's
+        // probabilities (hi, lo); the hi x hi, hi x lo and lo x hi products
+        if (work) {
+#pragma unroll
+            for (int n = 0; n < NCT; ++n) {
+                const h4 vh = *reinterpret_cast<const h4*>(&Tc.vh[16 * n + q16][4 * g]);
+                const h4 vl = *reinterpret_cast<const h4*>(&Tc.vl[16 * n + q16][4 * g]);
+#pragma unroll
+                for (int rt = 0; rt < kWideTiles; ++rt) {
+                    if (rt < R) {
+                        o[rt][n] = __builtin_amdgcn_mfma_f32_16x16x16f16(vh, ph[rt], o[rt][n], 0, 0, 0);
+                        o[rt][n] = __builtin_amdgcn_mfma_f32_16x16x16f16(vh, pl[rt], o[rt][n], 0, 0, 0);
+                        o[rt][n] = __builtin_amdgcn_mfma_f32_16x16x16f16(vl, ph[rt], o[rt][n], 0, 0, 0);
+                    }
+                }
+            }
+        }
+        __syncthreads();
+        // (4) the next page's COO entries; after the barrier its tiles are complete and this
+        //     page's are free for the page after
+        if (ok_next) pf_phase_entries<D, PG, TilesF16<D>>(S.st, Tn, tk, tv, tid);
+        __syncthreads();
+        ok_cur = ok_next;
     }
 
     // ---- outputs, or this range's partials ------------------------------------------------
