@@ -431,21 +431,30 @@ __global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(3)))
         return *reinterpret_cast<const uint4*>(record(b, pw_) + 16 * pc_);
     };
 
+    // One set of tiles and one staging area, with the next page's bucket phase overlapped:
+    // once a page's partial scores are out, its records are no longer read, so the next
+    // page is staged and its buckets, constants and table are formed while this page's
+    // softmax and value product run.
     uint4 cur = prefetch(pg_first), nxt = prefetch(pg_first + 1);
-    for (int pg = pg_first; pg < pg_end; ++pg) {
-        const int b = btab[pg];
-        // (1) stage this page's prefetched bytes, request the bytes two pages ahead
+    bool ok_cur = false;   // (uniform) the page in the tiles is valid
+    if (pg_first < pg_end) {
+        const int b = btab[pg_first];
         if (tid < 2 * PF::CH) *reinterpret_cast<uint4*>(&S.st.rec[pw_][16 * pc_]) = cur;
         cur = nxt;
-        nxt = prefetch(pg + 2);
+        nxt = prefetch(pg_first + 2);
         __syncthreads();
-        if (!valid_block(b)) continue;   // (uniform; a precondition violation reads nothing)
-        pf_dequant_page<D, PG>(S.st, S.tl, a, b, h, tk, tv, tid);
+        ok_cur = valid_block(b);   // (a precondition violation reads nothing)
+        if (ok_cur) pf_dequant_page<D, PG>(S.st, S.tl, a, b, h, tk, tv, tid);
+    }
+    for (int pg = pg_first; pg < pg_end; ++pg) {
+        const bool has_next = pg + 1 < pg_end;
+        const int bn = has_next ? btab[pg + 1] : -1;
+        const bool ok_next = has_next && valid_block(bn);
         const bool full = pg * kPage + kPage - 1 <= vis_hi && pg * kPage >= vis_lo;
 
         // (5) partial scores of every row tile over this wave's channels: lane (g, query
         //     row q) gets S^T[4 g + r][q] over channels CPW w .. + CPW
-        {
+        if (ok_cur) {
             const float* krow = &S.tl.kt[lane & 15][CPW * wave + KSW * g];
             float ka[KSW];
 #pragma unroll
@@ -462,60 +471,75 @@ __global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(3)))
                 S.sp[wave][rt][lane] = sc;
             }
         }
+        // (1) stage the next page's prefetched bytes, request the bytes three pages ahead
+        if (has_next && tid < 2 * PF::CH) *reinterpret_cast<uint4*>(&S.st.rec[pw_][16 * pc_]) = cur;
+        cur = nxt;
+        nxt = prefetch(pg + 3);
         __syncthreads();
+        // (2) the next page's buckets, constants and middle-reading table
+        if (ok_next) pf_phase_buckets<D, PG, TilesF32<D>>(S.st, tk, tv, tid);
 
-        // (6) whole scores (the waves' partials summed), online softmax of the lane's query
-        //     row over the page's 16 keys (four here, the other twelve on lanes +-16, +-32),
-        //     then the value product over this wave's output channels
+        if (ok_cur) {
+            // (6) whole scores (the waves' partials summed), online softmax of the lane's query
+            //     row over the page's 16 keys (four here, the other twelve on lanes +-16, +-32),
+            //     then the value product over this wave's output channels
 #pragma unroll
-        for (int rt = 0; rt < kMaxRowTiles; ++rt) {
-            if (rt >= R) break;
-            f4 sc = S.sp[0][rt][lane];
+            for (int rt = 0; rt < kMaxRowTiles; ++rt) {
+                if (rt >= R) break;
+                f4 sc = S.sp[0][rt][lane];
 #pragma unroll
-            for (int w = 1; w < kWaves; ++w) sc += S.sp[w][rt][lane];
-            float v[4];
-            if (full) {
+                for (int w = 1; w < kWaves; ++w) sc += S.sp[w][rt][lane];
+                float v[4];
+                if (full) {
 #pragma unroll
-                for (int r = 0; r < 4; ++r) v[r] = sc[r];
-            } else {
+                    for (int r = 0; r < 4; ++r) v[r] = sc[r];
+                } else {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int kp = pg * kPage + 4 * g + r;   // key position
+                        const bool vis = rok[rt] && kp <= rpos[rt] && kp >= rlo[rt];
+                        v[r] = vis ? sc[r] : -INFINITY;
+                    }
+                }
+                const float mx = max4(fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])));
+                const float mn = fmaxf(m[rt], mx);
+                // (a row with no visible key yet keeps l = 0 and o = 0 whatever alpha is)
+                const float ms = (mn == -INFINITY) ? 0.0f : mn;
+                const float alpha = __builtin_amdgcn_exp2f(m[rt] - ms);
+                float p[4], ps = 0.0f;
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    const int kp = pg * kPage + 4 * g + r;   // key position
-                    const bool vis = rok[rt] && kp <= rpos[rt] && kp >= rlo[rt];
-                    v[r] = vis ? sc[r] : -INFINITY;
+                    p[r] = __builtin_amdgcn_exp2f(v[r] - ms);
+                    ps += p[r];
+                }
+                ps = sum4(ps);
+                l[rt] = l[rt] * alpha + ps;
+                m[rt] = mn;
+                // (the accumulators are rescaled only when some row's maximum moved)
+                if (__builtin_amdgcn_ballot_w64(alpha != 1.0f)) {
+#pragma unroll
+                    for (int n = 0; n < NCT; ++n) o[rt][n] *= alpha;
+                }
+                // O^T += V^T P^T: A = the value tile's channels (row) x tokens 4 g + s, B = this
+                // lane's probabilities
+#pragma unroll
+                for (int n = 0; n < NCT; ++n) {
+                    const float4 va =
+                        *reinterpret_cast<const float4*>(&S.tl.vt[CPW * wave + 16 * n + (lane & 15)][4 * g]);
+                    o[rt][n] = mfma4(va.x, p[0], o[rt][n]);
+                    o[rt][n] = mfma4(va.y, p[1], o[rt][n]);
+                    o[rt][n] = mfma4(va.z, p[2], o[rt][n]);
+                    o[rt][n] = mfma4(va.w, p[3], o[rt][n]);
                 }
             }
-            const float mx = max4(fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])));
-            const float mn = fmaxf(m[rt], mx);
-            // (a row with no visible key yet keeps l = 0 and o = 0 whatever alpha is)
-            const float ms = (mn == -INFINITY) ? 0.0f : mn;
-            const float alpha = __builtin_amdgcn_exp2f(m[rt] - ms);
-            float p[4], ps = 0.0f;
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                p[r] = __builtin_amdgcn_exp2f(v[r] - ms);
-                ps += p[r];
-            }
-            ps = sum4(ps);
-            l[rt] = l[rt] * alpha + ps;
-            m[rt] = mn;
-            // (the accumulators are rescaled only when some row's maximum moved)
-            if (__builtin_amdgcn_ballot_w64(alpha != 1.0f)) {
-#pragma unroll
-                for (int n = 0; n < NCT; ++n) o[rt][n] *= alpha;
-            }
-            // O^T += V^T P^T: A = the value tile's channels (row) x tokens 4 g + s, B = this
-            // lane's probabilities
-#pragma unroll
-            for (int n = 0; n < NCT; ++n) {
-                const float4 va = *reinterpret_cast<const float4*>(&S.tl.vt[CPW * wave + 16 * n + (lane & 15)][4 * g]);
-                o[rt][n] = mfma4(va.x, p[0], o[rt][n]);
-                o[rt][n] = mfma4(va.y, p[1], o[rt][n]);
-                o[rt][n] = mfma4(va.z, p[2], o[rt][n]);
-                o[rt][n] = mfma4(va.w, p[3], o[rt][n]);
-            }
         }
-        // (the next page's staging and tiles wait at its first barrier for every wave)
+        __syncthreads();
+        // (3), (4) the next page's middle readings and COO entries into the tiles
+        if (ok_next) pf_phase_middle<D, PG, TilesF32<D>>(S.st, S.tl, a, bn, h, tid);
+        __syncthreads();
+        if (ok_next) pf_phase_entries<D, PG, TilesF32<D>>(S.st, S.tl, tk, tv, tid);
+        __syncthreads();
+        ok_cur = ok_next;
     }
 
     // ---- outputs (this wave's channels), or this range's partials ------------------------
