@@ -577,7 +577,7 @@ constexpr int kWideRows = 128;
 constexpr int kWideTiles = kWideRows / kWaves / 16;   // row tiles per wave
 
 template <bool PG>
-__global__ __launch_bounds__(kPfThreads) void prefill_wide_kernel(PrefillArgs a) {
+__global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(3))) void prefill_wide_kernel(PrefillArgs a) {
     constexpr int D = 128;
     using PL = PfLayout<D, PG>;
     using PF = PfPrefetch<D, PG>;
