@@ -326,8 +326,12 @@ def prefill_bench(args, w, cache, bt, lens, dev, bt_cpu):
     # query tokens per row block: blocks of 64 rows, or of 128 on the fp16 matrix cores when
     # the chunks hold more rows per KV head than 64 (head_dim 128; the library's rule)
     G = Hq // H
-    wide = d == 128 and G * -(-n_tok // n) > 64
-    tpb = (128 if wide else 64) // G
+    # (the library's block rule: 128-row blocks past 64 rows per KV head at head_dim 128, else
+    # blocks of 16, 32 or 64 rows sized to the mean chunk)
+    rows = G * -(-n_tok // n)
+    wide = d == 128 and rows > 64
+    block_rows = 128 if wide else (16 if rows <= 16 else (32 if rows <= 32 else 64))
+    tpb = max(1, block_rows // G)
     one_pass, passes = 0, 0
     for s in range(n):
         last = int(cached[s]) - 1
@@ -368,7 +372,7 @@ def prefill_bench(args, w, cache, bt, lens, dev, bt_cpu):
                                   f"({n_tok} query tokens), {Hq}/{H} heads, d {d}, context {w.ctx_min}..{w.ctx}"
                                   + (f", sliding window {win}" if win else ""),
                       "global_batch": n, "seq_len": max_len, "parallelism": "single GPU"},
-           "row_block_rows": 128 if wide else 64,
+           "row_block_rows": block_rows,
            "roofline": dict(roof, traffic=None,
                             row_blocks_per_chunk=round(passes / max(1, sum(1 for s in range(n) if int(clen[s]) > 0)), 3)),
            "roofline_other": other}

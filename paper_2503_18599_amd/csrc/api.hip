@@ -388,10 +388,11 @@ size_t oaken_prefill_attention_workspace_bytes(int32_t n_tokens, int32_t n_q_hea
         n_q_heads / n_kv_heads > 8 || !supported_dim(head_dim) || max_seq_len <= 0 || sliding_window < 0)
         return 0;
     // (the call picks the block width from the chunk lengths: room for either plan)
-    const oaken::PrefillPlan p0 = oaken::plan_prefill(n_tokens, n_q_heads, n_kv_heads, max_seq_len, sliding_window, false);
+    // (64-row blocks at most: the fewest blocks, hence the most splits any call can plan)
+    const oaken::PrefillPlan p0 = oaken::plan_prefill(n_tokens, n_q_heads, n_kv_heads, max_seq_len, sliding_window, false, 4);
     size_t total = prefill_ws(n_tokens, n_q_heads, head_dim, p0).total;
     if (head_dim == 128) {
-        const oaken::PrefillPlan p1 = oaken::plan_prefill(n_tokens, n_q_heads, n_kv_heads, max_seq_len, sliding_window, true);
+        const oaken::PrefillPlan p1 = oaken::plan_prefill(n_tokens, n_q_heads, n_kv_heads, max_seq_len, sliding_window, true, 4);
         total = std::max(total, prefill_ws(n_tokens, n_q_heads, head_dim, p1).total);
     }
     return total;
@@ -417,11 +418,16 @@ int oaken_prefill_attention(const oaken_cache* cache, const void* q, int32_t n_q
     if (!std::isfinite(softmax_scale)) return fail(OAKEN_ERR_INVALID_ARG, "softmax_scale not finite");
     if (sliding_window < 0) return fail(OAKEN_ERR_INVALID_ARG, "sliding_window must be >= 0");
     const bool wide = oaken::prefill_wide(n_tokens, n_seqs, n_q_heads, cache->n_kv_heads, cache->head_dim);
-    const oaken::PrefillPlan p = oaken::plan_prefill(n_tokens, n_q_heads, cache->n_kv_heads, max_seq_len,
-                                                     sliding_window, wide);
-    const PrefillWs w = prefill_ws(n_tokens, n_q_heads, cache->head_dim, p);
+    const int32_t rt = oaken::prefill_row_tiles(n_tokens, n_seqs, n_q_heads, cache->n_kv_heads);
     const size_t need = oaken_prefill_attention_workspace_bytes(n_tokens, n_q_heads, cache->n_kv_heads,
                                                                 cache->head_dim, max_seq_len, sliding_window);
+    oaken::PrefillPlan p = oaken::plan_prefill(n_tokens, n_q_heads, cache->n_kv_heads, max_seq_len, sliding_window,
+                                               wide, rt);
+    // (smaller blocks never plan more splits than the 64-row plan the query sized for; the
+    // check keeps that a guarantee)
+    if (prefill_ws(n_tokens, n_q_heads, cache->head_dim, p).total > need)
+        p = oaken::plan_prefill(n_tokens, n_q_heads, cache->n_kv_heads, max_seq_len, sliding_window, wide, 4);
+    const PrefillWs w = prefill_ws(n_tokens, n_q_heads, cache->head_dim, p);
     if (!workspace || workspace_bytes < need)
         return fail(OAKEN_ERR_WORKSPACE, "prefill attention workspace %zu < %zu bytes", workspace_bytes, need);
     if (reinterpret_cast<uintptr_t>(workspace) % 16 != 0)
@@ -457,6 +463,7 @@ int oaken_prefill_attention(const oaken_cache* cache, const void* q, int32_t n_q
     a.spool = static_cast<const uint8_t*>(cache->sparse_pool);
     a.spages = cache->sparse_pages;
     a.wide = p.wide ? 1 : 0;
+    a.row_tiles = p.row_tiles;
     const hipStream_t s = static_cast<hipStream_t>(stream);
     int rc = hip_status(oaken::launch_prefill(a, cache->head_dim, reinterpret_cast<int2*>(ws + w.part),
                                               reinterpret_cast<int32_t*>(ws + w.part + w.blocks), s),

@@ -81,7 +81,6 @@ struct PfLayout {
 };
 
 constexpr int kWaves = kPfThreads / 64;
-constexpr int kMaxRowTiles = kRowsPerBlock / 16;
 
 // What every prefill kernel stages per page: the two records' bytes, the per-slot
 // dequantization constants, the COO bytes used and each COO byte's (slot, chunk) bucket.
@@ -175,11 +174,11 @@ struct TilesF16 {
     }
 };
 
-template <int D, bool PG>
+template <int D, bool PG, int RT>
 struct PfSmem {
     PfStage<D, PG> st;
     TilesF32<D> tl;
-    f4 sp[kWaves][kMaxRowTiles][64];                 // per wave: partial scores over its channels
+    f4 sp[kWaves][RT][64];                           // per wave: partial scores over its channels
 };
 template <int D, bool PG>
 struct PfWideSmem {
@@ -358,8 +357,11 @@ __device__ __forceinline__ PfBlock pf_block(const PrefillArgs& a, int split) {
     return B;
 }
 
-template <int D, bool PG>
-__global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(3))) void prefill_kernel(PrefillArgs a) {
+// RT 16-row tiles per block (1, 2 or 4): registers and LDS sized for them, so that short
+// chunks get more workgroups per CU.
+template <int D, bool PG, int RT>
+__global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(RT == 1 ? 4 : 3))) void prefill_kernel(
+    PrefillArgs a) {
     using PL = PfLayout<D, PG>;
     using PF = PfPrefetch<D, PG>;
     constexpr int CPW = D / kWaves;    // channels of each wave (scores and outputs)
@@ -367,7 +369,7 @@ __global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(3)))
     constexpr int NCT = CPW / 16;      // 16-wide output tiles of a wave
     static_assert(PL::PRE % 16 == 0 && 2 * PF::CH <= kPfThreads, "one prefetch chunk per thread");
 
-    __shared__ PfSmem<D, PG> S;
+    __shared__ PfSmem<D, PG, RT> S;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 4;
     if ((int)blockIdx.x >= *a.n_row_blocks) return;   // (uniform)
     const int h = blockIdx.y, split = blockIdx.z;
@@ -390,9 +392,9 @@ __global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(3)))
     // probabilities as the B operand of the value product and its outputs, and the softmax
     // state of that row.  B operand (queries, scaled): row tile rt, query row lane & 15,
     // this wave's channels CPW w + KSW g + k.
-    float bq[kMaxRowTiles][KSW];
+    float bq[RT][KSW];
 #pragma unroll
-    for (int rt = 0; rt < kMaxRowTiles; ++rt) {
+    for (int rt = 0; rt < RT; ++rt) {
         const int ra = 16 * rt + (lane & 15);
         const bool ok = ra < n_rows;
         const int i = i0 + (ok ? ra / G : 0), hd = ok ? ra % G : 0;
@@ -401,19 +403,19 @@ __global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(3)))
         for (int k = 0; k < KSW; ++k) bq[rt][k] = ok ? sl2 * h2f(qp[k]) : 0.0f;
     }
     // this lane's query row in each tile, its position and window start
-    int rpos[kMaxRowTiles], rlo[kMaxRowTiles];
-    bool rok[kMaxRowTiles];
+    int rpos[RT], rlo[RT];
+    bool rok[RT];
 #pragma unroll
-    for (int rt = 0; rt < kMaxRowTiles; ++rt) {
+    for (int rt = 0; rt < RT; ++rt) {
         const int rc = 16 * rt + (lane & 15);
         rok[rt] = rc < n_rows;
         rpos[rt] = start + i0 + (rok[rt] ? rc / G : 0);
         rlo[rt] = a.window > 0 ? max(0, rpos[rt] + 1 - a.window) : 0;
     }
-    float m[kMaxRowTiles], l[kMaxRowTiles];
-    f4 o[kMaxRowTiles][NCT];   // O^T: channels CPW w + 16 n + 4 g + r of the lane's query row
+    float m[RT], l[RT];
+    f4 o[RT][NCT];   // O^T: channels CPW w + 16 n + 4 g + r of the lane's query row
 #pragma unroll
-    for (int rt = 0; rt < kMaxRowTiles; ++rt) {
+    for (int rt = 0; rt < RT; ++rt) {
         m[rt] = -INFINITY;
         l[rt] = 0.0f;
 #pragma unroll
@@ -463,7 +465,7 @@ __global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(3)))
                 ka[k] = v.x; ka[k + 1] = v.y; ka[k + 2] = v.z; ka[k + 3] = v.w;
             }
 #pragma unroll
-            for (int rt = 0; rt < kMaxRowTiles; ++rt) {
+            for (int rt = 0; rt < RT; ++rt) {
                 if (rt >= R) break;
                 f4 sc = f4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
@@ -484,7 +486,7 @@ __global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(3)))
             //     row over the page's 16 keys (four here, the other twelve on lanes +-16, +-32),
             //     then the value product over this wave's output channels
 #pragma unroll
-            for (int rt = 0; rt < kMaxRowTiles; ++rt) {
+            for (int rt = 0; rt < RT; ++rt) {
                 if (rt >= R) break;
                 f4 sc = S.sp[0][rt][lane];
 #pragma unroll
@@ -544,7 +546,7 @@ __global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(3)))
 
     // ---- outputs (this wave's channels), or this range's partials ------------------------
 #pragma unroll
-    for (int rt = 0; rt < kMaxRowTiles; ++rt) {
+    for (int rt = 0; rt < RT; ++rt) {
         if (rt >= R || !rok[rt]) continue;
         const int rc = 16 * rt + (lane & 15);
         const int64_t row = (int64_t)(tok0 + i0 + rc / G) * a.Hq + h * G + rc % G;
@@ -821,11 +823,12 @@ __global__ __launch_bounds__(1024) void prefill_blocks_kernel(const int32_t* cu_
 }  // namespace
 
 PrefillPlan plan_prefill(int32_t n_tokens, int32_t n_q_heads, int32_t n_kv_heads, int32_t max_seq_len,
-                         int32_t window, bool wide) {
+                         int32_t window, bool wide, int32_t row_tiles) {
     PrefillPlan p{};
     const int G = n_q_heads / n_kv_heads;
     p.wide = wide;
-    p.tokens_per_block = (wide ? kWideRows : kRowsPerBlock) / G;
+    p.row_tiles = wide ? kWideRows / 16 : (row_tiles <= 1 ? 1 : (row_tiles <= 2 ? 2 : 4));
+    p.tokens_per_block = std::max(1, (wide ? kWideRows : 16 * p.row_tiles) / G);
     // keys a block can see: its own tokens and everything before them (or a window of W
     // before its first token)
     const int64_t span = window > 0 ? std::min<int64_t>(max_seq_len, (int64_t)window + p.tokens_per_block + kPage)
@@ -853,16 +856,24 @@ hipError_t launch_prefill(const PrefillArgs& a, int d, int2* row_blocks, int32_t
             hipLaunchKernelGGL(prefill_wide_kernel<false>, grid, dim3(kPfThreads), 0, st, a);
         return hipGetLastError();
     }
-    if (d == 128 && !pg)
-        hipLaunchKernelGGL((prefill_kernel<128, false>), grid, dim3(kPfThreads), 0, st, a);
-    else if (d == 128)
-        hipLaunchKernelGGL((prefill_kernel<128, true>), grid, dim3(kPfThreads), 0, st, a);
-    else if (d == 64 && !pg)
-        hipLaunchKernelGGL((prefill_kernel<64, false>), grid, dim3(kPfThreads), 0, st, a);
-    else if (d == 64)
-        hipLaunchKernelGGL((prefill_kernel<64, true>), grid, dim3(kPfThreads), 0, st, a);
-    else
-        return hipErrorInvalidValue;
+    if (d != 64 && d != 128) return hipErrorInvalidValue;
+    if (a.row_tiles != 1 && a.row_tiles != 2 && a.row_tiles != 4) return hipErrorInvalidValue;
+    auto go = [&](auto kernel) { hipLaunchKernelGGL(kernel, grid, dim3(kPfThreads), 0, st, a); };
+    if (d == 128) {
+        if (pg)
+            a.row_tiles == 1 ? go(prefill_kernel<128, true, 1>) : a.row_tiles == 2 ? go(prefill_kernel<128, true, 2>)
+                                                                   : go(prefill_kernel<128, true, 4>);
+        else
+            a.row_tiles == 1 ? go(prefill_kernel<128, false, 1>) : a.row_tiles == 2 ? go(prefill_kernel<128, false, 2>)
+                                                                    : go(prefill_kernel<128, false, 4>);
+    } else {
+        if (pg)
+            a.row_tiles == 1 ? go(prefill_kernel<64, true, 1>) : a.row_tiles == 2 ? go(prefill_kernel<64, true, 2>)
+                                                                  : go(prefill_kernel<64, true, 4>);
+        else
+            a.row_tiles == 1 ? go(prefill_kernel<64, false, 1>) : a.row_tiles == 2 ? go(prefill_kernel<64, false, 2>)
+                                                                   : go(prefill_kernel<64, false, 4>);
+    }
     return hipGetLastError();
 }
 

@@ -55,12 +55,14 @@ def _run(B, ref, case, chunk, window=0, paged=False, seed=5):
 
 
 @pytest.mark.parametrize("cid,kw,chunk,window,paged", [
-    (3, dict(n_seqs=3, ctx=600), 37, 0, False),           # MHA, ragged chunk
-    (4, dict(n_seqs=4, ctx=700, ctx_min=40), 64, 0, False),  # GQA, chunk = whole prompt for short ones (256-row blocks)
-    (4, dict(n_seqs=4, ctx=700, ctx_min=40), 50, 100, False),  # GQA with a sliding window (256-row blocks)
-    (2, dict(n_seqs=3, ctx=203), 203, 0, False),          # whole prompts from position 0 (256-row blocks)
-    (2, dict(n_seqs=2, ctx=700), 300, 0, False),          # MHA chunks of 300 tokens: two 256-row blocks each
-    (1, dict(), 16, 0, False)])
+    (3, dict(n_seqs=3, ctx=600), 37, 0, False),           # MHA, ragged chunk (64-row blocks)
+    (3, dict(n_seqs=3, ctx=600), 24, 0, False),           # MHA, 32-row blocks
+    (4, dict(n_seqs=4, ctx=300, ctx_min=40), 8, 0, False),   # GQA, 8-token chunks: 32-row blocks
+    (4, dict(n_seqs=4, ctx=700, ctx_min=40), 64, 0, False),  # GQA, chunk = whole prompt for short ones (128-row blocks)
+    (4, dict(n_seqs=4, ctx=700, ctx_min=40), 50, 100, False),  # GQA with a sliding window (128-row blocks)
+    (2, dict(n_seqs=3, ctx=203), 203, 0, False),          # whole prompts from position 0 (128-row blocks)
+    (2, dict(n_seqs=2, ctx=700), 300, 0, False),          # MHA chunks of 300 tokens: three 128-row blocks each
+    (1, dict(), 16, 0, False)])                           # head_dim 64, 16-row blocks
 def test_prefill_attention_matches_oracle(B, ref, cid, kw, chunk, window, paged):
     case = Case(synth.scaled(synth.WORKLOADS[cid], **kw))
     case.calibrate_oracle(ref)
@@ -70,10 +72,20 @@ def test_prefill_attention_matches_oracle(B, ref, cid, kw, chunk, window, paged)
     assert ok, (max_abs, max_rel)
 
 
+def test_prefill_short_mean_long_chunks(B, ref):
+    """Blocks are sized to the mean chunk: chunks of 20, 3, 2 and 20 tokens average 12 rows,
+    so the blocks hold 16 rows and each 20-token chunk takes two of them."""
+    case = Case(synth.scaled(synth.WORKLOADS[3], n_seqs=4, ctx=64, ctx_min=1), lens=[64, 3, 2, 50])
+    case.calibrate_oracle(ref)
+    got, want = _run(B, ref, case, 20)
+    ok, max_abs, max_rel = attention_tolerance(got, want)
+    assert ok, (max_abs, max_rel)
+
+
 @pytest.mark.parametrize("cid,chunk", [(3, 48), (4, 40)])
 def test_prefill_attention_paged(B, ref, cid, chunk):
     """On-demand sparse pages: 48-token MHA chunks (64-row blocks) and 40-token chunks of
-    four query heads per KV head (160 rows: the 256-row blocks on fp16 matrix cores)."""
+    four query heads per KV head (160 rows: the 128-row blocks on fp16 matrix cores)."""
     case = Case(synth.scaled(synth.WORKLOADS[cid], n_seqs=3, ctx=600))
     case.calibrate_oracle(ref)
     got, want = _run(B, ref, case, chunk, paged=True)
