@@ -1,8 +1,9 @@
 // Chunked-prefill attention over the quantized cache (the prefill stage also reads the KV
 // cache, Sec. 2.1; the sliding window of Sec. 6.1 applies per query).
 //
-// A workgroup takes a block of up to 64 query rows: consecutive query tokens of one
-// sequence's chunk times the query heads of one KV head.  It reads every page of the
+// A workgroup takes a block of 16, 32 or 64 query rows (sized to the mean chunk; longer
+// chunks take several blocks): consecutive query tokens of one sequence's chunk times the
+// query heads of one KV head.  It reads every page of the
 // keys those rows can see once, whatever the number of rows: each page record is staged
 // in LDS, dequantized into an fp32 tile (middle values from the dense nibbles, looked up
 // in a per-page table of each slot's 16 possible readings, then the COO entries overwrite
@@ -38,7 +39,6 @@
 namespace oaken {
 namespace {
 
-constexpr int kRowsPerBlock = 64;
 constexpr int kPfThreads = 256;
 
 typedef float f4 __attribute__((ext_vector_type(4)));
