@@ -236,10 +236,11 @@ int oaken_decode_attention_window(const oaken_cache* cache, const void* q, int32
  * already be in the cache: quantize the chunk's keys and values first.
  * out: fp32 [n_tokens][n_q_heads][head_dim].  Every p + 1 <= max_seq_len.
  * Rows (query token, query head) are processed in blocks: consecutive tokens of one chunk
- * times the query heads of one KV head, up to 64 rows contracted in fp32, or, at head_dim
- * 128 when the chunks average more than 64 rows per KV head, up to 128 rows on fp16 matrix
- * cores with every real operand split into high and low fp16 parts (fp32 accumulation).
- * A block reads each page of its keys once.
+ * times the query heads of one KV head, up to 16, 32 or 64 rows (sized to the mean chunk,
+ * n_tokens / n_seqs; a longer chunk takes several blocks) contracted in fp32, or, at
+ * head_dim 128 when the chunks average more than 64 rows per KV head, up to 128 rows on
+ * fp16 matrix cores with every real operand split into high and low fp16 parts (fp32
+ * accumulation).  A block reads each page of its keys once.
  * workspace: oaken_prefill_attention_workspace_bytes(...) bytes, 16-byte aligned (never 0
  * for valid sizes: it holds the row-block list, and split partials of long prefixes).
  */
