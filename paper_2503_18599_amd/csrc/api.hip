@@ -2,6 +2,7 @@
 // planning and error reporting.  Nothing here touches device memory contents.
 #include "oaken.h"
 #include "oaken_internal.h"
+#include "prefill_internal.h"
 
 #include <algorithm>
 #include <cmath>

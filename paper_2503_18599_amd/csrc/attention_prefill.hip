@@ -33,6 +33,7 @@
 // O^T += V_hi P_hi + V_hi P_lo + V_lo P_hi, accumulated in fp32.  A page is then read and
 // dequantized once for all the rows.
 #include "oaken_internal.h"
+#include "prefill_internal.h"
 
 #include <hip/hip_fp16.h>
 
