@@ -206,9 +206,10 @@ __device__ __forceinline__ uint4 ld16(const uint8_t* p) {
 //
 // Buffers live only in the phase that needs them share storage, which keeps the wave's
 // LDS small enough for more waves per CU: the fixed-point query (qi) is read only
-// before the key pass and sits in the table's space; q (key pass) shares with oci (value
-// pass); tokc (key pass) shares with wv (value pass) and, after the value pass, with the
-// value corrections on their way to the output lanes.
+// before the key pass and sits in the table's space; tokc (key pass) shares with the
+// value pass's wv and oci, which take turns within a group (wv is read by the matrix-core
+// operands before the correction walk clears oci and sums into it), and after the value
+// pass with the value corrections on their way to the output lanes.
 //
 // The correction walks take one token per lane, and the table is token-major: row tg (64
 // bytes) holds the four classes at 16-byte slots rotated by bits 1-2 of tg (so that lanes
@@ -220,7 +221,7 @@ struct Smem {
     __align__(16) uint8_t tab_[4 * GT * 2 * 8];   // correction table; qi
     __align__(16) uint8_t dense[GRP][PSTR];       // K: token rows of 64 bytes; V: page pairs
                                                   // (vflat)
-    __align__(16) uint8_t qo_[G * D * 4];         // q (keys); oci (values)
+    __align__(16) uint8_t q_[G * D * 2];          // q (keys)
     __align__(16) uint8_t tw_[cmax(cmax(GT * 16, G * GT * 8), G * D * 4)];
     float pbase[G];
     float m[G], l[G];
@@ -234,9 +235,9 @@ struct Smem {
     // query in fixed point (before the key pass)
     __device__ int (&qi())[G][D] { return *reinterpret_cast<int (*)[G][D]>(tab_); }
     // query in fp16, the heads of a channel side by side (key pass)
-    __device__ __half (&q16())[D][G] { return *reinterpret_cast<__half (*)[D][G]>(qo_); }
+    __device__ __half (&q16())[D][G] { return *reinterpret_cast<__half (*)[D][G]>(q_); }
     // value corrections of one group, fixed point (value pass)
-    __device__ int& oci(int hd, int ch) { return reinterpret_cast<int*>(qo_)[hd * D + ch]; }
+    __device__ int& oci(int hd, int ch) { return reinterpret_cast<int*>(tw_)[hd * D + ch]; }
     // base, Delta, Gp of the group's tokens (key pass)
     __device__ float4 (&tokc())[GT] { return *reinterpret_cast<float4 (*)[GT]>(tw_); }
     // value-pass weights of token pairs: 4 features, 4 limbs (value pass)
@@ -419,8 +420,8 @@ __device__ __forceinline__ const T& lds_at(const Smem<G>& S, uint32_t off) {
     return *reinterpret_cast<const T*>(reinterpret_cast<const char*>(&S) + off);
 }
 
-static_assert(offsetof(Smem<1>, dense) == 4096 && offsetof(Smem<1>, qo_) % 256 == 0 &&
-              offsetof(Smem<2>, qo_) % 256 == 0 && offsetof(Smem<4>, qo_) % 256 == 0 &&
+static_assert(offsetof(Smem<1>, dense) == 4096 && offsetof(Smem<1>, q_) % 256 == 0 &&
+              offsetof(Smem<2>, q_) % 256 == 0 && offsetof(Smem<4>, q_) % 256 == 0 &&
               sizeof(Smem<4>::tab_) >= sizeof(int) * 4 * D, "LDS layout the correction addressing relies on");
 
 template <int G>
@@ -667,7 +668,7 @@ __device__ __forceinline__ void value_corrections(Smem<G>& S, const AttnArgs& a,
 }
 
 template <int G, bool PG>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 : 1))) void attn_mfma_kernel(AttnArgs a) {
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void attn_mfma_kernel(AttnArgs a) {
     constexpr int NRS = (G + 1) / 2;        // key-pass MFMA row sets (8 rows per head)
     __shared__ Smem<G> S;
     extern __shared__ float sc[];           // [G][cap]: scores, then probabilities
@@ -926,8 +927,6 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
             S.m[hd] = mx;
             S.l[hd] = sum;
         }
-        S.oci(hd, lane) = 0;
-        S.oci(hd, lane + 64) = 0;
     }
     stage_counts(S, hreg, lane);
     wave_sync();
@@ -1105,6 +1104,15 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
 #pragma unroll
             for (int nt = 0; nt < 8; ++nt) oacc[nt] += ldexpf(limbs(gacc[nt]), -e);
         }
+        // the integer sums replace the weights just read (a wave's LDS operations run in
+        // issue order)
+        wave_sync();
+#pragma unroll
+        for (int hd = 0; hd < G; ++hd) {
+            S.oci(hd, lane) = 0;
+            S.oci(hd, lane + 64) = 0;
+        }
+        wave_sync();
         value_corrections<G, PG>(S, a, sc, cap, unpack_run(run_c), staged, gc, tok0, lane);
         wave_sync();
         // fold the group's integer sums into the fp32 outputs
@@ -1112,9 +1120,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 1 ? 3 :
         for (int hd = 0; hd < G; ++hd) {
             ocr[hd][0] += ldexpf((float)S.oci(hd, lane), -fsh);
             ocr[hd][1] += ldexpf((float)S.oci(hd, lane + 64), -fsh);
-            S.oci(hd, lane) = 0;
-            S.oci(hd, lane + 64) = 0;
         }
+        wave_sync();   // (the next group's weights replace the sums)
         gc = gn;
         gn = gnn;
         tab_n = tab_nn;
@@ -1185,9 +1192,9 @@ bool mfma_attention_supported(int d, int G) { return d == D && G >= 1 && G <= 8;
 // G = 8 and 4 take four heads per workgroup, 6 and 2 two, the odd counts one.
 int mfma_wave_heads(int G) { return G % 4 == 0 ? 4 : (G % 2 == 0 ? 2 : 1); }
 
-// Four heads per workgroup keep 20 pages of scores (the wave's LDS then allows eight
-// waves per CU instead of seven; measured faster on the GQA layers), the others 32.
-int mfma_score_cap(int wave_heads) { return wave_heads == 4 ? 320 : 512; }
+// Four heads per workgroup keep 16 pages of scores (the wave's LDS then allows nine
+// waves per CU; measured faster on the GQA layers than 15 or 20 pages), the others 32.
+int mfma_score_cap(int wave_heads) { return wave_heads == 4 ? 256 : 512; }
 
 hipError_t launch_attention_mfma(const AttnArgs& a, hipStream_t st) {
     return a.spool ? launch_attention_mfma_paged(a, st) : launch_mfma<false>(a, st);
