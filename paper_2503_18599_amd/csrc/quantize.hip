@@ -484,30 +484,41 @@ __global__ __launch_bounds__(256) void quantize_token_kernel(QuantArgs a) {
     const int lane = threadIdx.x & 63, r = lane / LPV, m = lane % LPV;
     const int64_t v = ((int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6)) * VPW + r;
     const int nhw = 2 * a.H;
-    bool ok = v < (int64_t)a.n_seqs * nhw;
-    const int s = ok ? (int)(v / nhw) : 0, hw = ok ? (int)(v % nhw) : 0;
+    const bool in_range = v < (int64_t)a.n_seqs * nhw;
+    const int s = in_range ? (int)(v / nhw) : 0, hw = in_range ? (int)(v % nhw) : 0;
     const int h = hw >> 1, which = hw & 1;
-    const int row = a.cu_tokens[s];
-    ok = ok && a.cu_tokens[s + 1] - row == 1;
-    const int pos = a.start_pos[s];
+    // The loads form three dependent levels, each issued whole before its first use:
+    // the sequence's row and position; its block and the input vector; what the record
+    // keeps from earlier slots.
+    const int row = a.cu_tokens[s], row_end = a.cu_tokens[s + 1], pos = a.start_pos[s];
+    asm volatile("" ::"v"(row), "v"(row_end), "v"(pos));   // (issued together, one wait)
+    const float* th = a.thr + hw * 4;
+    const float lo_o = th[0], lo_i = th[1], hi_i = th[2], hi_o = th[3];
     const int page = pos / kPage, slot = pos % kPage;
-    ok = ok && pos >= 0 && page < a.max_blocks;
-    const int blk = ok ? a.block_table[(int64_t)s * a.max_blocks + page] : 0;
+    bool ok = in_range && row_end - row == 1 && pos >= 0 && page < a.max_blocks;
+    int blk = -1;
+    uint4 x = make_uint4(0, 0, 0, 0);
+    if (ok) {
+        blk = a.block_table[(int64_t)s * a.max_blocks + page];
+        x = *reinterpret_cast<const uint4*>((which ? a.v_new : a.k_new) + ((int64_t)row * a.H + h) * D + 8 * m);
+    }
     ok = ok && blk >= 0 && blk < a.num_blocks;
     uint8_t* rec = a.pool + (((int64_t)(ok ? blk : 0) * a.H + h) * 2 + which) * a.stride;
-
-    uint4 x = make_uint4(0, 0, 0, 0);
-    if (ok) x = *reinterpret_cast<const uint4*>((which ? a.v_new : a.k_new) + ((int64_t)row * a.H + h) * D + 8 * m);
-    // COO bytes of the record's earlier slots (2 count bytes per lane cover 2 * LPV >= slot * NC)
+    // COO bytes of the record's earlier slots (2 count bytes per lane cover 2 * LPV >=
+    // slot * NC), and V at an odd slot: the bytes it shares with the slot before
     int c = 0;
+    uint32_t old_b[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) old_b[e] = 0;
     if (ok) {
         const int b0 = 2 * m, b1 = 2 * m + 1;
         c = (b0 < slot * NC ? (int)rec[LY.counts + b0] : 0) + (b1 < slot * NC ? (int)rec[LY.counts + b1] : 0);
+        if (which == 1 && (slot & 1)) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) old_b[e] = rec[LY.dense + (8 * m + e) * (kPage / 2) + (slot >> 1)];
+        }
     }
     const int pre = min(group_sum<LPV>(c), CAP);
-    uint32_t old_b = 0;   // V at an odd slot shares its bytes with the slot before
-    const float* th = a.thr + hw * 4;
-    const float lo_o = th[0], lo_i = th[1], hi_i = th[2], hi_o = th[3];
 
     const uint32_t w4[4] = {x.x, x.y, x.z, x.w};
     const LaneCodes Q = quantize_lane<LPV>(w4, lo_o, lo_i, hi_i, hi_o, m, lane);
@@ -525,11 +536,9 @@ __global__ __launch_bounds__(256) void quantize_token_kernel(QuantArgs a) {
         // channel-major: channel j's byte slot / 2, low nibble the even slot; writing an
         // even slot clears the odd one after it
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            uint8_t* bp = rec + LY.dense + (8 * m + e) * (kPage / 2) + (slot >> 1);
-            if (slot & 1) old_b = *bp;
-            *bp = (uint8_t)((slot & 1) ? ((old_b & 0x0fu) | (Q.nib[e] << 4)) : Q.nib[e]);
-        }
+        for (int e = 0; e < 8; ++e)
+            rec[LY.dense + (8 * m + e) * (kPage / 2) + (slot >> 1)] =
+                (uint8_t)((slot & 1) ? ((old_b[e] & 0x0fu) | (Q.nib[e] << 4)) : Q.nib[e]);
     }
     if (m < 6) reinterpret_cast<uint16_t*>(rec + LY.meta + slot * 12)[m] = float_to_half_bits(Q.meta);
     if ((m & 7) == 0) rec[LY.counts + slot * NC + (m >> 3)] = (uint8_t)c8;
