@@ -176,7 +176,9 @@ int oaken_calibrate_thresholds(const void* k_calib, const void* v_calib, int32_t
  * cu_tokens[s+1]-1 belong to sequence s and land at positions start_pos[s] + i.
  * block_table: int32 [n_seqs][max_blocks_per_seq] maps logical page pos/P to a
  * physical block.  cu_tokens: int32 [n_seqs+1]; start_pos: int32 [n_seqs].
- * max_new_per_seq bounds cu_tokens[s+1]-cu_tokens[s] (it sizes the launch).
+ * max_new_per_seq bounds cu_tokens[s+1]-cu_tokens[s] (it sizes the launch); a
+ * sequence with more rows than that may have some of them left unwritten, and
+ * nothing outside its own pages is ever written.
  * Preconditions: every block id < num_blocks; each sequence owns its pages; the
  * positions written are the sequence's next positions.
  */
