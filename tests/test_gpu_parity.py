@@ -13,7 +13,7 @@ import pytest
 import torch
 
 from paper_2503_18599_amd import synth
-from tests.cases import Case, attention_tolerance, compare_pools, np16
+from tests.cases import P, Case, attention_tolerance, compare_pools, np16
 
 pytestmark = pytest.mark.gpu
 
@@ -117,6 +117,41 @@ def test_decode_append_bit_exact(B, ref, name):
                       cu.to(DEV), 1)
     want = case.oracle_pool(ref)
     compare_pools(ref, case, cache.pool.cpu().numpy(), want)
+
+
+@pytest.mark.parametrize("mode", ["segment", "token"])
+def test_quantize_rows_beyond_the_launch_bound(B, ref, mode):
+    """A sequence with more new rows than max_new_per_seq (a caller error the library cannot
+    see): the other sequence's record is exact, and no byte outside the two sequences' own
+    pages is written.  The segment kernel still writes the overrunning sequence's first page;
+    the decode-step kernel skips that sequence."""
+    lens, bound = ([60, 10], 20) if mode == "segment" else ([2, 1], 1)
+    w = synth.scaled(synth.WORKLOADS[2], n_seqs=2, ctx=max(lens))
+    case = Case(w, lens=lens)
+    case.calibrate_oracle(ref)
+    want = case.oracle_pool(ref)
+    cache, bt = _gpu_cache(B, case, prefill=False)
+    B.quantize_kv(cache, case.k.to(DEV), case.v.to(DEV), bt,
+                  torch.zeros(case.n_seqs, dtype=torch.int32, device=DEV), case.cu.to(DEV), bound)
+    got = cache.pool.cpu().numpy()
+    lay = ref.layout(P, case.d)
+    st = lay["stride"]
+    pages = [(int(lens[s]) + P - 1) // P for s in range(2)]
+    own0 = {int(b) for b in case.bt[0, :pages[0]]}
+    exact = {int(case.bt[1, 0])} | ({int(case.bt[0, 0])} if mode == "segment" else set())
+    for b in range(case.num_blocks):
+        for h in range(case.H):
+            for wv in (0, 1):
+                off = ((b * case.H + h) * 2 + wv) * st
+                g, e = got[off:off + st], want[off:off + st]
+                if b in exact:
+                    used = lay["sparse"] + int(e[:lay["meta"]].sum())
+                    assert np.array_equal(g[:used], e[:used]), (mode, b, h, wv)
+                elif b not in own0:
+                    assert not g.any(), (mode, b, h, wv)
+    if mode == "token":
+        b0 = int(case.bt[0, 0])
+        assert not got[b0 * case.H * 2 * st:(b0 + 1) * case.H * 2 * st].any()
 
 
 def test_quantize_edge_thresholds(B, ref):
