@@ -667,8 +667,10 @@ __device__ __forceinline__ void value_corrections(Smem<G>& S, const AttnArgs& a,
     }
 }
 
+// Three waves per SIMD (168 registers), except four heads over on-demand sparse pages, which
+// would spill there and take what they need (two waves per SIMD).
 template <int G, bool PG>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void attn_mfma_kernel(AttnArgs a) {
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 4 && PG ? 1 : 3))) void attn_mfma_kernel(AttnArgs a) {
     constexpr int NRS = (G + 1) / 2;        // key-pass MFMA row sets (8 rows per head)
     __shared__ Smem<G> S;
     extern __shared__ float sc[];           // [G][cap]: scores, then probabilities
@@ -807,7 +809,12 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void at
         wave_sync();
 #pragma unroll
         for (int pg = 0; pg < GRP; ++pg) dreg[pg] = ld16(gc.base[pg] + koff);
+        // (one head: issued in the loop's own order, dense bytes first, so that the wait
+        // counts at the loop head cover only what the first group needs first; with more
+        // heads the fixed order costs register spills)
+        if constexpr (G == 1) __builtin_amdgcn_sched_barrier(0);
         sparse_chunks<PG>(a, gc, tab_c, used, lane, sreg0, sreg1);
+        if constexpr (G == 1) __builtin_amdgcn_sched_barrier(0);
     }
     Grp gn = make_group(pl, krec, p_begin, p_begin + GRP, p_end, lane);
     hreg = count_chunk(gn, lane);
@@ -881,6 +888,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void at
         Grp gnn;
         int2 tab_nn = tab_n;
         {
+            // (the metadata first: the next group needs it before its sparse bytes)
+            mreg = meta_words(gn, lane);
             stage_counts(S, hreg, lane);
             wave_sync();
             Run r;
@@ -888,7 +897,6 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void at
             run_n = pack_run(r);
             wave_sync();
             sparse_chunks<PG>(a, gn, tab_n, used, lane, sreg0, sreg1);
-            mreg = meta_words(gn, lane);
             gnn = make_group(pl, krec, p_begin, g0 + 2 * GRP, p_end, lane);
             hreg = count_chunk(gnn, lane);
             if constexpr (PG) tab_nn = page_tab(gnn, lane);
@@ -951,7 +959,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void at
         wave_sync();
 #pragma unroll
         for (int pg = 0; pg < GRP; ++pg) dreg[pg] = ld16(gc.base[pg] + voff);
+        if constexpr (G == 1) __builtin_amdgcn_sched_barrier(0);   // (as for the keys)
         sparse_chunks<PG>(a, gc, tab_c, used, lane, sreg0, sreg1);
+        if constexpr (G == 1) __builtin_amdgcn_sched_barrier(0);
     }
     gn = make_group(pl, vrec, p_begin, p_begin + GRP, p_end, lane);
     hreg = count_chunk(gn, lane);
@@ -1026,6 +1036,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void at
         Grp gnn;
         int2 tab_nn = tab_n;
         {
+            // (the metadata first: the next group needs it before its sparse bytes)
+            mreg = meta_words(gn, lane);
             stage_counts(S, hreg, lane);
             wave_sync();
             Run r;
@@ -1033,7 +1045,6 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void at
             run_n = pack_run(r);
             wave_sync();
             sparse_chunks<PG>(a, gn, tab_n, used, lane, sreg0, sreg1);
-            mreg = meta_words(gn, lane);
             gnn = make_group(pl, vrec, p_begin, g0 + 2 * GRP, p_end, lane);
             hreg = count_chunk(gnn, lane);
             if constexpr (PG) tab_nn = page_tab(gnn, lane);
