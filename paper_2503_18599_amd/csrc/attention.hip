@@ -202,23 +202,34 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
     }
 }
 
-// Log-sum-exp merge of the per-range partials of one (sequence, query head).
 // Log-sum-exp merge of the page ranges' partials (m, l, o) of one (sequence, query head)
 // row.  NW waves share the row's ranges (wave w takes ranges w, w + NW, ...), each lane
 // D / 64 channels, with a running maximum (the sums are rescaled when it grows), unrolled
-// so that several ranges' loads are in flight together; ranges with l = 0 (past a
-// sequence's end) are skipped.  The waves' (M, den, num) then meet in LDS.
+// so that several ranges' loads are in flight together; ranges with l = 0 are skipped.
+// Decode rows (seq_lens given) read only the ranges that hold keys of their sequence:
+// those starting before its last page (the others are empty by construction), so a batch
+// of mixed lengths reads no partials of the empty ranges.  The waves' (M, den, num) then
+// meet in LDS.
 template <int D, int NW>
 __global__ __launch_bounds__(64 * NW) void attn_combine_kernel(AttnArgs a) {
     constexpr int V = D / 64;
     const int64_t row = blockIdx.x;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const float* pp = a.partial + row * a.n_splits * (D + 2);
+    int n_used = a.n_splits;
+    if (a.seq_lens) {
+        // the page ranges of the attention kernels: range k starts at page lo / P + k * pps
+        const int s = (int)(row / a.Hq);
+        const int L = max(0, min(a.seq_lens[s], min(a.max_seq_len, a.max_blocks * kPage)));
+        const int n_pages = (L + kPage - 1) / kPage;
+        const int lo = (a.window > 0 && L > a.window) ? L - a.window : 0;
+        n_used = min(a.n_splits, (n_pages - lo / kPage + a.pages_per_split - 1) / a.pages_per_split);
+    }
     float M = -INFINITY, den = 0.0f, num[V];
 #pragma unroll
     for (int v = 0; v < V; ++v) num[v] = 0.0f;
 #pragma unroll 4
-    for (int k = w; k < a.n_splits; k += NW) {
+    for (int k = w; k < n_used; k += NW) {
         const float* pk = pp + (int64_t)k * (D + 2);
         const float m = pk[D], l = pk[D + 1];
         float o[V];
