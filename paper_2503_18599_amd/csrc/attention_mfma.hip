@@ -853,26 +853,47 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 4 && PG
                 token_table(S, lane, T, 1.0f);
             }
             wave_sync();
-            // Lane (t + 16*grp4) holds rows 4*grp4 .. 4*grp4+3 of column t: the U (grp4
-            // even) or H (grp4 odd) limbs of head rs*2 + grp4/2.  Rows 1 and 3 reach rows 0
-            // and 2 by a row swap.
+            // Lane (t + 16*grp4) holds rows 4*grp4 .. 4*grp4+3 of column t of each page's
+            // tile: the U (grp4 even) or H (grp4 odd) limbs of head rs*2 + grp4/2.
             const int t = lane & 15, grp4 = lane >> 4;
-            const bool hi = (grp4 >> 1) != 0;
+            if constexpr (G == 1) {
+                // rows 8-15 are zero (no second head): two 16-lane swaps and two 32-lane swaps
+                // give lane group p the U and H sums of page p (its lane is its token), so
+                // every lane forms one score
+                static_assert(GRP == 4, "four pages, one per lane group");
+                float v[GRP];
 #pragma unroll
-            for (int pg = 0; pg < GRP; ++pg) {
-                const float4 tc = S.tokc()[pg * P + t];
-                const bool valid = t < gc.nval[pg] && (g0 + pg) * P + t >= lo;
+                for (int pg = 0; pg < GRP; ++pg) v[pg] = limbs(acc[pg][0]);
+                const auto s01 = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(int, v[0]),
+                                                                  __builtin_bit_cast(int, v[1]), false, false);
+                const auto s23 = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(int, v[2]),
+                                                                  __builtin_bit_cast(int, v[3]), false, false);
+                const float u = __builtin_bit_cast(float, (int)__builtin_amdgcn_permlane32_swap(s01[0], s23[0], false, false)[0]);
+                const float o = __builtin_bit_cast(float, (int)__builtin_amdgcn_permlane32_swap(s01[1], s23[1], false, false)[0]);
+                const float4 tc = S.tokc()[lane];
+                const bool valid = t < gc.nv && (g0 + grp4) * P + t >= lo;
+                const float dot = fmaf(tc.x, ssum[0], fmaf(tc.y, u, tc.z * o) * sfix[0]);
+                if (grp4 < gc.npg) sc[tok0 + lane] = valid ? dot : -INFINITY;
+            } else {
+                // (per page: the paired form of the one-head case spills registers here)
+                // rows 1 and 3 reach rows 0 and 2 by a row swap
+                const bool hi = (grp4 >> 1) != 0;
 #pragma unroll
-                for (int rs = 0; rs < NRS; ++rs) {
-                    const float v = limbs(acc[pg][rs]);
-                    const int vb = __builtin_bit_cast(int, v);
-                    const float o = __builtin_bit_cast(float, (int)__builtin_amdgcn_permlane16_swap(vb, vb, false, false)[1]);
-                    const int hd = rs * 2 + (hi ? 1 : 0);
-                    const float s1 = hi ? ssum[min(rs * 2 + 1, G - 1)] : ssum[rs * 2];
-                    const float s2 = hi ? sfix[min(rs * 2 + 1, G - 1)] : sfix[rs * 2];
-                    const float dot = fmaf(tc.x, s1, fmaf(tc.y, v, tc.z * o) * s2);
-                    if ((grp4 & 1) == 0 && hd < G && pg < gc.npg)
-                        sc[hd * cap + tok0 + pg * P + t] = valid ? dot : -INFINITY;
+                for (int pg = 0; pg < GRP; ++pg) {
+                    const float4 tc = S.tokc()[pg * P + t];
+                    const bool valid = t < gc.nval[pg] && (g0 + pg) * P + t >= lo;
+#pragma unroll
+                    for (int rs = 0; rs < NRS; ++rs) {
+                        const float v = limbs(acc[pg][rs]);
+                        const int vb = __builtin_bit_cast(int, v);
+                        const float o = __builtin_bit_cast(float, (int)__builtin_amdgcn_permlane16_swap(vb, vb, false, false)[1]);
+                        const int hd = rs * 2 + (hi ? 1 : 0);
+                        const float s1 = hi ? ssum[min(rs * 2 + 1, G - 1)] : ssum[rs * 2];
+                        const float s2 = hi ? sfix[min(rs * 2 + 1, G - 1)] : sfix[rs * 2];
+                        const float dot = fmaf(tc.x, s1, fmaf(tc.y, v, tc.z * o) * s2);
+                        if ((grp4 & 1) == 0 && hd < G && pg < gc.npg)
+                            sc[hd * cap + tok0 + pg * P + t] = valid ? dot : -INFINITY;
+                    }
                 }
             }
         }
