@@ -491,17 +491,16 @@ __device__ __forceinline__ uint2 q_heads(const Smem<G>& S, uint32_t qa) {
 }
 
 // Scores: each entry adds q_j * (true value - middle reading) to its token's score, for
-// each of the G query heads.
+// each of the G query heads; corr receives the lane's token's sums (before the scale).
 template <int G, bool PG>
-__device__ __forceinline__ void key_corrections(Smem<G>& S, const AttnArgs& a, float* sc, int cap, float scale,
-                                                const Run& r, bool staged, const Grp& gr, int tok0, int lane) {
+__device__ __forceinline__ void key_corrections(Smem<G>& S, const AttnArgs& a, const Run& r, bool staged,
+                                                const Grp& gr, int lane, float (&corr)[G]) {
     constexpr int QS = 1 + log2g<G>();                            // log2 of the query bytes per channel
     const int pg = lane >> 4, t = lane & 15;
     const uint32_t tbo = (uint32_t)lane * 64u;                    // the token's table row
     const uint32_t swz = (uint32_t)((lane >> 1) & 3) * 0x10101010u;
     const uint32_t qb = off_of(S, &S.q16()[0][0]);                // 256-aligned
     const uint32_t drow = off_of(S, &S.dense[pg][t * 64]);        // 64-aligned
-    float corr[G];
 #pragma unroll
     for (int hd = 0; hd < G; ++hd) corr[hd] = 0.0f;
     // one entry: query offset qo (channel << QS), dense offset byte dof (dword of the
@@ -576,11 +575,6 @@ __device__ __forceinline__ void key_corrections(Smem<G>& S, const AttnArgs& a, f
             const uint32_t ch = (b & 63u) | (kk >= r.c0 ? 64u : 0u);
             entry(ch << QS, (ch >> 3) * 4u, (ch & 7u) * 4u, ((b >> 2) & 0x30u) ^ (swz & 0xffu));
         }
-    }
-    const int nv = gr.nv;
-    if (t < nv) {
-#pragma unroll
-        for (int hd = 0; hd < G; ++hd) sc[hd * cap + tok0 + lane] += scale * corr[hd];
     }
 }
 
@@ -822,6 +816,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 4 && PG
     for (int g0 = p_begin; g0 < p_end; g0 += GRP) {
         const int tok0 = (g0 - p_begin) * P;
         const bool staged = fits_c;
+        float dot1 = 0.0f;     // one head: the lane's token's dense score
+        bool valid1 = false;
         // dense part on the matrix cores: one accumulator per page and the pages' MFMAs
         // interleaved, so that no MFMA waits on the one before it; stage the group in LDS
         {
@@ -871,9 +867,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 4 && PG
                 const float u = __builtin_bit_cast(float, (int)__builtin_amdgcn_permlane32_swap(s01[0], s23[0], false, false)[0]);
                 const float o = __builtin_bit_cast(float, (int)__builtin_amdgcn_permlane32_swap(s01[1], s23[1], false, false)[0]);
                 const float4 tc = S.tokc()[lane];
-                const bool valid = t < gc.nv && (g0 + grp4) * P + t >= lo;
-                const float dot = fmaf(tc.x, ssum[0], fmaf(tc.y, u, tc.z * o) * sfix[0]);
-                if (grp4 < gc.npg) sc[tok0 + lane] = valid ? dot : -INFINITY;
+                // (the score is stored once, after the correction walk has added to it)
+                valid1 = t < gc.nv && (g0 + grp4) * P + t >= lo;
+                dot1 = fmaf(tc.x, ssum[0], fmaf(tc.y, u, tc.z * o) * sfix[0]);
             } else {
                 // (per page: the paired form of the one-head case spills registers here)
                 // rows 1 and 3 reach rows 0 and 2 by a row swap
@@ -924,7 +920,16 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 4 && PG
         }
         wave_sync();
         // sparse part
-        key_corrections<G, PG>(S, a, sc, cap, a.scale, unpack_run(run_c), staged, gc, tok0, lane);
+        {
+            float corr[G];
+            key_corrections<G, PG>(S, a, unpack_run(run_c), staged, gc, lane, corr);
+            if constexpr (G == 1) {
+                if ((lane >> 4) < gc.npg) sc[tok0 + lane] = valid1 ? dot1 + a.scale * corr[0] : -INFINITY;
+            } else if ((lane & 15) < gc.nv) {
+#pragma unroll
+                for (int hd = 0; hd < G; ++hd) sc[hd * cap + tok0 + lane] += a.scale * corr[hd];
+            }
+        }
         wave_sync();
         gc = gn;
         gn = gnn;
