@@ -202,7 +202,7 @@ __device__ __forceinline__ uint4 ld16(const uint8_t* p) {
 // The correction slots build LDS addresses by OR-ing entry bits into aligned bases, so
 // the first members sit at offsets that are multiples of their sizes: tab at 0 (bits
 // 10-11 select the class, bit 3 the nibble half), dense at 4096 (a page per 1024 bytes;
-// K rows of 64 bytes, V channel rows of 8 bytes), q and oci 512-aligned.
+// K rows of 64 bytes, V channel rows of 8 bytes), q 256-aligned.
 //
 // Buffers live only in the phase that needs them share storage, which keeps the wave's
 // LDS small enough for more waves per CU: the fixed-point query (qi) is read only
