@@ -476,33 +476,32 @@ __device__ inline int group_incl_scan(int x, int m) {
 // for a segment of one slot; the vector's COO offset comes from a prefix sum over its
 // own lanes and the record's counts of the earlier slots.  All lanes stay active through
 // the lane exchanges; vectors without a token only skip their loads and stores.
+// A workgroup takes (KV head, K|V) vectors of one sequence (grid x: the sequence), so the
+// sequence's row, position and block are uniform loads.
 template <int D>
 __global__ __launch_bounds__(256) void quantize_token_kernel(QuantArgs a) {
     constexpr int NC = D / 64, LPV = D / 8, VPW = 64 / LPV;
     constexpr Layout LY = make_layout(kPage, D);
     constexpr int CAP = kPage * D;
     const int lane = threadIdx.x & 63, r = lane / LPV, m = lane % LPV;
-    const int64_t v = ((int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6)) * VPW + r;
-    const int nhw = 2 * a.H;
-    const bool in_range = v < (int64_t)a.n_seqs * nhw;
-    const int s = in_range ? (int)(v / nhw) : 0, hw = in_range ? (int)(v % nhw) : 0;
+    const int s = (int)blockIdx.x;
+    const int hw_l = ((int)blockIdx.y * (int)(blockDim.x >> 6) + (int)(threadIdx.x >> 6)) * VPW + r;
+    const bool in_range = hw_l < 2 * a.H;
+    const int hw = in_range ? hw_l : 0;
     const int h = hw >> 1, which = hw & 1;
     // The loads form three dependent levels, each issued whole before its first use:
     // the sequence's row and position; its block and the input vector; what the record
     // keeps from earlier slots.
     const int row = a.cu_tokens[s], row_end = a.cu_tokens[s + 1], pos = a.start_pos[s];
-    asm volatile("" ::"v"(row), "v"(row_end), "v"(pos));   // (issued together, one wait)
     const float* th = a.thr + hw * 4;
     const float lo_o = th[0], lo_i = th[1], hi_i = th[2], hi_o = th[3];
     const int page = pos / kPage, slot = pos % kPage;
-    bool ok = in_range && row_end - row == 1 && pos >= 0 && page < a.max_blocks;
-    int blk = -1;
+    const bool seq_ok = row_end - row == 1 && pos >= 0 && page < a.max_blocks;   // (uniform)
+    const int blk = seq_ok ? a.block_table[(int64_t)s * a.max_blocks + page] : -1;
     uint4 x = make_uint4(0, 0, 0, 0);
-    if (ok) {
-        blk = a.block_table[(int64_t)s * a.max_blocks + page];
+    if (in_range && seq_ok)   // (beside the block load, not after it)
         x = *reinterpret_cast<const uint4*>((which ? a.v_new : a.k_new) + ((int64_t)row * a.H + h) * D + 8 * m);
-    }
-    ok = ok && blk >= 0 && blk < a.num_blocks;
+    const bool ok = in_range && seq_ok && blk >= 0 && blk < a.num_blocks;
     uint8_t* rec = a.pool + (((int64_t)(ok ? blk : 0) * a.H + h) * 2 + which) * a.stride;
     // COO bytes of the record's earlier slots (2 count bytes per lane cover 2 * LPV >=
     // slot * NC), and V at an odd slot: the bytes it shares with the slot before
@@ -557,15 +556,13 @@ __global__ __launch_bounds__(256) void quantize_token_kernel(QuantArgs a) {
 hipError_t launch_quantize(const QuantArgs& a, int d, int max_new_per_seq, hipStream_t st) {
     const bool pg = a.spool != nullptr;
     if (max_new_per_seq == 1 && !pg) {
-        // the decode step: one vector per d/8 lanes
-        const int64_t nvec = (int64_t)a.n_seqs * 2 * a.H;
+        // the decode step: one vector per d/8 lanes, the sequences along x
         const int per_block = 4 * (64 / (d / 8));
-        const int64_t blocks = (nvec + per_block - 1) / per_block;
-        if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+        const dim3 grid((uint32_t)a.n_seqs, (uint32_t)((2 * a.H + per_block - 1) / per_block));
         if (d == 64)
-            hipLaunchKernelGGL(quantize_token_kernel<64>, dim3((uint32_t)blocks), dim3(256), 0, st, a);
+            hipLaunchKernelGGL(quantize_token_kernel<64>, grid, dim3(256), 0, st, a);
         else if (d == 128)
-            hipLaunchKernelGGL(quantize_token_kernel<128>, dim3((uint32_t)blocks), dim3(256), 0, st, a);
+            hipLaunchKernelGGL(quantize_token_kernel<128>, grid, dim3(256), 0, st, a);
         else
             return hipErrorInvalidValue;
         return hipGetLastError();
