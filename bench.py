@@ -98,6 +98,7 @@ def layer_bench(args, w, cache, bt, lens, dev):
     from paper_2503_18599_amd.layer import PHASES, DecoderLayer
 
     n = args.layer_batch or w.n_seqs
+    steps = args.steps or 20
     H, Hq, d = w.n_kv_heads, w.n_q_heads, w.head_dim
     d_model = Hq * d
     d_ff = {5120: 13824, 4096: 14336}.get(d_model, 4 * d_model)   # Llama-2-13B / Mistral-7B MLP widths
@@ -110,13 +111,13 @@ def layer_bench(args, w, cache, bt, lens, dev):
         layer.step(x, bt_n, lens_n, max_len, workspace=ws)
     torch.cuda.synchronize()
     ev = [{p: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for p in PHASES}
-          for _ in range(args.steps)]
+          for _ in range(steps)]
     t0 = time.perf_counter()
-    for i in range(args.steps):
+    for i in range(steps):
         layer.step(x, bt_n, lens_n, max_len, events=ev[i], workspace=ws)
     torch.cuda.synchronize()
-    seq_s = (time.perf_counter() - t0) / args.steps
-    phase_ms = {p: sum(e[p][0].elapsed_time(e[p][1]) for e in ev) / args.steps for p in PHASES}
+    seq_s = (time.perf_counter() - t0) / steps
+    phase_ms = {p: sum(e[p][0].elapsed_time(e[p][1]) for e in ev) / steps for p in PHASES}
     gpu_ms = sum(phase_ms.values())
     streams = [torch.cuda.Stream(), torch.cuda.Stream()]
     halves = [n // 2, n - n // 2]
@@ -126,15 +127,15 @@ def layer_bench(args, w, cache, bt, lens, dev):
         layer.step_overlapped(x, bt_n, lens_n, max_len, streams, wss)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    for _ in range(steps):
         layer.step_overlapped(x, bt_n, lens_n, max_len, streams, wss)
     torch.cuda.synchronize()
-    ovl_s = (time.perf_counter() - t0) / args.steps
+    ovl_s = (time.perf_counter() - t0) / steps
     log(f"layer step: sequential {seq_s * 1e3:.3f} ms (phases {phase_ms}), two streams {ovl_s * 1e3:.3f} ms")
     res = {
         "metric": "decoder-layer decode step tokens/sec (quantize + attention inside a full layer)",
         "value": round(n / min(seq_s, ovl_s), 1), "unit": "tokens/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(min(seq_s, ovl_s) * 1e3, 4),
+        "steps": steps, "warmup": args.warmup, "ms_per_step": round(min(seq_s, ovl_s) * 1e3, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16+f32", "data": "synthetic",
         "config": {"workload": f"one {w.name} decoder layer (d_model {d_model}, {Hq}/{H} heads, MLP {d_ff}, "
                                f"random bf16 weights), batch {n}, context {w.ctx_min}..{w.ctx}"
