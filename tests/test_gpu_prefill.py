@@ -2,6 +2,7 @@
 attends causally over its sequence's keys up to its own position.  The reference is the
 oracle's decode attention evaluated once per query token (its sequence's block table,
 length = position + 1), over the oracle's bit-identical cache."""
+import dataclasses
 import math
 
 import numpy as np
@@ -69,6 +70,23 @@ def test_prefill_attention_matches_oracle(B, ref, cid, kw, chunk, window, paged)
     got, want = _run(B, ref, case, chunk, window, paged)
     ok, max_abs, max_rel = attention_tolerance(got, want)
     print(f"{case.w.name} chunk {chunk} window {window}: {got.shape[0]} query tokens, max_abs={max_abs:.3e}")
+    assert ok, (max_abs, max_rel)
+
+
+@pytest.mark.parametrize("hq,hkv,chunk", [
+    (16, 8, 40),    # two query heads per KV head: 80 rows per chunk, 128-row blocks
+    (32, 4, 10),    # eight: 80 rows, 128-row blocks of 16 tokens
+    (32, 4, 3),     # eight: 24 rows, 32-row blocks of 4 tokens
+    (12, 4, 5)])    # three: 15 rows, 16-row blocks of 5 tokens
+def test_prefill_other_head_ratios(B, ref, hq, hkv, chunk):
+    """Head ratios the benchmark workloads do not have, through every block width."""
+    w = dataclasses.replace(synth.scaled(synth.WORKLOADS[4], n_seqs=3, ctx=300, ctx_min=40),
+                            n_q_heads=hq, n_kv_heads=hkv)
+    case = Case(w)
+    case.calibrate_oracle(ref)
+    got, want = _run(B, ref, case, chunk)
+    ok, max_abs, max_rel = attention_tolerance(got, want)
+    print(f"{hq}/{hkv} heads chunk {chunk}: {got.shape[0]} query tokens, max_abs={max_abs:.3e}")
     assert ok, (max_abs, max_rel)
 
 
