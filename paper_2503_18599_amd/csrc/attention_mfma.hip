@@ -238,6 +238,10 @@ struct Smem {
     __device__ __half (&q16())[D][G] { return *reinterpret_cast<__half (*)[D][G]>(q_); }
     // value corrections of one group, fixed point (value pass)
     __device__ int& oci(int hd, int ch) { return reinterpret_cast<int*>(tw_)[hd * D + ch]; }
+    // (two or four heads: heads 2p and 2p + 1 of channel ch packed in one 64-bit sum)
+    __device__ unsigned long long& oci2(int hp, int ch) {
+        return reinterpret_cast<unsigned long long*>(tw_)[hp * D + ch];
+    }
     // base, Delta, Gp of the group's tokens (key pass)
     __device__ float4 (&tokc())[GT] { return *reinterpret_cast<float4 (*)[GT]>(tw_); }
     // value-pass weights of token pairs: 4 features, 4 limbs (value pass)
@@ -595,9 +599,20 @@ __device__ __forceinline__ void value_corrections(Smem<G>& S, const AttnArgs& a,
 #pragma unroll
     for (int hd = 0; hd < G; ++hd) pt[hd] = (G > 1 && t < nv) ? sc[hd * cap + tok0 + lane] : 1.0f;
     auto add = [&](uint32_t x, float delta) {
+        if constexpr (G == 1) {
+            atomicAdd(&const_cast<int&>(lds_at<int>(S, occ + x)), (int)delta);
+        } else {
+            // two heads per 64-bit add: (v1 + borrow) * 2^32 + v0 sums exactly to
+            // S1 * 2^32 + S0 while each head's sum stays within 32 bits
+            const uint32_t o8 = occ + 2 * x;
 #pragma unroll
-        for (int hd = 0; hd < G; ++hd)
-            atomicAdd(&const_cast<int&>(lds_at<int>(S, occ + x + hd * D * 4)), (int)(G == 1 ? delta : pt[hd] * delta));
+            for (int hp = 0; hp < G / 2; ++hp) {
+                const int v0 = (int)(pt[2 * hp] * delta), v1 = (int)(pt[2 * hp + 1] * delta);
+                const uint64_t pk = ((uint64_t)(uint32_t)(v1 + (v0 >> 31)) << 32) | (uint32_t)v0;
+                atomicAdd(&const_cast<unsigned long long&>(lds_at<unsigned long long>(S, o8 + hp * D * 8)),
+                          (unsigned long long)pk);
+            }
+        }
     };
     // one entry: channel offset x = 4 * channel, table slot byte ct
     auto entry = [&](uint32_t x, uint32_t ct) {
@@ -1153,10 +1168,21 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(G == 4 && PG
         value_corrections<G, PG>(S, a, sc, cap, unpack_run(run_c), staged, gc, tok0, lane);
         wave_sync();
         // fold the group's integer sums into the fp32 outputs
+        if constexpr (G == 1) {
+            ocr[0][0] += ldexpf((float)S.oci(0, lane), -fsh);
+            ocr[0][1] += ldexpf((float)S.oci(0, lane + 64), -fsh);
+        } else {
 #pragma unroll
-        for (int hd = 0; hd < G; ++hd) {
-            ocr[hd][0] += ldexpf((float)S.oci(hd, lane), -fsh);
-            ocr[hd][1] += ldexpf((float)S.oci(hd, lane + 64), -fsh);
+            for (int hp = 0; hp < G / 2; ++hp) {
+#pragma unroll
+                for (int c = 0; c < 2; ++c) {
+                    const unsigned long long T = S.oci2(hp, lane + 64 * c);
+                    const int s0 = (int)(uint32_t)T;
+                    const int s1 = (int)(uint32_t)(T >> 32) + (s0 < 0 ? 1 : 0);
+                    ocr[2 * hp][c] += ldexpf((float)s0, -fsh);
+                    ocr[2 * hp + 1][c] += ldexpf((float)s1, -fsh);
+                }
+            }
         }
         wave_sync();   // (the next group's weights replace the sums)
         gc = gn;
